@@ -1,0 +1,38 @@
+"""Build step for libwtconv.so (hipcc, gfx950), in-tree next to this file.
+
+Every HIP source is compiled with packed-FP32 instructions disabled
+(``-target-feature -packed-fp32-ops``); the kernels are written for plain
+fp32 VALU FMAs.
+"""
+import os
+import subprocess
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(HERE)
+CSRC = os.path.join(HERE, "csrc")
+INCLUDE = os.path.join(ROOT, "include")
+LIB = os.path.join(HERE, "libwtconv.so")
+SOURCES = ["wtconv_api.cpp", "wtconv_kernels.hip"]
+ARCH = os.environ.get("WTCONV_OFFLOAD_ARCH", "gfx950")
+
+
+def hipcc_flags():
+    return ["--offload-arch=" + ARCH, "-O3", "-std=c++17", "-fPIC", "-Wall",
+            "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+            "-I", INCLUDE, "-I", CSRC]
+
+
+def build(verbose: bool = False, extra=None) -> str:
+    """Compile every HIP source into libwtconv.so and return its path."""
+    hipcc = os.path.join(os.environ.get("ROCM_PATH", "/opt/rocm"), "bin", "hipcc")
+    srcs = [os.path.join(CSRC, s) for s in SOURCES]
+    cmd = [hipcc] + hipcc_flags() + list(extra or []) + ["-shared", "-x", "hip"] + srcs + ["-o", LIB + ".tmp"]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    subprocess.run(cmd, check=True)
+    os.replace(LIB + ".tmp", LIB)
+    return LIB
+
+
+if __name__ == "__main__":
+    print(build(verbose=True))

@@ -1,0 +1,435 @@
+// Host side of libwtconv: argument validation (before any HIP call), on-chip
+// layout planning and kernel launches. See include/wtconv.h for the contract.
+#include <stdint.h>
+#include <string.h>
+
+#include <algorithm>
+
+#include "wtconv_internal.h"
+
+namespace {
+
+using wtc::FusedArgs;
+using wtc::kMaxLevels;
+using wtc::LevelGeom;
+using wtc::PlaneGeom;
+
+constexpr int kLdsFloatsMax = 160 * 1024 / 4;     // one compute unit's LDS
+constexpr int kLdsFloatsShared = 64 * 1024 / 4;   // keep >= 2 workgroups per CU when possible
+constexpr int kForwardTargetWorkgroups = 4096;
+constexpr int kBackwardTargetWorkgroups = 1536;
+
+int ceil_to(int v, int m) { return (v + m - 1) / m * m; }
+int cdiv(long a, long b) { return (int)((a + b - 1) / b); }
+
+struct Plan {
+    PlaneGeom g;
+    int PP = 1;        // planes resident at once
+    int nb = 1;        // planes per workgroup
+    int nchunks = 1;   // workgroups per channel
+    int lds_floats = 0;
+};
+
+int window_floats(int T, int R)
+{
+    const int n = T + 2 * R;
+    return T == 4 ? ceil_to(n, 4) : (T == 2 ? ceil_to(n, 2) : n);
+}
+
+int round_cap(int T)
+{
+    return T == 4 ? wtc::kMaxRounds4 : (T == 2 ? wtc::kMaxRounds2 : wtc::kMaxRounds1);
+}
+
+// Tile edge for filtering an h x w level with PP resident planes: the fewest
+// register-tile rounds per wavefront, preferring larger tiles (more reuse of
+// every LDS read) when they cost at most 25% more issue slots.
+int pick_tile(int h, int w, int PP)
+{
+    int rounds[5] = {0, 0, 0, 0, 0};
+    int cost[5] = {0, 0, 0, 0, 0};
+    int best = 1 << 30;
+    for (int T : {4, 2, 1}) {
+        const long tiles = (long)PP * (ceil_to(h, T) / T) * (ceil_to(w, T) / T);
+        rounds[T] = cdiv(tiles, 64);
+        cost[T] = rounds[T] * T * T;
+        if (rounds[T] <= round_cap(T)) best = std::min(best, cost[T]);
+    }
+    if (best == (1 << 30)) return 0;
+    for (int T : {4, 2, 1})
+        if (rounds[T] <= round_cap(T) && cost[T] * 4 <= best * 5) return T;
+    return 0;
+}
+
+// Lay out one plane's input array and pyramid for a given number of resident
+// planes. Returns false if a level cannot be tiled within the register caps.
+bool layout(const wtconv_desc& d, int PP, PlaneGeom& g)
+{
+    const int R = d.k / 2;
+    memset(&g, 0, sizeof(g));
+    g.H = d.H;
+    g.W = d.W;
+    g.L = d.L;
+    g.xrows = ceil_to(d.H, 4) + 2 * R;
+    g.xpitch = ceil_to(d.W, 4) - 4 + ceil_to(4 + 2 * R, 4);
+    g.tiles_x = ceil_to(d.W, 4) / 4;
+    g.tiles_y = ceil_to(d.H, 4) / 4;
+    long off = (long)g.xrows * g.xpitch;
+    int h = d.H, w = d.W;
+    for (int l = 1; l <= d.L; ++l) {
+        h = (h + 1) / 2;
+        w = (w + 1) / 2;
+        LevelGeom& lg = g.lv[l];
+        lg.h = h;
+        lg.w = w;
+        lg.T = pick_tile(h, w, PP);
+        if (lg.T == 0) return false;
+        lg.eh = ceil_to(h, lg.T);
+        lg.ew = ceil_to(w, lg.T);
+        const int rows = R + std::max(lg.eh + R, h + 1);
+        const int pitch = std::max(lg.ew - lg.T + window_floats(lg.T, R), R + std::max(lg.ew + R, w + 1));
+        lg.pitch = ceil_to(pitch, 4);
+        lg.band = rows * lg.pitch;
+        lg.off = (int)off;
+        lg.r_w = 1.0f / (float)w;
+        lg.r_hw = 1.0f / (float)(h * w);
+        lg.r_tx = 1.0f / (float)(lg.ew / lg.T);
+        lg.r_tper = 1.0f / (float)((lg.ew / lg.T) * (lg.eh / lg.T));
+        off += 4L * lg.band;
+        if (off > (1L << 30)) return false;
+    }
+    g.plane_floats = (int)off;
+    g.r_W = 1.0f / (float)d.W;
+    g.r_tiles_x = 1.0f / (float)g.tiles_x;
+    g.r_tiles = 1.0f / (float)(g.tiles_x * g.tiles_y);
+    // flat indices decomposed with fp32 reciprocals must stay below 2^20
+    if ((long)PP * g.tiles_x * g.tiles_y * 16 >= (1L << 20)) return false;
+    return true;
+}
+
+int lds_floats_for(const wtconv_desc& d, bool bwd, int PP, const PlaneGeom& g)
+{
+    const int KK = d.k * d.k;
+    const int wt = ceil_to((1 + 4 * d.L) * KK, 4);
+    const int gc = bwd ? d.L * wtc::kWaves * 64 : 0;
+    const long planes = std::max((long)PP * (bwd ? 2 : 1) * g.plane_floats, (long)2 * wtc::kWaves * KK);
+    const long total = wt + gc + ceil_to((int)std::min(planes, 1L << 30), 4);
+    return total > (1L << 30) ? (1 << 30) : (int)total;
+}
+
+bool make_plan(const wtconv_desc& d, bool bwd, Plan& pl)
+{
+    const long px = (long)ceil_to(d.H, 4) * ceil_to(d.W, 4);
+    int want = std::max(1, cdiv(4096, px));  // aim for >= 256 output tiles per workgroup
+    want = std::min(want, d.B);
+    int PP = 0;
+    for (int pp = want; pp >= 1; --pp) {
+        PlaneGeom g;
+        if (!layout(d, pp, g)) continue;
+        const int lds = lds_floats_for(d, bwd, pp, g);
+        if (lds <= kLdsFloatsShared || (pp == 1 && lds <= kLdsFloatsMax)) {
+            PP = pp;
+            pl.g = g;
+            pl.lds_floats = lds;
+            break;
+        }
+    }
+    if (PP == 0) return false;
+    pl.PP = PP;
+    const int target = bwd ? kBackwardTargetWorkgroups : kForwardTargetWorkgroups;
+    const int chunks_target = std::max(1, cdiv(target, d.C));
+    int nb = ceil_to(cdiv(d.B, chunks_target), PP);
+    if (bwd) nb = std::max(nb, std::min(ceil_to(4, PP), ceil_to(d.B, PP)));
+    pl.nb = nb;
+    pl.nchunks = cdiv(d.B, nb);
+    return true;
+}
+
+bool overlaps(const void* a, size_t na, const void* b, size_t nb)
+{
+    if (!a || !b || na == 0 || nb == 0) return false;
+    const uintptr_t pa = (uintptr_t)a, pb = (uintptr_t)b;
+    return pa < pb + nb && pb < pa + na;
+}
+
+size_t elem_size(wtconv_dtype dt) { return dt == WTCONV_F32 ? 4 : 2; }
+
+wtconv_status check_desc(const wtconv_desc* d)
+{
+    if (!d) return WTCONV_ERR_NULL;
+    if (d->B < 1 || d->C < 1 || d->H < 1 || d->W < 1) return WTCONV_ERR_SHAPE;
+    if ((long)d->H * d->W > (1L << 30) || (long)d->B * d->C > (1L << 30) ||
+        (long)d->C * 4 * 49 > (1L << 30))
+        return WTCONV_ERR_SHAPE;
+    if (d->k != 1 && d->k != 3 && d->k != 5 && d->k != 7) return WTCONV_ERR_KSIZE;
+    if (d->L < 0 || d->L > WTCONV_MAX_LEVELS) return WTCONV_ERR_LEVELS;
+    if (d->dtype != WTCONV_F32 && d->dtype != WTCONV_BF16 && d->dtype != WTCONV_F16) return WTCONV_ERR_DTYPE;
+    return WTCONV_OK;
+}
+
+wtconv_status check_levels(int L, const float* const* lw, const float* const* ls)
+{
+    if (L == 0) return WTCONV_OK;
+    if (!lw || !ls) return WTCONV_ERR_NULL;
+    for (int l = 0; l < L; ++l)
+        if (!lw[l] || !ls[l]) return WTCONV_ERR_NULL;
+    return WTCONV_OK;
+}
+
+void fill_params(wtc::ParamPtrs& p, int L, const float* w0, const float* s0, const float* const* lw,
+                 const float* const* ls)
+{
+    memset(&p, 0, sizeof(p));
+    p.w0 = w0;
+    p.s0 = s0;
+    for (int l = 0; l < L; ++l) {
+        p.lw[l] = lw[l];
+        p.ls[l] = ls[l];
+    }
+}
+
+int vec_ok(wtconv_dtype dt, const void* a, const void* b, const void* c)
+{
+    const uintptr_t m = 15;  // 16-byte loads of the input planes
+    (void)dt;
+    return (((uintptr_t)a & m) == 0 && ((uintptr_t)b & m) == 0 && ((uintptr_t)c & m) == 0) ? 1 : 0;
+}
+
+}  // namespace
+
+extern "C" {
+
+int wtconv_version(void) { return 100; }
+
+const char* wtconv_status_string(wtconv_status s)
+{
+    switch (s) {
+        case WTCONV_OK: return "ok";
+        case WTCONV_ERR_NULL: return "a required pointer is NULL";
+        case WTCONV_ERR_SHAPE: return "invalid shape (B, C, H, W must be >= 1 and sizes must fit)";
+        case WTCONV_ERR_KSIZE: return "unsupported kernel size (k must be 1, 3, 5 or 7)";
+        case WTCONV_ERR_LEVELS: return "unsupported number of levels (0 <= L <= 8)";
+        case WTCONV_ERR_DTYPE: return "unknown dtype";
+        case WTCONV_ERR_ALIAS: return "an output overlaps an input or another output";
+        case WTCONV_ERR_WORKSPACE: return "workspace missing or too small";
+        case WTCONV_ERR_UNSUPPORTED: return "plane too large for the on-chip working set";
+        case WTCONV_ERR_HIP: return "HIP runtime error";
+    }
+    return "unknown status";
+}
+
+wtconv_status wtconv_forward(const wtconv_desc* desc, const void* x, const float* base_w,
+                             const float* base_scale, const float* const* level_w,
+                             const float* const* level_scale, void* y, hipStream_t stream)
+{
+    wtconv_status st = check_desc(desc);
+    if (st != WTCONV_OK) return st;
+    const wtconv_desc& d = *desc;
+    if (!x || !y || !base_w || !base_scale) return WTCONV_ERR_NULL;
+    if ((st = check_levels(d.L, level_w, level_scale)) != WTCONV_OK) return st;
+    const size_t bytes = (size_t)d.B * d.C * d.H * d.W * elem_size(d.dtype);
+    if (overlaps(x, bytes, y, bytes)) return WTCONV_ERR_ALIAS;
+    Plan pl;
+    if (!make_plan(d, false, pl)) return WTCONV_ERR_UNSUPPORTED;
+
+    FusedArgs a;
+    memset(&a, 0, sizeof(a));
+    a.in = x;
+    a.aux = nullptr;
+    a.out = y;
+    a.partial = nullptr;
+    fill_params(a.p, d.L, base_w, base_scale, level_w, level_scale);
+    a.B = d.B;
+    a.C = d.C;
+    a.nb = pl.nb;
+    a.PP = pl.PP;
+    a.vec_ok = vec_ok(d.dtype, x, y, x);
+    a.lds_floats = pl.lds_floats;
+    a.g = pl.g;
+    const hipError_t e = wtc::launch_forward(d.k, d.dtype, a, pl.nchunks * d.C, stream);
+    return e == hipSuccess ? WTCONV_OK : WTCONV_ERR_HIP;
+}
+
+size_t wtconv_backward_workspace_bytes(const wtconv_desc* desc)
+{
+    if (check_desc(desc) != WTCONV_OK) return 0;
+    Plan pl;
+    if (!make_plan(*desc, true, pl)) return 0;
+    const size_t n = (size_t)pl.nchunks * desc->C * wtc::partial_floats_per_channel(desc->k, desc->L);
+    return (n * sizeof(float) + 255) / 256 * 256;
+}
+
+namespace {
+
+struct Range {
+    const void* p;
+    size_t n;
+};
+
+bool any_overlap(const Range* outs, int no, const Range* ins, int ni)
+{
+    for (int i = 0; i < no; ++i) {
+        for (int j = 0; j < ni; ++j)
+            if (overlaps(outs[i].p, outs[i].n, ins[j].p, ins[j].n)) return true;
+        for (int j = i + 1; j < no; ++j)
+            if (overlaps(outs[i].p, outs[i].n, outs[j].p, outs[j].n)) return true;
+    }
+    return false;
+}
+
+int param_ranges(const wtconv_desc& d, const float* w0, const float* s0, const float* const* lw,
+                 const float* const* ls, Range* r)
+{
+    const size_t KK = (size_t)d.k * d.k;
+    int n = 0;
+    r[n++] = {w0, (size_t)d.C * KK * 4};
+    r[n++] = {s0, (size_t)d.C * 4};
+    for (int l = 0; l < d.L; ++l) {
+        r[n++] = {lw[l], (size_t)4 * d.C * KK * 4};
+        r[n++] = {ls[l], (size_t)4 * d.C * 4};
+    }
+    return n;
+}
+
+wtconv_status partials_impl(const wtconv_desc* desc, const void* x, const void* dy, const float* base_w,
+                            const float* base_scale, const float* const* level_w,
+                            const float* const* level_scale, void* dx, void* workspace, size_t workspace_bytes,
+                            hipStream_t stream, const Plan* plan_in, const Range* extra_outs, int n_extra)
+{
+    wtconv_status st = check_desc(desc);
+    if (st != WTCONV_OK) return st;
+    const wtconv_desc& d = *desc;
+    if (!x || !dy || !base_w || !base_scale) return WTCONV_ERR_NULL;
+    if ((st = check_levels(d.L, level_w, level_scale)) != WTCONV_OK) return st;
+    Plan pl;
+    if (plan_in)
+        pl = *plan_in;
+    else if (!make_plan(d, true, pl))
+        return WTCONV_ERR_UNSUPPORTED;
+    const size_t need = wtconv_backward_workspace_bytes(desc);
+    if (!workspace || workspace_bytes < need || ((uintptr_t)workspace & 15)) return WTCONV_ERR_WORKSPACE;
+
+    const size_t act = (size_t)d.B * d.C * d.H * d.W * elem_size(d.dtype);
+    Range ins[4 + 2 * kMaxLevels];
+    int ni = 0;
+    ins[ni++] = {x, act};
+    ins[ni++] = {dy, act};
+    ni += param_ranges(d, base_w, base_scale, level_w, level_scale, ins + ni);
+    Range outs[2 + 2 + 2 * kMaxLevels];
+    int no = 0;
+    outs[no++] = {dx, act};
+    outs[no++] = {workspace, need};
+    for (int i = 0; i < n_extra; ++i) outs[no++] = extra_outs[i];
+    if (any_overlap(outs, no, ins, ni)) return WTCONV_ERR_ALIAS;
+
+    FusedArgs a;
+    memset(&a, 0, sizeof(a));
+    a.in = dy;
+    a.aux = x;
+    a.out = dx;
+    a.partial = reinterpret_cast<float*>(workspace);
+    fill_params(a.p, d.L, base_w, base_scale, level_w, level_scale);
+    a.B = d.B;
+    a.C = d.C;
+    a.nb = pl.nb;
+    a.PP = pl.PP;
+    a.vec_ok = vec_ok(d.dtype, x, dy, dx ? dx : x);
+    a.lds_floats = pl.lds_floats;
+    a.g = pl.g;
+    const hipError_t e = wtc::launch_backward(d.k, d.dtype, a, pl.nchunks * d.C, stream);
+    return e == hipSuccess ? WTCONV_OK : WTCONV_ERR_HIP;
+}
+
+wtconv_status finalize_impl(const wtconv_desc* desc, const float* base_w, const float* base_scale,
+                            const float* const* level_w, const float* const* level_scale, float* d_base_w,
+                            float* d_base_scale, float* const* d_level_w, float* const* d_level_scale,
+                            const void* workspace, size_t workspace_bytes, hipStream_t stream,
+                            bool checked_alias)
+{
+    wtconv_status st = check_desc(desc);
+    if (st != WTCONV_OK) return st;
+    const wtconv_desc& d = *desc;
+    if (!base_w || !base_scale || !d_base_w || !d_base_scale) return WTCONV_ERR_NULL;
+    if ((st = check_levels(d.L, level_w, level_scale)) != WTCONV_OK) return st;
+    if ((st = check_levels(d.L, (const float* const*)d_level_w, (const float* const*)d_level_scale)) != WTCONV_OK)
+        return st;
+    Plan pl;
+    if (!make_plan(d, true, pl)) return WTCONV_ERR_UNSUPPORTED;
+    const size_t need = wtconv_backward_workspace_bytes(desc);
+    if (!workspace || workspace_bytes < need || ((uintptr_t)workspace & 15)) return WTCONV_ERR_WORKSPACE;
+    if (!checked_alias) {
+        Range ins[3 + 2 * kMaxLevels];
+        int ni = param_ranges(d, base_w, base_scale, level_w, level_scale, ins);
+        ins[ni++] = {workspace, need};
+        Range outs[2 + 2 * kMaxLevels];
+        const int no = param_ranges(d, d_base_w, d_base_scale, (const float* const*)d_level_w,
+                                    (const float* const*)d_level_scale, outs);
+        if (any_overlap(outs, no, ins, ni)) return WTCONV_ERR_ALIAS;
+    }
+    wtc::ReduceArgs r;
+    memset(&r, 0, sizeof(r));
+    r.partial = reinterpret_cast<const float*>(workspace);
+    r.nchunks = pl.nchunks;
+    r.C = d.C;
+    r.k = d.k;
+    r.L = d.L;
+    fill_params(r.p, d.L, base_w, base_scale, level_w, level_scale);
+    r.dw0 = d_base_w;
+    r.ds0 = d_base_scale;
+    for (int l = 0; l < d.L; ++l) {
+        r.dlw[l] = d_level_w[l];
+        r.dls[l] = d_level_scale[l];
+    }
+    const hipError_t e = wtc::launch_reduce(r, stream);
+    return e == hipSuccess ? WTCONV_OK : WTCONV_ERR_HIP;
+}
+
+}  // namespace
+
+wtconv_status wtconv_backward_partials(const wtconv_desc* desc, const void* x, const void* dy,
+                                       const float* base_w, const float* base_scale,
+                                       const float* const* level_w, const float* const* level_scale,
+                                       void* dx, void* workspace, size_t workspace_bytes,
+                                       hipStream_t stream)
+{
+    return partials_impl(desc, x, dy, base_w, base_scale, level_w, level_scale, dx, workspace, workspace_bytes,
+                         stream, nullptr, nullptr, 0);
+}
+
+wtconv_status wtconv_backward_finalize(const wtconv_desc* desc, const float* base_w, const float* base_scale,
+                                       const float* const* level_w, const float* const* level_scale,
+                                       float* d_base_w, float* d_base_scale, float* const* d_level_w,
+                                       float* const* d_level_scale, const void* workspace,
+                                       size_t workspace_bytes, hipStream_t stream)
+{
+    return finalize_impl(desc, base_w, base_scale, level_w, level_scale, d_base_w, d_base_scale, d_level_w,
+                         d_level_scale, workspace, workspace_bytes, stream, false);
+}
+
+wtconv_status wtconv_backward(const wtconv_desc* desc, const void* x, const void* dy,
+                              const float* base_w, const float* base_scale,
+                              const float* const* level_w, const float* const* level_scale,
+                              void* dx, float* d_base_w, float* d_base_scale,
+                              float* const* d_level_w, float* const* d_level_scale,
+                              void* workspace, size_t workspace_bytes, hipStream_t stream)
+{
+    wtconv_status st = check_desc(desc);
+    if (st != WTCONV_OK) return st;
+    const wtconv_desc& d = *desc;
+    if (!d_base_w || !d_base_scale) return WTCONV_ERR_NULL;
+    if ((st = check_levels(d.L, (const float* const*)d_level_w, (const float* const*)d_level_scale)) != WTCONV_OK)
+        return st;
+    if (!base_w || !base_scale) return WTCONV_ERR_NULL;
+    if ((st = check_levels(d.L, level_w, level_scale)) != WTCONV_OK) return st;
+    // the gradient outputs join the overlap check of the fused phase
+    Range grads[2 + 2 * kMaxLevels];
+    const int ng = param_ranges(d, d_base_w, d_base_scale, (const float* const*)d_level_w,
+                                (const float* const*)d_level_scale, grads);
+    st = partials_impl(desc, x, dy, base_w, base_scale, level_w, level_scale, dx, workspace, workspace_bytes,
+                       stream, nullptr, grads, ng);
+    if (st != WTCONV_OK) return st;
+    return finalize_impl(desc, base_w, base_scale, level_w, level_scale, d_base_w, d_base_scale, d_level_w,
+                         d_level_scale, workspace, workspace_bytes, stream, true);
+}
+
+}  // extern "C"

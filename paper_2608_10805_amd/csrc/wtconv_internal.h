@@ -1,0 +1,91 @@
+// Internal interface between the host dispatcher (wtconv_api.cpp) and the
+// gfx950 kernels (wtconv_kernels.hip). Not part of the public ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include "wtconv.h"
+
+namespace wtc {
+
+constexpr int kMaxLevels = WTCONV_MAX_LEVELS;
+constexpr int kThreads = 256;  // 4 wavefronts of 64 lanes per workgroup
+constexpr int kWaves = kThreads / 64;
+
+// Caps on how many tiles of one subband a lane may hold in registers while a
+// level is filtered in place (the filtered coefficients overwrite the
+// unfiltered ones only after every read of the level is done).
+constexpr int kMaxRounds4 = 4;   // 4x4-site tiles
+constexpr int kMaxRounds2 = 8;   // 2x2-site tiles
+constexpr int kMaxRounds1 = 16;  // single sites
+
+// On-chip layout of one level of the Haar pyramid of one plane: four
+// band-planar arrays, each with a zero halo of R sites on every side.
+// Site (j, i) of band q lives at off + q * band + (j + R) * pitch + (i + R).
+struct LevelGeom {
+    int h, w;    // grid size ceil(H / 2^l) x ceil(W / 2^l)
+    int T;       // edge of the site tiles used to filter this level (1, 2, 4)
+    int eh, ew;  // tile-aligned extents (multiples of T)
+    int pitch;   // floats per row, multiple of 4
+    int band;    // floats per band, multiple of 4
+    int off;     // float offset of band 0 within the plane's region
+    // fp32 reciprocals of the divisors used to decompose flat indices
+    float r_w;     // 1 / w
+    float r_hw;    // 1 / (h * w)
+    float r_tx;    // 1 / (ew / T), tiles per row
+    float r_tper;  // 1 / ((ew / T) * (eh / T)), tiles per plane
+};
+
+// On-chip layout of one plane: the zero-haloed input plane (pixel (y, x) at
+// (y + R) * xpitch + (x + R)) followed by the L levels.
+struct PlaneGeom {
+    int H, W, L;
+    int xpitch, xrows;
+    int tiles_x, tiles_y;  // 4x4-pixel output tiles per row / column
+    LevelGeom lv[kMaxLevels + 1];  // entries 1..L are used
+    int plane_floats;              // size of one plane's region (multiple of 4)
+    float r_W;                     // 1 / W
+    float r_tiles_x;               // 1 / tiles_x
+    float r_tiles;                 // 1 / (tiles_x * tiles_y)
+};
+
+struct ParamPtrs {
+    const float* w0;  // [C][k][k]
+    const float* s0;  // [C]
+    const float* lw[kMaxLevels];  // [4C][k][k] per level
+    const float* ls[kMaxLevels];  // [4C] per level
+};
+
+struct FusedArgs {
+    const void* in;      // forward: x; backward: dy
+    const void* aux;     // backward: x (correlation partner of dy); forward: unused
+    void* out;           // forward: y; backward: dx (may be null)
+    float* partial;      // backward: [nchunks][C][NP] kernel-gradient partials
+    ParamPtrs p;
+    int B, C;
+    int nb;              // planes of one channel handled by one workgroup
+    int PP;              // planes resident on chip at once
+    int vec_ok;          // 1 if plane bases allow 16-byte (f32) / 8-byte (16-bit) vector access
+    int lds_floats;      // dynamic LDS of the workgroup, in floats
+    PlaneGeom g;
+};
+
+struct ReduceArgs {
+    const float* partial;
+    int nchunks, C, k, L;
+    ParamPtrs p;
+    float* dw0;
+    float* ds0;
+    float* dlw[kMaxLevels];
+    float* dls[kMaxLevels];
+};
+
+// Number of kernel-gradient floats per (chunk, channel): base k*k, then
+// levels 1..L x bands 0..3 x k*k.
+inline int partial_floats_per_channel(int k, int L) { return k * k * (1 + 4 * L); }
+
+hipError_t launch_forward(int k, wtconv_dtype dt, const FusedArgs& a, int grid, hipStream_t s);
+hipError_t launch_backward(int k, wtconv_dtype dt, const FusedArgs& a, int grid, hipStream_t s);
+hipError_t launch_reduce(const ReduceArgs& a, hipStream_t s);
+
+}  // namespace wtc

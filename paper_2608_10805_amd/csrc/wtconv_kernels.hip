@@ -1,0 +1,735 @@
+// Fused WTConv kernels for gfx950 (MI355X).
+//
+// One workgroup owns one channel c and a run of batch planes of that channel.
+// Per plane it:
+//   1. reads the plane from HBM once (coalesced, vectorised) into a zero-
+//      haloed fp32 LDS array;
+//   2. builds the whole Haar pyramid on chip: the butterfly of eq. (butterfly)
+//      (Section 4.1) recomputed in LDS, without the 1/2 factors (they are
+//      powers of two and are folded into the kernels, see below);
+//   3. filters every subband of every level with its depthwise k x k kernel,
+//      one band per wavefront (so each wavefront's 25 taps sit in scalar
+//      registers), writing the filtered coefficients over the unfiltered ones;
+//   4. forms each 4x4 output tile as the base convolution plus the
+//      closed-form bit-indexed synthesis of Proposition 2 (Section 4.2) and
+//      stores it to HBM once.
+// Scales are folded into the kernels (eq. fold, Section 4.3): the base kernel
+// becomes s0 * W0 and the level-l kernel s_l * W_l * 4^-l, where 4^-l absorbs
+// the 2^-l of the unnormalised analysis pyramid and the 2^-l of Proposition 2.
+// Multiplying by a power of two is exact, so only the s * W product rounds.
+//
+// The backward kernel runs the same pipeline on dy with the kernels rotated
+// by 180 degrees (the Haar transform is symmetric and self-inverse, Section
+// 2.2, so backward through synthesis is analysis and vice versa), writes dx,
+// and accumulates the kernel gradients of eq. (foldgrad): correlations of the
+// dy pyramid with the x pyramid (and of dy with x for the base path), held in
+// registers across the workgroup's planes and reduced once per workgroup in a
+// fixed order. A second small kernel sums the per-workgroup partials in a fixed
+// order and unfolds them into dW and d(scale).
+#include <stdint.h>
+
+#include "wtconv_internal.h"
+
+namespace wtc {
+namespace {
+
+#define DEV __device__ __forceinline__
+
+// ----------------------------------------------------------------------------
+// storage types
+// ----------------------------------------------------------------------------
+DEV float to_f32(float v) { return v; }
+DEV float to_f32(uint16_t v) { return __uint_as_float(((uint32_t)v) << 16); }  // bf16
+DEV float to_f32(_Float16 v) { return (float)v; }
+
+template <typename T>
+DEV T from_f32(float v);
+template <>
+DEV float from_f32<float>(float v) { return v; }
+template <>
+DEV uint16_t from_f32<uint16_t>(float v)  // bf16, round to nearest even
+{
+    uint32_t u = __float_as_uint(v);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x0040u);
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return (uint16_t)(u >> 16);
+}
+template <>
+DEV _Float16 from_f32<_Float16>(float v) { return (_Float16)v; }
+
+DEV float readlane_f(float v, int lane)
+{
+    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), lane));
+}
+
+// n / d for 0 <= n < 2^20 from rinv = fp32(1 / d): the exact quotient
+// (n + 0.5) / d lies at least 0.5 / d away from an integer, while the two
+// fp32 roundings perturb it by at most about (n / d) * 2^-23, far less.
+DEV int fdiv(int n, float rinv) { return (int)(((float)n + 0.5f) * rinv); }
+
+constexpr int ceil4c(int v) { return (v + 3) / 4 * 4; }
+constexpr int ceil2c(int v) { return (v + 1) / 2 * 2; }
+
+// Width (floats) read per window row for a T-wide tile: whole vectors.
+template <int K, int T>
+struct Win {
+    static constexpr int R = K / 2;
+    static constexpr int N = T + 2 * R;                       // taps touched
+    static constexpr int NA = T == 4 ? ceil4c(N) : (T == 2 ? ceil2c(N) : N);  // loaded
+};
+
+// Load NA consecutive floats starting at an address aligned to the vector
+// width used for tile edge T (16 bytes for T = 4, 8 bytes for T = 2).
+template <int K, int T>
+DEV void load_row(const float* __restrict__ p, float (&row)[Win<K, T>::NA])
+{
+    constexpr int NA = Win<K, T>::NA;
+    if constexpr (T == 4) {
+#pragma unroll
+        for (int v = 0; v < NA / 4; ++v) {
+            const float4 f = reinterpret_cast<const float4*>(p)[v];
+            row[4 * v + 0] = f.x;
+            row[4 * v + 1] = f.y;
+            row[4 * v + 2] = f.z;
+            row[4 * v + 3] = f.w;
+        }
+    } else if constexpr (T == 2) {
+#pragma unroll
+        for (int v = 0; v < NA / 2; ++v) {
+            const float2 f = reinterpret_cast<const float2*>(p)[v];
+            row[2 * v + 0] = f.x;
+            row[2 * v + 1] = f.y;
+        }
+    } else {
+#pragma unroll
+        for (int v = 0; v < NA; ++v) row[v] = p[v];
+    }
+}
+
+// ----------------------------------------------------------------------------
+// 1. plane load: HBM -> zero-haloed fp32 LDS array
+// ----------------------------------------------------------------------------
+template <typename T>
+DEV void load_plane(const T* __restrict__ src, float* __restrict__ dst, int H, int W, float rW, int pitch,
+                    int R, bool vec_ok, int tid)
+{
+    const int n = H * W;
+    constexpr int V = 16 / (int)sizeof(T);  // elements per 16-byte load
+    if (vec_ok && (n % V) == 0) {
+        const uint4* s4 = reinterpret_cast<const uint4*>(src);
+        for (int e = tid; e < n / V; e += kThreads) {
+            const uint4 raw = s4[e];
+            T vals[V];
+            __builtin_memcpy(vals, &raw, 16);
+            const int first = e * V;
+            int y = fdiv(first, rW);
+            int x = first - y * W;
+#pragma unroll
+            for (int v = 0; v < V; ++v) {
+                dst[(y + R) * pitch + x + R] = to_f32(vals[v]);
+                if (++x == W) {
+                    x = 0;
+                    ++y;
+                }
+            }
+        }
+    } else {
+        for (int e = tid; e < n; e += kThreads) {
+            const int y = fdiv(e, rW), x = e - y * W;
+            dst[(y + R) * pitch + x + R] = to_f32(src[e]);
+        }
+    }
+}
+
+// ----------------------------------------------------------------------------
+// 2. one analysis level, all resident planes: unnormalised butterfly
+//    (LL, LH, HL, HH) = (a+b+c+d, a+b-c-d, a-b+c-d, a-b-c+d), eq. (butterfly)
+//    without the 1/2. Zero extension comes from the zero halo / ragged rows.
+// ----------------------------------------------------------------------------
+DEV void analysis_level(const float* __restrict__ src, int sp, float* __restrict__ dst, const LevelGeom& lg,
+                        int R, int np, int stride, int tid)
+{
+    const int per = lg.h * lg.w;
+    for (int e = tid; e < np * per; e += kThreads) {
+        const int p = fdiv(e, lg.r_hw);
+        const int r = e - p * per;
+        const int j = fdiv(r, lg.r_w);
+        const int i = r - j * lg.w;
+        const float* s = src + p * stride + (2 * j + R) * sp + 2 * i + R;
+        const float a = s[0], b = s[1], c = s[sp], d = s[sp + 1];
+        const float ab = a + b, cd = c + d, amb = a - b, cmd = c - d;
+        float* o = dst + p * stride + (j + R) * lg.pitch + i + R;
+        o[0] = ab + cd;
+        o[lg.band] = ab - cd;
+        o[2 * lg.band] = amb + cmd;
+        o[3 * lg.band] = amb - cmd;
+    }
+}
+
+// ----------------------------------------------------------------------------
+// depthwise "same" correlation of a T x T tile of sites (or pixels):
+//   out[oy][ox] = sum_{p,t} w[p][t] * src[j0+oy+p-R][i0+ox+t-R]
+// `band` points at the array origin (the top-left halo element).
+// ----------------------------------------------------------------------------
+template <int K, int T>
+DEV void conv_tile(const float* __restrict__ band, int pitch, int j0, int i0, const float (&w)[K * K],
+                   float (&out)[T][T])
+{
+    constexpr int N = Win<K, T>::N;
+#pragma unroll
+    for (int oy = 0; oy < T; ++oy)
+#pragma unroll
+        for (int ox = 0; ox < T; ++ox) out[oy][ox] = 0.f;
+#pragma unroll
+    for (int r = 0; r < N; ++r) {
+        float row[Win<K, T>::NA];
+        load_row<K, T>(band + (j0 + r) * pitch + i0, row);
+#pragma unroll
+        for (int oy = 0; oy < T; ++oy) {
+            const int p = r - oy;
+            if (p < 0 || p >= K) continue;
+#pragma unroll
+            for (int ox = 0; ox < T; ++ox)
+#pragma unroll
+                for (int t = 0; t < K; ++t) out[oy][ox] = __builtin_fmaf(w[p * K + t], row[ox + t], out[oy][ox]);
+        }
+    }
+}
+
+// Kernel-gradient correlation of one tile:
+//   acc[p][t] += sum_{oy,ox} ctr[oy][ox] * src[j0+oy+p-R][i0+ox+t-R]
+template <int K, int T>
+DEV void corr_tile(const float* __restrict__ band, int pitch, int j0, int i0, const float (&ctr)[T][T],
+                   float (&acc)[K * K])
+{
+    constexpr int N = Win<K, T>::N;
+#pragma unroll
+    for (int r = 0; r < N; ++r) {
+        float row[Win<K, T>::NA];
+        load_row<K, T>(band + (j0 + r) * pitch + i0, row);
+#pragma unroll
+        for (int oy = 0; oy < T; ++oy) {
+            const int p = r - oy;
+            if (p < 0 || p >= K) continue;
+#pragma unroll
+            for (int ox = 0; ox < T; ++ox)
+#pragma unroll
+                for (int t = 0; t < K; ++t) acc[p * K + t] = __builtin_fmaf(ctr[oy][ox], row[ox + t], acc[p * K + t]);
+        }
+    }
+}
+
+template <int K, int T>
+DEV void load_center(const float* __restrict__ band, int pitch, int j0, int i0, float (&ctr)[T][T])
+{
+    constexpr int R = K / 2;
+#pragma unroll
+    for (int oy = 0; oy < T; ++oy)
+#pragma unroll
+        for (int ox = 0; ox < T; ++ox) ctr[oy][ox] = band[(j0 + oy + R) * pitch + i0 + ox + R];
+}
+
+// Decompose a flat tile index over (plane, tile row, tile column).
+struct TileIdx {
+    int p, j0, i0;
+};
+DEV TileIdx tile_at(int it, int per, float rper, int tx, float rtx, int T)
+{
+    TileIdx ti;
+    ti.p = fdiv(it, rper);
+    const int r = it - ti.p * per;
+    const int jt = fdiv(r, rtx);
+    ti.j0 = jt * T;
+    ti.i0 = (r - jt * tx) * T;
+    return ti;
+}
+
+// ----------------------------------------------------------------------------
+// 3. filter one subband of one level in place, for all resident planes.
+//    Every lane computes all of its tiles into registers first; only then are
+//    the filtered values written over the unfiltered ones (one band is read
+//    and written by one wavefront only, and a wavefront's LDS operations
+//    complete in program order). Ragged sites outside the true grid are not
+//    written, so they stay zero for the next plane.
+// ----------------------------------------------------------------------------
+template <int K, int T, int MAXR>
+DEV void filter_band_inplace(float* __restrict__ region0, int stride, const LevelGeom& lg, int q, int np,
+                             const float (&w)[K * K], int lane)
+{
+    constexpr int R = K / 2;
+    const int tx = lg.ew / T;
+    const int per = tx * (lg.eh / T);
+    const int total = np * per;
+    float res[MAXR][T][T];
+#pragma unroll
+    for (int k = 0; k < MAXR; ++k) {
+        const int it = lane + 64 * k;
+        if (it < total) {
+            const TileIdx ti = tile_at(it, per, lg.r_tper, tx, lg.r_tx, T);
+            const float* band = region0 + ti.p * stride + lg.off + q * lg.band;
+            conv_tile<K, T>(band, lg.pitch, ti.j0, ti.i0, w, res[k]);
+        }
+    }
+#pragma unroll
+    for (int k = 0; k < MAXR; ++k) {
+        const int it = lane + 64 * k;
+        if (it < total) {
+            const TileIdx ti = tile_at(it, per, lg.r_tper, tx, lg.r_tx, T);
+            float* band = region0 + ti.p * stride + lg.off + q * lg.band;
+#pragma unroll
+            for (int oy = 0; oy < T; ++oy)
+#pragma unroll
+                for (int ox = 0; ox < T; ++ox) {
+                    const int j = ti.j0 + oy, i = ti.i0 + ox;
+                    if (j < lg.h && i < lg.w) band[(j + R) * lg.pitch + i + R] = res[k][oy][ox];
+                }
+        }
+    }
+}
+
+template <int K>
+DEV void filter_band(float* region0, int stride, const LevelGeom& lg, int q, int np, const float (&w)[K * K],
+                     int lane)
+{
+    if (lg.T == 4)
+        filter_band_inplace<K, 4, kMaxRounds4>(region0, stride, lg, q, np, w, lane);
+    else if (lg.T == 2)
+        filter_band_inplace<K, 2, kMaxRounds2>(region0, stride, lg, q, np, w, lane);
+    else
+        filter_band_inplace<K, 1, kMaxRounds1>(region0, stride, lg, q, np, w, lane);
+}
+
+// Kernel-gradient correlation of one subband over all resident planes with
+// tiles: acc += sum over sites of dZ(site) * Y(site + tap offset).
+template <int K, int T>
+DEV void corr_band_tiles(const float* __restrict__ dz0, const float* __restrict__ y0, int stride,
+                         const LevelGeom& lg, int q, int np, float (&acc)[K * K], int lane)
+{
+    const int tx = lg.ew / T;
+    const int per = tx * (lg.eh / T);
+    const int total = np * per;
+    for (int it = lane; it < total; it += 64) {
+        const TileIdx ti = tile_at(it, per, lg.r_tper, tx, lg.r_tx, T);
+        const int boff = ti.p * stride + lg.off + q * lg.band;
+        float ctr[T][T];
+        load_center<K, T>(dz0 + boff, lg.pitch, ti.j0, ti.i0, ctr);
+        corr_tile<K, T>(y0 + boff, lg.pitch, ti.j0, ti.i0, ctr, acc);
+    }
+}
+
+template <int K>
+DEV void corr_band(const float* dz0, const float* y0, int stride, const LevelGeom& lg, int q, int np,
+                   float (&acc)[K * K], int lane)
+{
+    if (lg.T == 4)
+        corr_band_tiles<K, 4>(dz0, y0, stride, lg, q, np, acc, lane);
+    else if (lg.T == 2)
+        corr_band_tiles<K, 2>(dz0, y0, stride, lg, q, np, acc, lane);
+    else
+        corr_band_tiles<K, 1>(dz0, y0, stride, lg, q, np, acc, lane);
+}
+
+// Kernel-gradient correlation of one small (coarse) subband, one tap per lane:
+// lane (half hf, tap tt) sums dZ(site) * Y(site + offset(tt)) over the rows of
+// its half. Returns the lane's running sum (kept in LDS between planes).
+template <int K>
+DEV float corr_band_taps(const float* __restrict__ dz0, const float* __restrict__ y0, int stride,
+                         const LevelGeom& lg, int q, int np, float acc, int lane)
+{
+    constexpr int R = K / 2, KK = K * K;
+    constexpr bool two = KK <= 32;
+    const int hf = two ? (lane >> 5) : 0;
+    const int tt = two ? (lane & 31) : lane;
+    const bool active = tt < KK;
+    const int tp = active ? tt / K : R, tq = active ? tt - (tt / K) * K : R;
+    const int off = (tp - R) * lg.pitch + (tq - R);
+    for (int p = 0; p < np; ++p) {
+        const int boff = p * stride + lg.off + q * lg.band;
+        const float* dz = dz0 + boff;
+        const float* yy = y0 + boff + off;
+        for (int j = hf; j < lg.h; j += (two ? 2 : 1)) {
+            const int rowo = (j + R) * lg.pitch + R;
+            for (int i = 0; i < lg.w; ++i) acc = __builtin_fmaf(dz[rowo + i], yy[rowo + i], acc);
+        }
+    }
+    return active ? acc : 0.f;
+}
+
+// ----------------------------------------------------------------------------
+// 4. one 4x4 output tile: base correlation + closed-form synthesis
+// ----------------------------------------------------------------------------
+// Base correlation of the 4x4 tile at (y0, x0); also returns the tile's own
+// input values (the window centre), which the backward pass correlates with x.
+template <int K>
+DEV void base_tile(const float* __restrict__ xa, int xpitch, int y0, int x0, const float (&w)[K * K],
+                   float (&acc)[4][4], float (&ctr)[4][4])
+{
+    constexpr int R = K / 2, N = Win<K, 4>::N;
+#pragma unroll
+    for (int oy = 0; oy < 4; ++oy)
+#pragma unroll
+        for (int ox = 0; ox < 4; ++ox) acc[oy][ox] = 0.f;
+#pragma unroll
+    for (int r = 0; r < N; ++r) {
+        float row[Win<K, 4>::NA];
+        load_row<K, 4>(xa + (y0 + r) * xpitch + x0, row);
+        if (r >= R && r < R + 4) {
+#pragma unroll
+            for (int ox = 0; ox < 4; ++ox) ctr[r - R][ox] = row[R + ox];
+        }
+#pragma unroll
+        for (int oy = 0; oy < 4; ++oy) {
+            const int p = r - oy;
+            if (p < 0 || p >= K) continue;
+#pragma unroll
+            for (int ox = 0; ox < 4; ++ox)
+#pragma unroll
+                for (int t = 0; t < K; ++t) acc[oy][ox] = __builtin_fmaf(w[p * K + t], row[ox + t], acc[oy][ox]);
+        }
+    }
+}
+
+// Proposition 2 for the 4x4 tile at (y0, x0), y0 and x0 multiples of 4, added
+// to acc. Every coefficient has its 4^-l already folded into the kernels, so
+// each level contributes LL + sy*LH + sx*HL + sy*sx*HH at (y >> l, x >> l) with
+// sy = (-1)^bit(l-1) of y, sx likewise. For l >= 3 the whole tile shares one
+// coefficient tuple and one sign pair; level 2 has one tuple and a sign pair
+// per 2x2 quadrant; level 1 has a tuple per quadrant and a sign pair per pixel.
+// Because the LL term of every level enters with sign +, the coarser levels'
+// sum for a quadrant is simply added to that quadrant's level-1 LL.
+template <int K>
+DEV void synth_tile(const float* __restrict__ reg, const PlaneGeom& g, int y0, int x0, float (&acc)[4][4])
+{
+    constexpr int R = K / 2;
+    const int L = g.L;
+    if (L < 1) return;
+    float coarse = 0.f;
+    for (int l = 3; l <= L; ++l) {
+        const LevelGeom& lg = g.lv[l];
+        const float* z = reg + lg.off + ((y0 >> l) + R) * lg.pitch + (x0 >> l) + R;
+        const float ll = z[0], lh = z[lg.band], hl = z[2 * lg.band], hh = z[3 * lg.band];
+        const bool by = (y0 >> (l - 1)) & 1, bx = (x0 >> (l - 1)) & 1;
+        const float t1 = by ? ll - lh : ll + lh;  // LL + sy LH
+        const float t2 = by ? hl - hh : hl + hh;  // HL + sy HH
+        coarse += bx ? t1 - t2 : t1 + t2;
+    }
+    float quad[2][2];
+    if (L >= 2) {
+        const LevelGeom& lg = g.lv[2];
+        const float* z = reg + lg.off + ((y0 >> 2) + R) * lg.pitch + (x0 >> 2) + R;
+        const float ll = z[0] + coarse, lh = z[lg.band], hl = z[2 * lg.band], hh = z[3 * lg.band];
+        const float u = ll + lh, v = ll - lh, s = hl + hh, d = hl - hh;
+        quad[0][0] = u + s;
+        quad[0][1] = u - s;
+        quad[1][0] = v + d;
+        quad[1][1] = v - d;
+    } else {
+        quad[0][0] = quad[0][1] = quad[1][0] = quad[1][1] = coarse;
+    }
+    const LevelGeom& lg = g.lv[1];
+#pragma unroll
+    for (int a = 0; a < 2; ++a)
+#pragma unroll
+        for (int b = 0; b < 2; ++b) {
+            const float* z = reg + lg.off + ((y0 >> 1) + a + R) * lg.pitch + (x0 >> 1) + b + R;
+            const float ll = z[0] + quad[a][b], lh = z[lg.band], hl = z[2 * lg.band], hh = z[3 * lg.band];
+            const float u = ll + lh, v = ll - lh, s = hl + hh, d = hl - hh;
+            acc[2 * a][2 * b] += u + s;
+            acc[2 * a][2 * b + 1] += u - s;
+            acc[2 * a + 1][2 * b] += v + d;
+            acc[2 * a + 1][2 * b + 1] += v - d;
+        }
+}
+
+template <typename T>
+DEV void store_tile(T* __restrict__ plane, int H, int W, int y0, int x0, const float (&v)[4][4], bool vec)
+{
+#pragma unroll
+    for (int oy = 0; oy < 4; ++oy) {
+        const int y = y0 + oy;
+        if (y >= H) break;
+        T* row = plane + (long)y * W + x0;
+        if (vec && x0 + 4 <= W) {
+            if constexpr (sizeof(T) == 4) {
+                *reinterpret_cast<float4*>(row) = make_float4(v[oy][0], v[oy][1], v[oy][2], v[oy][3]);
+            } else {
+                T h[4] = {from_f32<T>(v[oy][0]), from_f32<T>(v[oy][1]), from_f32<T>(v[oy][2]),
+                          from_f32<T>(v[oy][3])};
+                uint2 packed;
+                __builtin_memcpy(&packed, h, 8);
+                *reinterpret_cast<uint2*>(row) = packed;
+            }
+        } else {
+#pragma unroll
+            for (int ox = 0; ox < 4; ++ox)
+                if (x0 + ox < W) row[ox] = from_f32<T>(v[oy][ox]);
+        }
+    }
+}
+
+DEV float wave_sum(float v)
+{
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m, 64);
+    return v;
+}
+
+// Index of the folded-weight row for the base kernel (0) or level l band q.
+DEV int wrow(int l, int q) { return l == 0 ? 0 : 1 + (l - 1) * 4 + q; }
+
+// Fetch one folded kernel into scalar registers: lane i of `packed` holds tap
+// i; `rot` reverses the tap order (180-degree rotation, used for dx).
+template <int K>
+DEV void fetch_weights(const float* __restrict__ wtab, int row, bool rot, int lane, float (&w)[K * K])
+{
+    constexpr int KK = K * K;
+    const float packed = lane < KK ? wtab[row * KK + lane] : 0.f;
+#pragma unroll
+    for (int i = 0; i < KK; ++i) w[i] = readlane_f(packed, rot ? KK - 1 - i : i);
+}
+
+// ----------------------------------------------------------------------------
+// the fused kernel
+// ----------------------------------------------------------------------------
+template <int K, typename ST, bool BWD>
+__global__ void __launch_bounds__(kThreads) fused_kernel(const FusedArgs a)
+{
+    constexpr int R = K / 2, KK = K * K;
+    extern __shared__ float4 lds4[];
+    float* lds = reinterpret_cast<float*>(lds4);
+
+    const PlaneGeom& g = a.g;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int C = a.C;
+    const int c = blockIdx.x % C;
+    const int chunk = blockIdx.x / C;
+    const int b_begin = chunk * a.nb;
+    const int b_end = min(a.B, b_begin + a.nb);
+    const int L = g.L;
+    const long HW = (long)g.H * g.W;
+
+    // LDS: [folded weights][coarse kernel-gradient sums (backward)][planes]
+    const int wt_floats = ceil4c((1 + 4 * L) * KK);
+    const int gc_floats = BWD ? L * kWaves * 64 : 0;
+    float* wtab = lds;
+    float* gco = lds + wt_floats;
+    float* planes = lds + wt_floats + gc_floats;
+    const int stride = BWD ? 2 * g.plane_floats : g.plane_floats;  // region of one plane
+    float* side_in = planes;                                       // input side (x / dy)
+    float* side_aux = planes + g.plane_floats;                     // backward: x side
+
+    for (int i = tid; i < a.lds_floats / 4; i += kThreads) lds4[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+    __syncthreads();
+
+    // eq. (fold): base s0*W0; level l band q: s_l*W_l*4^-l
+    for (int i = tid; i < KK; i += kThreads) wtab[i] = a.p.s0[c] * a.p.w0[c * KK + i];
+    for (int l = 1; l <= L; ++l) {
+        const float norm = __builtin_ldexpf(1.f, -2 * l);
+        const float* lw = a.p.lw[l - 1];
+        const float* ls = a.p.ls[l - 1];
+        for (int i = tid; i < 4 * KK; i += kThreads) {
+            const int q = i / KK, t = i - q * KK;
+            wtab[wrow(l, q) * KK + t] = ls[4 * c + q] * lw[(4 * c + q) * KK + t] * norm;
+        }
+    }
+    __syncthreads();
+
+    float g0[KK], g1[KK];  // backward: per-lane kernel-gradient sums (base, level 1 band `wave`)
+#pragma unroll
+    for (int t = 0; t < KK; ++t) g0[t] = g1[t] = 0.f;
+
+    const ST* in = reinterpret_cast<const ST*>(a.in);
+    const ST* aux = reinterpret_cast<const ST*>(a.aux);
+    ST* out = reinterpret_cast<ST*>(a.out);
+    const bool have_out = out != nullptr;
+    const bool vec_ok = a.vec_ok != 0;
+    const bool vec_store = vec_ok && (g.W % 4) == 0;
+    const int q = wave;  // the subband this wavefront filters
+
+    for (int b0 = b_begin; b0 < b_end; b0 += a.PP) {
+        const int np = min(a.PP, b_end - b0);
+
+        // 1. planes -> LDS
+        for (int p = 0; p < np; ++p) {
+            const long plane = (long)(b0 + p) * C + c;
+            load_plane<ST>(in + plane * HW, side_in + p * stride, g.H, g.W, g.r_W, g.xpitch, R, vec_ok, tid);
+            if constexpr (BWD)
+                load_plane<ST>(aux + plane * HW, side_aux + p * stride, g.H, g.W, g.r_W, g.xpitch, R, vec_ok,
+                               tid);
+        }
+        __syncthreads();
+
+        // 2. Haar pyramid on chip
+        for (int l = 1; l <= L; ++l) {
+            const LevelGeom& lg = g.lv[l];
+            const int soff = l == 1 ? 0 : g.lv[l - 1].off;
+            const int sp = l == 1 ? g.xpitch : g.lv[l - 1].pitch;
+            analysis_level(side_in + soff, sp, side_in + lg.off, lg, R, np, stride, tid);
+            if constexpr (BWD) analysis_level(side_aux + soff, sp, side_aux + lg.off, lg, R, np, stride, tid);
+            __syncthreads();
+        }
+
+        // 3. subband filtering, one band per wavefront
+        for (int l = 1; l <= L; ++l) {
+            const LevelGeom& lg = g.lv[l];
+            if constexpr (BWD) {
+                // kernel gradient of level l band q: dZ_l (the dy pyramid) against Y_l(x)
+                if (l == 1) {
+                    corr_band<K>(side_in, side_aux, stride, lg, q, np, g1, lane);
+                } else {
+                    float* slot = gco + ((l - 1) * kWaves + q) * 64 + lane;
+                    *slot = corr_band_taps<K>(side_in, side_aux, stride, lg, q, np, *slot, lane);
+                }
+            }
+            if (!BWD || have_out) {
+                float w[KK];
+                fetch_weights<K>(wtab, wrow(l, q), BWD, lane, w);
+                filter_band<K>(side_in, stride, lg, q, np, w, lane);
+            }
+        }
+        __syncthreads();
+
+        // 4. output tiles
+        {
+            float w[KK];
+            fetch_weights<K>(wtab, 0, BWD, lane, w);
+            const int tx = g.tiles_x, per = g.tiles_x * g.tiles_y;
+            for (int it = tid; it < np * per; it += kThreads) {
+                const TileIdx ti = tile_at(it, per, g.r_tiles, tx, g.r_tiles_x, 4);
+                const float* reg = side_in + ti.p * stride;
+                float acc[4][4], ctr[4][4];
+                if (!BWD || have_out) {
+                    base_tile<K>(reg, g.xpitch, ti.j0, ti.i0, w, acc, ctr);
+                    synth_tile<K>(reg, g, ti.j0, ti.i0, acc);
+                    const long plane = (long)(b0 + ti.p) * C + c;
+                    store_tile<ST>(out + plane * HW, g.H, g.W, ti.j0, ti.i0, acc, vec_store);
+                } else {
+                    load_center<K, 4>(reg, g.xpitch, ti.j0, ti.i0, ctr);
+                }
+                if constexpr (BWD) corr_tile<K, 4>(side_aux + ti.p * stride, g.xpitch, ti.j0, ti.i0, ctr, g0);
+            }
+        }
+        __syncthreads();
+    }
+
+    if constexpr (BWD) {
+        // fixed-order reduction of the kernel-gradient sums of this workgroup
+        const int NP = KK * (1 + 4 * L);
+        float* red = planes;  // the plane regions are free now
+#pragma unroll
+        for (int t = 0; t < KK; ++t) {
+            const float v0 = wave_sum(g0[t]);
+            const float v1 = wave_sum(g1[t]);
+            if (lane == 0) {
+                red[wave * KK + t] = v0;
+                red[(kWaves + wave) * KK + t] = v1;
+            }
+        }
+        __syncthreads();
+        float* dst = a.partial + ((long)chunk * C + c) * NP;
+        for (int t = tid; t < KK; t += kThreads)
+            dst[t] = ((red[t] + red[KK + t]) + red[2 * KK + t]) + red[3 * KK + t];
+        if (L >= 1)
+            for (int i = tid; i < 4 * KK; i += kThreads) dst[KK + i] = red[kWaves * KK + i];
+        for (int l = 2; l <= L; ++l)
+            for (int i = tid; i < 4 * KK; i += kThreads) {
+                const int qq = i / KK, t = i - qq * KK;
+                const float* s = gco + ((l - 1) * kWaves + qq) * 64;
+                dst[KK + ((l - 1) * 4 + qq) * KK + t] = (KK <= 32) ? s[t] + s[32 + t] : s[t];
+            }
+    }
+}
+
+// Sum the per-workgroup partials over chunks in increasing order, then unfold
+// eq. (foldgrad): dW = s * G and ds = <G, W>, where G is the gradient of the
+// folded kernel s*W (the level partials carry an extra 4^l from the
+// unnormalised pyramids, removed here exactly).
+__global__ void __launch_bounds__(256) reduce_kernel(const ReduceArgs a)
+{
+    const int KK = a.k * a.k;
+    const int NP = KK * (1 + 4 * a.L);
+    const int band = blockIdx.y;  // 0 = base, else 1 + (l-1)*4 + q
+    const int c = blockIdx.x * blockDim.x + threadIdx.x;
+    if (c >= a.C) return;
+    float scale, norm;
+    const float* w;
+    float* dw;
+    float* ds;
+    if (band == 0) {
+        scale = a.p.s0[c];
+        norm = 1.f;
+        w = a.p.w0 + (long)c * KK;
+        dw = a.dw0 + (long)c * KK;
+        ds = a.ds0 + c;
+    } else {
+        const int l = (band - 1) / 4 + 1, q = (band - 1) % 4;
+        const int ch = 4 * c + q;
+        scale = a.p.ls[l - 1][ch];
+        norm = __builtin_ldexpf(1.f, -2 * l);
+        w = a.p.lw[l - 1] + (long)ch * KK;
+        dw = a.dlw[l - 1] + (long)ch * KK;
+        ds = a.dls[l - 1] + ch;
+    }
+    float dsum = 0.f;
+    for (int t = 0; t < KK; ++t) {
+        float G = 0.f;
+        for (int ch = 0; ch < a.nchunks; ++ch) G += a.partial[((long)ch * a.C + c) * NP + band * KK + t];
+        G *= norm;
+        dw[t] = scale * G;
+        dsum = __builtin_fmaf(G, w[t], dsum);
+    }
+    *ds = dsum;
+}
+
+template <int K, typename ST, bool BWD>
+hipError_t launch_one(const FusedArgs& a, int grid, hipStream_t s)
+{
+    const size_t bytes = (size_t)a.lds_floats * sizeof(float);
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&fused_kernel<K, ST, BWD>),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((fused_kernel<K, ST, BWD>), dim3(grid), dim3(kThreads), bytes, s, a);
+    return hipGetLastError();
+}
+
+template <bool BWD>
+hipError_t dispatch(int k, wtconv_dtype dt, const FusedArgs& a, int grid, hipStream_t s)
+{
+#define WTC_CASE(KV)                                                            \
+    case KV:                                                                    \
+        switch (dt) {                                                           \
+            case WTCONV_F32: return launch_one<KV, float, BWD>(a, grid, s);     \
+            case WTCONV_BF16: return launch_one<KV, uint16_t, BWD>(a, grid, s); \
+            case WTCONV_F16: return launch_one<KV, _Float16, BWD>(a, grid, s);  \
+        }                                                                       \
+        break;
+    switch (k) {
+        WTC_CASE(1)
+        WTC_CASE(3)
+        WTC_CASE(5)
+        WTC_CASE(7)
+    }
+#undef WTC_CASE
+    return hipErrorInvalidValue;
+}
+
+}  // namespace
+
+hipError_t launch_forward(int k, wtconv_dtype dt, const FusedArgs& a, int grid, hipStream_t s)
+{
+    return dispatch<false>(k, dt, a, grid, s);
+}
+
+hipError_t launch_backward(int k, wtconv_dtype dt, const FusedArgs& a, int grid, hipStream_t s)
+{
+    return dispatch<true>(k, dt, a, grid, s);
+}
+
+hipError_t launch_reduce(const ReduceArgs& a, hipStream_t s)
+{
+    const dim3 grid((a.C + 255) / 256, 1 + 4 * a.L);
+    hipLaunchKernelGGL(reduce_kernel, grid, dim3(256), 0, s, a);
+    return hipGetLastError();
+}
+
+}  // namespace wtc

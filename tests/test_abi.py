@@ -1,0 +1,130 @@
+"""Host-side tests of the C ABI: the library loads on a machine without a GPU,
+exports every entry point include/wtconv.h declares, and rejects invalid
+arguments on the host before any HIP call (no compute call is made here)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2608_10805_amd import binding
+from paper_2608_10805_amd.binding import Desc, make_desc
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "wtconv.h")
+
+FAKE = 1 << 40  # a non-null address that is never dereferenced by these tests
+
+
+def header_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(wtconv_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declares_expected_entry_points():
+    assert header_functions() == sorted(binding.EXPORTS)
+
+
+def test_library_exports_every_declared_symbol():
+    lib = binding.load()
+    for name in header_functions():
+        assert hasattr(lib, name), name
+    assert binding.wtconv_version() >= 100
+
+
+def test_status_strings():
+    for code in range(10):
+        s = binding.status_string(code)
+        assert isinstance(s, str) and s
+    assert binding.status_string(0) == "ok"
+    assert binding.status_string(99) == "unknown status"
+
+
+def fwd(desc, x=FAKE, bw=FAKE + 4096, bs=FAKE + 8192, lw=None, ls=None, y=FAKE + (1 << 36)):
+    L = desc.L if desc is not None else 0
+    lw = [FAKE + 16384 + 64 * i for i in range(L)] if lw is None else lw
+    ls = [FAKE + 32768 + 64 * i for i in range(L)] if ls is None else ls
+    lib = binding.load()
+    return lib.wtconv_forward(ctypes.byref(desc) if desc is not None else None, x, bw, bs,
+                              binding._ptr_array(lw), binding._ptr_array(ls), y, None)
+
+
+@pytest.mark.parametrize("shape,code", [
+    ((0, 1, 8, 8, 5, 1), 2), ((1, 0, 8, 8, 5, 1), 2), ((1, 1, 0, 8, 5, 1), 2), ((1, 1, 8, -3, 5, 1), 2),
+    ((1, 1, 8, 8, 4, 1), 3), ((1, 1, 8, 8, 9, 1), 3), ((1, 1, 8, 8, 0, 1), 3), ((1, 1, 8, 8, -1, 1), 3),
+    ((1, 1, 8, 8, 5, -1), 4), ((1, 1, 8, 8, 5, 9), 4),
+])
+def test_forward_rejects_bad_descriptors(shape, code):
+    assert fwd(make_desc(*shape)) == code
+
+
+def test_forward_rejects_bad_dtype():
+    assert fwd(make_desc(1, 1, 8, 8, 5, 1, dtype=7)) == 5
+
+
+def test_forward_rejects_nulls():
+    d = make_desc(2, 3, 8, 8, 5, 2)
+    assert fwd(None) == 1
+    assert fwd(d, x=None) == 1
+    assert fwd(d, y=None) == 1
+    assert fwd(d, bw=None) == 1
+    assert fwd(d, bs=None) == 1
+    lib = binding.load()
+    assert lib.wtconv_forward(ctypes.byref(d), FAKE, FAKE, FAKE, None, None, FAKE + (1 << 36), None) == 1
+    assert fwd(d, lw=[FAKE, 0]) == 1
+
+
+def test_forward_rejects_alias():
+    d = make_desc(2, 3, 8, 8, 5, 1)
+    assert fwd(d, x=FAKE, y=FAKE + 64) == 6
+    assert fwd(d, x=FAKE + 64, y=FAKE) == 6
+
+
+def test_forward_rejects_unsupported_plane():
+    # a 512 x 512 fp32 plane plus its pyramid cannot be resident in 160 KB of LDS
+    assert fwd(make_desc(1, 1, 512, 512, 5, 3)) == 8
+
+
+def bwd(desc, ws=FAKE + (1 << 38), ws_bytes=1 << 30, dx=FAKE + (1 << 37), **kw):
+    L = desc.L
+    lib = binding.load()
+    p = dict(x=FAKE, dy=FAKE + (1 << 35), bw=FAKE + (1 << 34), bs=FAKE + (1 << 34) + 65536,
+             dbw=FAKE + (1 << 39), dbs=FAKE + (1 << 39) + 65536)
+    p.update(kw)
+    lw = [FAKE + (1 << 33) + 4096 * i for i in range(L)]
+    ls = [FAKE + (1 << 33) + 65536 + 4096 * i for i in range(L)]
+    dlw = kw.get("dlw", [FAKE + (1 << 41) + (1 << 20) * i for i in range(L)])
+    dls = kw.get("dls", [FAKE + (1 << 41) + (1 << 30) + (1 << 20) * i for i in range(L)])
+    return lib.wtconv_backward(ctypes.byref(desc), p["x"], p["dy"], p["bw"], p["bs"], binding._ptr_array(lw),
+                               binding._ptr_array(ls), dx, p["dbw"], p["dbs"], binding._ptr_array(dlw),
+                               binding._ptr_array(dls), ws, ctypes.c_size_t(ws_bytes), None)
+
+
+def test_backward_workspace_query():
+    d = make_desc(64, 96, 56, 56, 5, 3)
+    n = binding.wtconv_backward_workspace_bytes(d)
+    assert n > 0 and n % 256 == 0
+    assert binding.wtconv_backward_workspace_bytes(make_desc(1, 1, 8, 8, 4, 1)) == 0
+    assert binding.load().wtconv_backward_workspace_bytes(None) == 0
+
+
+def test_backward_rejects_bad_arguments():
+    d = make_desc(4, 8, 16, 16, 5, 2)
+    need = binding.wtconv_backward_workspace_bytes(d)
+    assert bwd(make_desc(4, 8, 16, 16, 6, 2)) == 3
+    assert bwd(make_desc(4, 8, 16, 16, 5, 12)) == 4
+    assert bwd(d, x=None) == 1
+    assert bwd(d, dy=None) == 1
+    assert bwd(d, dbw=None) == 1
+    assert bwd(d, ws=None) == 7
+    assert bwd(d, ws_bytes=need - 1) == 7
+    assert bwd(d, ws=FAKE + (1 << 38) + 4) == 7  # misaligned workspace
+    assert bwd(d, dx=FAKE + 128) == 6            # dx overlaps x
+    assert bwd(d, ws=FAKE + (1 << 35)) == 6      # workspace overlaps dy
+    assert bwd(d, dbs=FAKE + (1 << 39) + 16) == 6  # two gradient outputs overlap
+    assert bwd(d, dlw=[FAKE + (1 << 41), 0]) == 1
+
+
+def test_descriptor_layout_matches_header():
+    assert ctypes.sizeof(Desc) == 7 * 4

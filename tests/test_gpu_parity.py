@@ -1,0 +1,222 @@
+"""GPU parity: the fused HIP path, called through the C ABI, against the float64
+oracle on the same seeded (and storage-rounded) inputs.
+
+Tolerances (max abs error over max abs reference, per tensor): 1e-5 for fp32,
+2e-2 for bf16 / fp16 storage (fp32 accumulation in both cases).
+"""
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+import oracle  # noqa: E402
+from tests._gpu import TOL, channel_slice, rel_err, setup, to_np  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+
+if not torch.cuda.is_available():
+    pytest.skip("needs a GPU", allow_module_level=True)
+
+
+def check_forward(B, C, H, W, k, L, dtype, seed=0):
+    inp, dev = setup(B, C, H, W, k, L, dtype, seed)
+    y = to_np(dev.forward())
+    ref = oracle.forward(inp.x, inp.base_w, inp.base_scale, inp.level_w, inp.level_scale)
+    e = rel_err(y, ref)
+    assert e < TOL[dtype], f"forward rel err {e:.3e}"
+    return e
+
+
+def check_backward(B, C, H, W, k, L, dtype, seed=0, need_dx=True):
+    inp, dev = setup(B, C, H, W, k, L, dtype, seed)
+    dx, dbw, dbs, dlw, dls = dev.backward(need_dx=need_dx)
+    ref = oracle.backward(inp.x, inp.dy, inp.base_w, inp.base_scale, inp.level_w, inp.level_scale)
+    errs = {"d_base_w": rel_err(to_np(dbw), ref["d_base_w"]),
+            "d_base_scale": rel_err(to_np(dbs), ref["d_base_scale"])}
+    if need_dx:
+        errs["dx"] = rel_err(to_np(dx), ref["dx"])
+    for l in range(L):
+        errs[f"d_level_w{l + 1}"] = rel_err(to_np(dlw[l]), ref["d_level_w"][l])
+        errs[f"d_level_scale{l + 1}"] = rel_err(to_np(dls[l]), ref["d_level_scale"][l])
+    tol = TOL[dtype]
+    bad = {k_: v for k_, v in errs.items() if not v < tol}
+    assert not bad, f"backward rel errs over {tol}: {bad}"
+    return errs
+
+
+# shapes small enough for the oracle to check every element, spanning several
+# tiles, ragged tails, odd and 1-pixel sizes, every kernel size and L = 0..8
+SMALL = [
+    (2, 16, 32, 32, 5, 1, "f32"),   # the small forward workload
+    (2, 3, 13, 11, 5, 3, "f32"),
+    (1, 2, 7, 7, 5, 5, "f32"),      # grids reaching 1 x 1
+    (2, 2, 1, 1, 3, 2, "f32"),
+    (1, 1, 1, 9, 5, 2, "f32"),
+    (3, 2, 9, 1, 3, 1, "f32"),
+    (2, 4, 28, 28, 5, 4, "f32"),
+    (1, 2, 63, 95, 5, 5, "f32"),
+    (2, 2, 56, 56, 5, 3, "f32"),
+    (2, 3, 17, 23, 1, 2, "f32"),
+    (2, 3, 17, 23, 3, 3, "f32"),
+    (2, 3, 17, 23, 7, 2, "f32"),
+    (2, 2, 20, 20, 5, 0, "f32"),
+    (1, 2, 40, 36, 5, 8, "f32"),
+    (5, 3, 14, 14, 5, 2, "f32"),    # several planes resident per workgroup
+    (9, 2, 7, 7, 3, 3, "f32"),
+    (2, 4, 28, 28, 5, 3, "bf16"),
+    (2, 3, 13, 11, 5, 2, "bf16"),
+    (2, 4, 28, 28, 5, 3, "f16"),
+    (1, 2, 63, 95, 3, 4, "f16"),
+]
+
+
+@pytest.mark.parametrize("B,C,H,W,k,L,dtype", SMALL)
+def test_forward_small(B, C, H, W, k, L, dtype):
+    check_forward(B, C, H, W, k, L, dtype)
+
+
+@pytest.mark.parametrize("B,C,H,W,k,L,dtype", SMALL)
+def test_backward_small(B, C, H, W, k, L, dtype):
+    check_backward(B, C, H, W, k, L, dtype)
+
+
+def test_backward_without_dx_matches():
+    check_backward(3, 4, 21, 19, 5, 3, "f32", need_dx=False)
+
+
+def _sample_planes(B, C, n, rng):
+    picks = {(0, 0), (B - 1, C - 1)}
+    while len(picks) < n:
+        picks.add((int(rng.integers(B)), int(rng.integers(C))))
+    return sorted(picks)
+
+
+def check_full_size(B, C, H, W, k, L, dtype, backward, n_planes=12, n_channels=3, seed=0):
+    """Full-size run in the benchmark's launch configuration; the oracle checks
+    sampled planes of y / dx and all parameter gradients of sampled channels."""
+    inp, dev = setup(B, C, H, W, k, L, dtype, seed)
+    rng = np.random.default_rng(1)
+    planes = _sample_planes(B, C, n_planes, rng)
+    tol = TOL[dtype]
+    y = dev.forward()
+    for b, c in planes:
+        wl = np.stack([w[4 * c:4 * c + 4] for w in inp.level_w]) if L else []
+        sl = np.stack([s[4 * c:4 * c + 4] for s in inp.level_scale]) if L else []
+        ref = oracle.plane_forward(inp.x[b, c], inp.base_w[c], inp.base_scale[c], wl, sl)
+        e = rel_err(to_np(y[b, c]), ref)
+        assert e < tol, f"y plane {(b, c)} rel err {e:.3e}"
+    del y
+    if not backward:
+        return
+    dx, dbw, dbs, dlw, dls = dev.backward()
+    for b, c in planes:
+        wl = np.stack([w[4 * c:4 * c + 4] for w in inp.level_w]) if L else []
+        sl = np.stack([s[4 * c:4 * c + 4] for s in inp.level_scale]) if L else []
+        ref = oracle.plane_backward(inp.x[b, c], inp.dy[b, c], inp.base_w[c], inp.base_scale[c], wl, sl)[0]
+        e = rel_err(to_np(dx[b, c]), ref)
+        assert e < tol, f"dx plane {(b, c)} rel err {e:.3e}"
+    cs = sorted({0, C - 1} | {int(v) for v in rng.integers(0, C, n_channels)})
+    xs, dys, bws, bss, lws, lss = channel_slice(inp, cs)
+    ref = oracle.backward(xs, dys, bws, bss, lws, lss)
+    idx = np.asarray(cs)
+    sub4 = lambda t: to_np(t).reshape(C, 4, *t.shape[1:])[idx].reshape(-1, *t.shape[1:])  # noqa: E731
+    errs = {"d_base_w": rel_err(to_np(dbw)[idx], ref["d_base_w"]),
+            "d_base_scale": rel_err(to_np(dbs)[idx], ref["d_base_scale"])}
+    for l in range(L):
+        errs[f"d_level_w{l + 1}"] = rel_err(sub4(dlw[l]), ref["d_level_w"][l])
+        errs[f"d_level_scale{l + 1}"] = rel_err(sub4(dls[l]), ref["d_level_scale"][l])
+    bad = {k_: v for k_, v in errs.items() if not v < tol}
+    assert not bad, f"full-size gradient rel errs over {tol}: {bad}"
+
+
+def test_convnext_stage1_forward_full():
+    """B=64 C=96 56x56, k=5, L=3, fp32 (forward workload)."""
+    check_full_size(64, 96, 56, 56, 5, 3, "f32", backward=False)
+
+
+def test_convnext_stage1_fwdbwd_full():
+    """The benchmarked fwd+bwd workload: B=64 C=96 56x56, k=5, L=3, fp32."""
+    check_full_size(64, 96, 56, 56, 5, 3, "f32", backward=True)
+
+
+@pytest.mark.parametrize("L", [1, 2, 3, 4, 5])
+def test_convnext_stage2_fwdbwd_full(L):
+    """B=64 C=192 28x28, k=5, L sweep, fp32."""
+    check_full_size(64, 192, 28, 28, 5, L, "f32", backward=True)
+
+
+def test_convnext_stage1_bf16_l5_full():
+    """B=128 C=96 56x56, k=5, L=5, bf16 storage."""
+    check_full_size(128, 96, 56, 56, 5, 5, "bf16", backward=True)
+
+
+SWEEP = [(128, 96, 56, 56), (128, 192, 28, 28), (128, 384, 14, 14), (128, 768, 7, 7), (32, 128, 63, 95)]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("L", [1, 3, 5])
+@pytest.mark.parametrize("shape", SWEEP)
+def test_sweep_fwdbwd(shape, L, dtype):
+    B, C, H, W = shape
+    check_full_size(B, C, H, W, 5, L, dtype, backward=True, n_planes=6, n_channels=2)
+
+
+def test_determinism_bitwise():
+    inp, dev = setup(8, 12, 56, 56, 5, 3, "f32", seed=3)
+    y1, y2 = dev.forward(), dev.forward()
+    assert torch.equal(y1, y2)
+    g1, g2 = dev.backward(), dev.backward()
+    for a, b in zip([g1[0], g1[1], g1[2]] + g1[3] + g1[4], [g2[0], g2[1], g2[2]] + g2[3] + g2[4]):
+        assert torch.equal(a, b)
+
+
+def test_identity_pattern_reproduces_input():
+    """Base zeroed, identity on LH/HL/HH at every level and on LL at level L only,
+    unit scales: the operator returns x (up to fp32 rounding)."""
+    B, C, H, W, k, L = 2, 3, 37, 29, 5, 4
+    inp, dev = setup(B, C, H, W, k, L, "f32")
+    dev.bw.zero_()
+    for l in range(L):
+        w = torch.zeros(4 * C, k, k, device="cuda:0")
+        for c in range(C):
+            for q in range(4):
+                if q > 0 or l == L - 1:
+                    w[4 * c + q, k // 2, k // 2] = 1.0
+        dev.lw[l].copy_(w)
+        dev.ls[l].fill_(1.0)
+    y = to_np(dev.forward())
+    assert rel_err(y, inp.x) < 1e-6
+
+
+def test_autograd_module_matches_binding():
+    from paper_2608_10805_amd.autograd import WTConv2d
+
+    torch.manual_seed(0)
+    m = WTConv2d(6, kernel_size=5, levels=3, device="cuda:0")
+    x = torch.randn(3, 6, 30, 26, device="cuda:0", requires_grad=True)
+    y = m(x)
+    g = torch.randn_like(y)
+    y.backward(g)
+    inp_x = x.detach().cpu().double().numpy()
+    bw = m.base_w.detach().cpu().double().numpy()
+    bs = m.base_scale.detach().cpu().double().numpy()
+    lw = [p.detach().cpu().double().numpy() for p in m.level_w]
+    ls = [p.detach().cpu().double().numpy() for p in m.level_scale]
+    assert rel_err(to_np(y), oracle.forward(inp_x, bw, bs, lw, ls)) < 1e-5
+    ref = oracle.backward(inp_x, g.cpu().double().numpy(), bw, bs, lw, ls)
+    assert rel_err(to_np(x.grad), ref["dx"]) < 1e-5
+    assert rel_err(to_np(m.base_w.grad), ref["d_base_w"]) < 1e-5
+    for l in range(3):
+        assert rel_err(to_np(m.level_w[l].grad), ref["d_level_w"][l]) < 1e-5
+        assert rel_err(to_np(m.level_scale[l].grad), ref["d_level_scale"][l]) < 1e-5
+
+
+def test_large_plane_reports_unsupported():
+    """Planes whose working set exceeds one compute unit's LDS are rejected with
+    WTCONV_ERR_UNSUPPORTED (no silent fallback)."""
+    from paper_2608_10805_amd.binding import WTConvError
+
+    inp, dev = setup(1, 1, 224, 224, 5, 5, "f32")
+    with pytest.raises(WTConvError) as ei:
+        dev.backward()
+    assert ei.value.status == 8
