@@ -42,6 +42,8 @@ def parse():
     ap.add_argument("--sets", type=int, default=4, help="distinct input/output buffer sets rotated over")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="target duration of the oracle timing")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration-mib", type=int, default=0,
+                    help="only run a plain device-to-device copy of this many MiB (profiler counter calibration)")
     ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "traffic_counters.json"),
                     help="measured HBM bytes of the dominant kernel (from rocprofv3 counters)")
     return ap.parse_args()
@@ -101,6 +103,14 @@ def main():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
     dev = torch.device("cuda:0")
+    if args.copy_calibration_mib:
+        n = args.copy_calibration_mib * 1024 * 1024 // 4
+        a, b = torch.ones(n, device=dev), torch.empty(n, device=dev)
+        for _ in range(3):
+            b.copy_(a)
+        torch.cuda.synchronize()
+        log(f"copy calibration: 3 copies of {args.copy_calibration_mib} MiB")
+        return
     B, C, H, W, k, L = (WORKLOAD[n] for n in ("B", "C", "H", "W", "k", "L"))
     log(f"bench: {WORKLOAD['workload']} B={B} C={C} H={H} W={W} k={k} L={L} f32, steps={args.steps} "
         f"warmup={args.warmup} sets={args.sets}")

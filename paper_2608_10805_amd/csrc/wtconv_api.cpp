@@ -24,6 +24,7 @@ int cdiv(long a, long b) { return (int)((a + b - 1) / b); }
 
 struct Plan {
     PlaneGeom g;
+    int one_round = 0;  // every level filtered in one register-tile round per lane
     int PP = 1;        // planes resident at once
     int nb = 1;        // planes per workgroup
     int nchunks = 1;   // workgroups per channel
@@ -136,6 +137,11 @@ bool make_plan(const wtconv_desc& d, bool bwd, Plan& pl)
     }
     if (PP == 0) return false;
     pl.PP = PP;
+    pl.one_round = 1;
+    for (int l = 1; l <= d.L; ++l) {
+        const LevelGeom& lg = pl.g.lv[l];
+        if ((long)PP * (lg.eh / lg.T) * (lg.ew / lg.T) > 64) pl.one_round = 0;
+    }
     const int target = bwd ? kBackwardTargetWorkgroups : kForwardTargetWorkgroups;
     const int chunks_target = std::max(1, cdiv(target, d.C));
     int nb = ceil_to(cdiv(d.B, chunks_target), PP);
@@ -245,6 +251,7 @@ wtconv_status wtconv_forward(const wtconv_desc* desc, const void* x, const float
     a.PP = pl.PP;
     a.vec_ok = vec_ok(d.dtype, x, y, x);
     a.lds_floats = pl.lds_floats;
+    a.one_round = pl.one_round;
     a.g = pl.g;
     const hipError_t e = wtc::launch_forward(d.k, d.dtype, a, pl.nchunks * d.C, stream);
     return e == hipSuccess ? WTCONV_OK : WTCONV_ERR_HIP;
@@ -335,6 +342,7 @@ wtconv_status partials_impl(const wtconv_desc* desc, const void* x, const void* 
     a.PP = pl.PP;
     a.vec_ok = vec_ok(d.dtype, x, dy, dx ? dx : x);
     a.lds_floats = pl.lds_floats;
+    a.one_round = pl.one_round;
     a.g = pl.g;
     const hipError_t e = wtc::launch_backward(d.k, d.dtype, a, pl.nchunks * d.C, stream);
     return e == hipSuccess ? WTCONV_OK : WTCONV_ERR_HIP;

@@ -67,6 +67,7 @@ struct FusedArgs {
     int PP;              // planes resident on chip at once
     int vec_ok;          // 1 if plane bases allow 16-byte (f32) / 8-byte (16-bit) vector access
     int lds_floats;      // dynamic LDS of the workgroup, in floats
+    int one_round;       // 1 if every level is filtered in a single register-tile round
     PlaneGeom g;
 };
 

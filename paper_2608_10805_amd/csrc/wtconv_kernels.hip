@@ -106,39 +106,108 @@ DEV void load_row(const float* __restrict__ p, float (&row)[Win<K, T>::NA])
     }
 }
 
-// ----------------------------------------------------------------------------
-// 1. plane load: HBM -> zero-haloed fp32 LDS array
-// ----------------------------------------------------------------------------
-template <typename T>
-DEV void load_plane(const T* __restrict__ src, float* __restrict__ dst, int H, int W, float rW, int pitch,
-                    int R, bool vec_ok, int tid)
+// Four consecutive storage elements -> fp32 (one 16-byte or 8-byte load).
+DEV void load4(const float* __restrict__ p, float (&v)[4])
 {
-    const int n = H * W;
-    constexpr int V = 16 / (int)sizeof(T);  // elements per 16-byte load
-    if (vec_ok && (n % V) == 0) {
-        const uint4* s4 = reinterpret_cast<const uint4*>(src);
-        for (int e = tid; e < n / V; e += kThreads) {
-            const uint4 raw = s4[e];
-            T vals[V];
-            __builtin_memcpy(vals, &raw, 16);
-            const int first = e * V;
-            int y = fdiv(first, rW);
-            int x = first - y * W;
+    const float4 f = *reinterpret_cast<const float4*>(p);
+    v[0] = f.x;
+    v[1] = f.y;
+    v[2] = f.z;
+    v[3] = f.w;
+}
+DEV void load4(const uint16_t* __restrict__ p, float (&v)[4])
+{
+    const uint2 u = *reinterpret_cast<const uint2*>(p);
+    v[0] = __uint_as_float(u.x << 16);
+    v[1] = __uint_as_float(u.x & 0xffff0000u);
+    v[2] = __uint_as_float(u.y << 16);
+    v[3] = __uint_as_float(u.y & 0xffff0000u);
+}
+DEV void load4(const _Float16* __restrict__ p, float (&v)[4])
+{
+    const uint2 u = *reinterpret_cast<const uint2*>(p);
+    _Float16 h[4];
+    __builtin_memcpy(h, &u, 8);
 #pragma unroll
-            for (int v = 0; v < V; ++v) {
-                dst[(y + R) * pitch + x + R] = to_f32(vals[v]);
-                if (++x == W) {
-                    x = 0;
-                    ++y;
-                }
-            }
-        }
+    for (int i = 0; i < 4; ++i) v[i] = (float)h[i];
+}
+
+// Store N consecutive floats to LDS; with PAIRS the address is 8-byte aligned
+// and pairs go out as 64-bit stores.
+template <bool PAIRS, int N>
+DEV void st_row(float* __restrict__ p, const float* v)
+{
+    if constexpr (PAIRS && N % 2 == 0) {
+#pragma unroll
+        for (int i = 0; i < N; i += 2) *reinterpret_cast<float2*>(p + i) = make_float2(v[i], v[i + 1]);
     } else {
-        for (int e = tid; e < n; e += kThreads) {
-            const int y = fdiv(e, rW), x = e - y * W;
-            dst[(y + R) * pitch + x + R] = to_f32(src[e]);
-        }
+#pragma unroll
+        for (int i = 0; i < N; ++i) p[i] = v[i];
     }
+}
+
+// Unnormalised Haar butterfly of the 2x2 patch [[a, b], [c, d]]:
+// (LL, LH, HL, HH) = (a+b+c+d, a+b-c-d, a-b+c-d, a-b-c+d), eq. (butterfly)
+// without its factor 1/2.
+DEV void butterfly(float a, float b, float c, float d, float (&o)[4])
+{
+    const float ab = a + b, cd = c + d, amb = a - b, cmd = c - d;
+    o[0] = ab + cd;
+    o[1] = ab - cd;
+    o[2] = amb + cmd;
+    o[3] = amb - cmd;
+}
+
+// ----------------------------------------------------------------------------
+// 1. one 4x4 pixel block: HBM -> LDS, plus Haar levels 1 and 2 in registers
+//    (the block holds exactly four level-1 sites and one level-2 site).
+//    Pixels outside the plane are zero (zero extension). Ragged sites beyond
+//    the level grids are written as the zeros they are.
+// ----------------------------------------------------------------------------
+template <int K, typename T>
+DEV void load_block(const T* __restrict__ src, float* __restrict__ reg, const PlaneGeom& g, int y0, int x0,
+                    bool vec)
+{
+    constexpr int R = K / 2;
+    constexpr bool PAIRS = (R % 2) == 0;  // interior origin keeps 8-byte alignment
+    const int H = g.H, W = g.W;
+    float v[4][4];
+    if (vec && y0 + 4 <= H) {  // vec implies W % 4 == 0: the 4 columns are inside
+#pragma unroll
+        for (int r = 0; r < 4; ++r) load4(src + (long)(y0 + r) * W + x0, v[r]);
+    } else {
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                const int y = y0 + r, x = x0 + c;
+                v[r][c] = (y < H && x < W) ? to_f32(src[(long)y * W + x]) : 0.f;
+            }
+    }
+#pragma unroll
+    for (int r = 0; r < 4; ++r) st_row<PAIRS, 4>(reg + (y0 + r + R) * g.xpitch + x0 + R, v[r]);
+    if (g.L < 1) return;
+    const LevelGeom& l1 = g.lv[1];
+    float c1[2][2][4];  // [a][b][band]
+#pragma unroll
+    for (int a = 0; a < 2; ++a)
+#pragma unroll
+        for (int b = 0; b < 2; ++b)
+            butterfly(v[2 * a][2 * b], v[2 * a][2 * b + 1], v[2 * a + 1][2 * b], v[2 * a + 1][2 * b + 1], c1[a][b]);
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+#pragma unroll
+        for (int a = 0; a < 2; ++a) {
+            const float pair[2] = {c1[a][0][q], c1[a][1][q]};
+            st_row<PAIRS, 2>(reg + l1.off + q * l1.band + ((y0 >> 1) + a + R) * l1.pitch + (x0 >> 1) + R, pair);
+        }
+    if (g.L < 2) return;
+    const LevelGeom& l2 = g.lv[2];
+    float c2[4];
+    butterfly(c1[0][0][0], c1[0][1][0], c1[1][0][0], c1[1][1][0], c2);
+    float* o = reg + l2.off + ((y0 >> 2) + R) * l2.pitch + (x0 >> 2) + R;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) o[q * l2.band] = c2[q];
 }
 
 // ----------------------------------------------------------------------------
@@ -156,13 +225,13 @@ DEV void analysis_level(const float* __restrict__ src, int sp, float* __restrict
         const int j = fdiv(r, lg.r_w);
         const int i = r - j * lg.w;
         const float* s = src + p * stride + (2 * j + R) * sp + 2 * i + R;
-        const float a = s[0], b = s[1], c = s[sp], d = s[sp + 1];
-        const float ab = a + b, cd = c + d, amb = a - b, cmd = c - d;
+        float co[4];
+        butterfly(s[0], s[1], s[sp], s[sp + 1], co);
         float* o = dst + p * stride + (j + R) * lg.pitch + i + R;
-        o[0] = ab + cd;
-        o[lg.band] = ab - cd;
-        o[2 * lg.band] = amb + cmd;
-        o[3 * lg.band] = amb - cmd;
+        o[0] = co[0];
+        o[lg.band] = co[1];
+        o[2 * lg.band] = co[2];
+        o[3 * lg.band] = co[3];
     }
 }
 
@@ -275,28 +344,31 @@ DEV void filter_band_inplace(float* __restrict__ region0, int stride, const Leve
         const int it = lane + 64 * k;
         if (it < total) {
             const TileIdx ti = tile_at(it, per, lg.r_tper, tx, lg.r_tx, T);
-            float* band = region0 + ti.p * stride + lg.off + q * lg.band;
+            float* band = region0 + ti.p * stride + lg.off + q * lg.band + (ti.j0 + R) * lg.pitch + ti.i0 + R;
+            if (ti.j0 + T <= lg.h && ti.i0 + T <= lg.w) {
 #pragma unroll
-            for (int oy = 0; oy < T; ++oy)
+                for (int oy = 0; oy < T; ++oy) st_row<(R % 2) == 0, T>(band + oy * lg.pitch, res[k][oy]);
+            } else {
 #pragma unroll
-                for (int ox = 0; ox < T; ++ox) {
-                    const int j = ti.j0 + oy, i = ti.i0 + ox;
-                    if (j < lg.h && i < lg.w) band[(j + R) * lg.pitch + i + R] = res[k][oy][ox];
-                }
+                for (int oy = 0; oy < T; ++oy)
+#pragma unroll
+                    for (int ox = 0; ox < T; ++ox)
+                        if (ti.j0 + oy < lg.h && ti.i0 + ox < lg.w) band[oy * lg.pitch + ox] = res[k][oy][ox];
+            }
         }
     }
 }
 
-template <int K>
+template <int K, bool ONE>
 DEV void filter_band(float* region0, int stride, const LevelGeom& lg, int q, int np, const float (&w)[K * K],
                      int lane)
 {
     if (lg.T == 4)
-        filter_band_inplace<K, 4, kMaxRounds4>(region0, stride, lg, q, np, w, lane);
+        filter_band_inplace<K, 4, ONE ? 1 : kMaxRounds4>(region0, stride, lg, q, np, w, lane);
     else if (lg.T == 2)
-        filter_band_inplace<K, 2, kMaxRounds2>(region0, stride, lg, q, np, w, lane);
+        filter_band_inplace<K, 2, ONE ? 1 : kMaxRounds2>(region0, stride, lg, q, np, w, lane);
     else
-        filter_band_inplace<K, 1, kMaxRounds1>(region0, stride, lg, q, np, w, lane);
+        filter_band_inplace<K, 1, ONE ? 1 : kMaxRounds1>(region0, stride, lg, q, np, w, lane);
 }
 
 // Kernel-gradient correlation of one subband over all resident planes with
@@ -348,8 +420,10 @@ DEV float corr_band_taps(const float* __restrict__ dz0, const float* __restrict_
         const float* dz = dz0 + boff;
         const float* yy = y0 + boff + off;
         for (int j = hf; j < lg.h; j += (two ? 2 : 1)) {
-            const int rowo = (j + R) * lg.pitch + R;
-            for (int i = 0; i < lg.w; ++i) acc = __builtin_fmaf(dz[rowo + i], yy[rowo + i], acc);
+            const float* dzr = dz + (j + R) * lg.pitch + R;
+            const float* yyr = yy + (j + R) * lg.pitch + R;
+#pragma unroll 4
+            for (int i = 0; i < lg.w; ++i) acc = __builtin_fmaf(dzr[i], yyr[i], acc);
         }
     }
     return active ? acc : 0.f;
@@ -491,7 +565,7 @@ DEV void fetch_weights(const float* __restrict__ wtab, int row, bool rot, int la
 // ----------------------------------------------------------------------------
 // the fused kernel
 // ----------------------------------------------------------------------------
-template <int K, typename ST, bool BWD>
+template <int K, typename ST, bool BWD, bool ONE>
 __global__ void __launch_bounds__(kThreads) fused_kernel(const FusedArgs a)
 {
     constexpr int R = K / 2, KK = K * K;
@@ -544,28 +618,31 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(const FusedArgs a)
     const bool have_out = out != nullptr;
     const bool vec_ok = a.vec_ok != 0;
     const bool vec_store = vec_ok && (g.W % 4) == 0;
+    const bool vec_load = vec_store;
     const int q = wave;  // the subband this wavefront filters
 
     for (int b0 = b_begin; b0 < b_end; b0 += a.PP) {
         const int np = min(a.PP, b_end - b0);
 
-        // 1. planes -> LDS
-        for (int p = 0; p < np; ++p) {
-            const long plane = (long)(b0 + p) * C + c;
-            load_plane<ST>(in + plane * HW, side_in + p * stride, g.H, g.W, g.r_W, g.xpitch, R, vec_ok, tid);
-            if constexpr (BWD)
-                load_plane<ST>(aux + plane * HW, side_aux + p * stride, g.H, g.W, g.r_W, g.xpitch, R, vec_ok,
-                               tid);
+        // 1. planes -> LDS, with Haar levels 1 and 2 formed on the way in
+        {
+            const int tx = g.tiles_x, per = g.tiles_x * g.tiles_y;
+            for (int it = tid; it < np * per; it += kThreads) {
+                const TileIdx ti = tile_at(it, per, g.r_tiles, tx, g.r_tiles_x, 4);
+                const long plane = (long)(b0 + ti.p) * C + c;
+                load_block<K, ST>(in + plane * HW, side_in + ti.p * stride, g, ti.j0, ti.i0, vec_load);
+                if constexpr (BWD)
+                    load_block<K, ST>(aux + plane * HW, side_aux + ti.p * stride, g, ti.j0, ti.i0, vec_load);
+            }
         }
         __syncthreads();
 
-        // 2. Haar pyramid on chip
-        for (int l = 1; l <= L; ++l) {
+        // 2. the remaining Haar levels on chip
+        for (int l = 3; l <= L; ++l) {
             const LevelGeom& lg = g.lv[l];
-            const int soff = l == 1 ? 0 : g.lv[l - 1].off;
-            const int sp = l == 1 ? g.xpitch : g.lv[l - 1].pitch;
-            analysis_level(side_in + soff, sp, side_in + lg.off, lg, R, np, stride, tid);
-            if constexpr (BWD) analysis_level(side_aux + soff, sp, side_aux + lg.off, lg, R, np, stride, tid);
+            const LevelGeom& lp = g.lv[l - 1];
+            analysis_level(side_in + lp.off, lp.pitch, side_in + lg.off, lg, R, np, stride, tid);
+            if constexpr (BWD) analysis_level(side_aux + lp.off, lp.pitch, side_aux + lg.off, lg, R, np, stride, tid);
             __syncthreads();
         }
 
@@ -584,7 +661,7 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(const FusedArgs a)
             if (!BWD || have_out) {
                 float w[KK];
                 fetch_weights<K>(wtab, wrow(l, q), BWD, lane, w);
-                filter_band<K>(side_in, stride, lg, q, np, w, lane);
+                filter_band<K, ONE>(side_in, stride, lg, q, np, w, lane);
             }
         }
         __syncthreads();
@@ -643,14 +720,15 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(const FusedArgs a)
 // Sum the per-workgroup partials over chunks in increasing order, then unfold
 // eq. (foldgrad): dW = s * G and ds = <G, W>, where G is the gradient of the
 // folded kernel s*W (the level partials carry an extra 4^l from the
-// unnormalised pyramids, removed here exactly).
-__global__ void __launch_bounds__(256) reduce_kernel(const ReduceArgs a)
+// unnormalised pyramids, removed here exactly). One wavefront per (channel,
+// band row); lane t owns tap t; <G, W> is a fixed-order wavefront reduction.
+__global__ void __launch_bounds__(64) reduce_kernel(const ReduceArgs a)
 {
     const int KK = a.k * a.k;
     const int NP = KK * (1 + 4 * a.L);
+    const int c = blockIdx.x;
     const int band = blockIdx.y;  // 0 = base, else 1 + (l-1)*4 + q
-    const int c = blockIdx.x * blockDim.x + threadIdx.x;
-    if (c >= a.C) return;
+    const int t = threadIdx.x;
     float scale, norm;
     const float* w;
     float* dw;
@@ -670,26 +748,35 @@ __global__ void __launch_bounds__(256) reduce_kernel(const ReduceArgs a)
         dw = a.dlw[l - 1] + (long)ch * KK;
         ds = a.dls[l - 1] + ch;
     }
-    float dsum = 0.f;
-    for (int t = 0; t < KK; ++t) {
+    float prod = 0.f;
+    if (t < KK) {
+        const float* src = a.partial + (long)c * NP + band * KK + t;
+        const long step = (long)a.C * NP;
         float G = 0.f;
-        for (int ch = 0; ch < a.nchunks; ++ch) G += a.partial[((long)ch * a.C + c) * NP + band * KK + t];
+        for (int ch = 0; ch < a.nchunks; ++ch) G += src[ch * step];
         G *= norm;
         dw[t] = scale * G;
-        dsum = __builtin_fmaf(G, w[t], dsum);
+        prod = G * w[t];
     }
-    *ds = dsum;
+    prod = wave_sum(prod);
+    if (t == 0) *ds = prod;
+}
+
+template <int K, typename ST, bool BWD, bool ONE>
+hipError_t launch_variant(const FusedArgs& a, int grid, hipStream_t s)
+{
+    const size_t bytes = (size_t)a.lds_floats * sizeof(float);
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&fused_kernel<K, ST, BWD, ONE>),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((fused_kernel<K, ST, BWD, ONE>), dim3(grid), dim3(kThreads), bytes, s, a);
+    return hipGetLastError();
 }
 
 template <int K, typename ST, bool BWD>
 hipError_t launch_one(const FusedArgs& a, int grid, hipStream_t s)
 {
-    const size_t bytes = (size_t)a.lds_floats * sizeof(float);
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&fused_kernel<K, ST, BWD>),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((fused_kernel<K, ST, BWD>), dim3(grid), dim3(kThreads), bytes, s, a);
-    return hipGetLastError();
+    return a.one_round ? launch_variant<K, ST, BWD, true>(a, grid, s) : launch_variant<K, ST, BWD, false>(a, grid, s);
 }
 
 template <bool BWD>
@@ -727,8 +814,8 @@ hipError_t launch_backward(int k, wtconv_dtype dt, const FusedArgs& a, int grid,
 
 hipError_t launch_reduce(const ReduceArgs& a, hipStream_t s)
 {
-    const dim3 grid((a.C + 255) / 256, 1 + 4 * a.L);
-    hipLaunchKernelGGL(reduce_kernel, grid, dim3(256), 0, s, a);
+    const dim3 grid(a.C, 1 + 4 * a.L);
+    hipLaunchKernelGGL(reduce_kernel, grid, dim3(64), 0, s, a);
     return hipGetLastError();
 }
 
