@@ -88,7 +88,11 @@ bool layout(const wtconv_desc& d, int PP, PlaneGeom& g)
         lg.eh = ceil_to(h, lg.T);
         lg.ew = ceil_to(w, lg.T);
         const int rows = R + std::max(lg.eh + R, h + 1);
-        const int pitch = std::max(lg.ew - lg.T + window_floats(lg.T, R), R + std::max(lg.ew + R, w + 1));
+        int pitch = std::max(lg.ew - lg.T + window_floats(lg.T, R), R + std::max(lg.ew + R, w + 1));
+        if (l >= 2) {  // whole-row chunks of the coarse kernel-gradient pass stay inside the row
+            const int cw = w <= 8 ? 8 : 16;
+            pitch = std::max(pitch, ceil_to(w, cw) - cw + ceil_to(cw + 2 * R, 4));
+        }
         lg.pitch = ceil_to(pitch, 4);
         lg.band = rows * lg.pitch;
         lg.off = (int)off;
@@ -112,8 +116,8 @@ int lds_floats_for(const wtconv_desc& d, bool bwd, int PP, const PlaneGeom& g)
 {
     const int KK = d.k * d.k;
     const int wt = ceil_to((1 + 4 * d.L) * KK, 4);
-    const int gc = bwd ? d.L * wtc::kWaves * 64 : 0;
-    const long planes = std::max((long)PP * (bwd ? 2 : 1) * g.plane_floats, (long)2 * wtc::kWaves * KK);
+    const int gc = bwd ? ceil_to(d.L * 4 * KK, 4) : 0;
+    const long planes = std::max((long)PP * (bwd ? 2 : 1) * g.plane_floats, (long)4 * wtc::kWaves * KK);
     const long total = wt + gc + ceil_to((int)std::min(planes, 1L << 30), 4);
     return total > (1L << 30) ? (1 << 30) : (int)total;
 }
@@ -137,7 +141,9 @@ bool make_plan(const wtconv_desc& d, bool bwd, Plan& pl)
     }
     if (PP == 0) return false;
     pl.PP = PP;
-    pl.one_round = 1;
+    // single-round variant: one 4x4 block / output tile per thread and one
+    // register tile per lane for every level
+    pl.one_round = (long)PP * pl.g.tiles_x * pl.g.tiles_y <= wtc::kThreads ? 1 : 0;
     for (int l = 1; l <= d.L; ++l) {
         const LevelGeom& lg = pl.g.lv[l];
         if ((long)PP * (lg.eh / lg.T) * (lg.ew / lg.T) > 64) pl.one_round = 0;

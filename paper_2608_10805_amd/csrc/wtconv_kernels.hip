@@ -35,6 +35,12 @@ namespace {
 
 #define DEV __device__ __forceinline__
 
+// Levels whose kernel gradient is accumulated in per-lane registers across a
+// workgroup's planes (two in the single-round variant, which has the register
+// room, one otherwise); deeper levels accumulate row by row in LDS.
+template <bool ONE>
+constexpr int reg_levels() { return ONE ? 2 : 1; }
+
 // ----------------------------------------------------------------------------
 // storage types
 // ----------------------------------------------------------------------------
@@ -164,14 +170,10 @@ DEV void butterfly(float a, float b, float c, float d, float (&o)[4])
 //    Pixels outside the plane are zero (zero extension). Ragged sites beyond
 //    the level grids are written as the zeros they are.
 // ----------------------------------------------------------------------------
-template <int K, typename T>
-DEV void load_block(const T* __restrict__ src, float* __restrict__ reg, const PlaneGeom& g, int y0, int x0,
-                    bool vec)
+template <typename T>
+DEV void fetch_block(const T* __restrict__ src, const PlaneGeom& g, int y0, int x0, bool vec, float (&v)[4][4])
 {
-    constexpr int R = K / 2;
-    constexpr bool PAIRS = (R % 2) == 0;  // interior origin keeps 8-byte alignment
     const int H = g.H, W = g.W;
-    float v[4][4];
     if (vec && y0 + 4 <= H) {  // vec implies W % 4 == 0: the 4 columns are inside
 #pragma unroll
         for (int r = 0; r < 4; ++r) load4(src + (long)(y0 + r) * W + x0, v[r]);
@@ -184,6 +186,13 @@ DEV void load_block(const T* __restrict__ src, float* __restrict__ reg, const Pl
                 v[r][c] = (y < H && x < W) ? to_f32(src[(long)y * W + x]) : 0.f;
             }
     }
+}
+
+template <int K>
+DEV void store_block(const float (&v)[4][4], float* __restrict__ reg, const PlaneGeom& g, int y0, int x0)
+{
+    constexpr int R = K / 2;
+    constexpr bool PAIRS = (R % 2) == 0;  // interior origin keeps 8-byte alignment
 #pragma unroll
     for (int r = 0; r < 4; ++r) st_row<PAIRS, 4>(reg + (y0 + r + R) * g.xpitch + x0 + R, v[r]);
     if (g.L < 1) return;
@@ -208,6 +217,19 @@ DEV void load_block(const T* __restrict__ src, float* __restrict__ reg, const Pl
     float* o = reg + l2.off + ((y0 >> 2) + R) * l2.pitch + (x0 >> 2) + R;
 #pragma unroll
     for (int q = 0; q < 4; ++q) o[q * l2.band] = c2[q];
+}
+
+// One 4x4 pixel block: HBM -> LDS, plus Haar levels 1 and 2 in registers (the
+// block holds exactly four level-1 sites and one level-2 site). Pixels outside
+// the plane are zero (zero extension); ragged sites beyond the level grids are
+// written as the zeros they are.
+template <int K, typename T>
+DEV void load_block(const T* __restrict__ src, float* __restrict__ reg, const PlaneGeom& g, int y0, int x0,
+                    bool vec)
+{
+    float v[4][4];
+    fetch_block<T>(src, g, y0, x0, vec, v);
+    store_block<K>(v, reg, g, y0, x0);
 }
 
 // ----------------------------------------------------------------------------
@@ -253,6 +275,36 @@ DEV void conv_tile(const float* __restrict__ band, int pitch, int j0, int i0, co
     for (int r = 0; r < N; ++r) {
         float row[Win<K, T>::NA];
         load_row<K, T>(band + (j0 + r) * pitch + i0, row);
+#pragma unroll
+        for (int oy = 0; oy < T; ++oy) {
+            const int p = r - oy;
+            if (p < 0 || p >= K) continue;
+#pragma unroll
+            for (int ox = 0; ox < T; ++ox)
+#pragma unroll
+                for (int t = 0; t < K; ++t) out[oy][ox] = __builtin_fmaf(w[p * K + t], row[ox + t], out[oy][ox]);
+        }
+    }
+}
+
+// conv_tile that also returns the tile's own input values (the window centre).
+template <int K, int T>
+DEV void conv_tile_ctr(const float* __restrict__ band, int pitch, int j0, int i0, const float (&w)[K * K],
+                       float (&out)[T][T], float (&ctr)[T][T])
+{
+    constexpr int R = K / 2, N = Win<K, T>::N;
+#pragma unroll
+    for (int oy = 0; oy < T; ++oy)
+#pragma unroll
+        for (int ox = 0; ox < T; ++ox) out[oy][ox] = 0.f;
+#pragma unroll
+    for (int r = 0; r < N; ++r) {
+        float row[Win<K, T>::NA];
+        load_row<K, T>(band + (j0 + r) * pitch + i0, row);
+        if (r >= R && r < R + T) {
+#pragma unroll
+            for (int ox = 0; ox < T; ++ox) ctr[r - R][ox] = row[R + ox];
+        }
 #pragma unroll
         for (int oy = 0; oy < T; ++oy) {
             const int p = r - oy;
@@ -321,9 +373,10 @@ DEV TileIdx tile_at(int it, int per, float rper, int tx, float rtx, int T)
 //    complete in program order). Ragged sites outside the true grid are not
 //    written, so they stay zero for the next plane.
 // ----------------------------------------------------------------------------
-template <int K, int T, int MAXR>
-DEV void filter_band_inplace(float* __restrict__ region0, int stride, const LevelGeom& lg, int q, int np,
-                             const float (&w)[K * K], int lane)
+template <int K, int T, int MAXR, bool GRAD>
+DEV void filter_band_inplace(float* __restrict__ region0, const float* __restrict__ aux0, int stride,
+                             const LevelGeom& lg, int q, int np, const float (&w)[K * K], float (&gacc)[K * K],
+                             int lane)
 {
     constexpr int R = K / 2;
     const int tx = lg.ew / T;
@@ -335,8 +388,16 @@ DEV void filter_band_inplace(float* __restrict__ region0, int stride, const Leve
         const int it = lane + 64 * k;
         if (it < total) {
             const TileIdx ti = tile_at(it, per, lg.r_tper, tx, lg.r_tx, T);
-            const float* band = region0 + ti.p * stride + lg.off + q * lg.band;
-            conv_tile<K, T>(band, lg.pitch, ti.j0, ti.i0, w, res[k]);
+            const int boff = ti.p * stride + lg.off + q * lg.band;
+            if constexpr (GRAD) {
+                // the kernel gradient of this band: the unfiltered tile (dZ)
+                // against the partner pyramid, before the tile is overwritten
+                float ctr[T][T];
+                conv_tile_ctr<K, T>(region0 + boff, lg.pitch, ti.j0, ti.i0, w, res[k], ctr);
+                corr_tile<K, T>(aux0 + boff, lg.pitch, ti.j0, ti.i0, ctr, gacc);
+            } else {
+                conv_tile<K, T>(region0 + boff, lg.pitch, ti.j0, ti.i0, w, res[k]);
+            }
         }
     }
 #pragma unroll
@@ -359,16 +420,16 @@ DEV void filter_band_inplace(float* __restrict__ region0, int stride, const Leve
     }
 }
 
-template <int K, bool ONE>
-DEV void filter_band(float* region0, int stride, const LevelGeom& lg, int q, int np, const float (&w)[K * K],
-                     int lane)
+template <int K, bool ONE, bool GRAD>
+DEV void filter_band(float* region0, const float* aux0, int stride, const LevelGeom& lg, int q, int np,
+                     const float (&w)[K * K], float (&gacc)[K * K], int lane)
 {
     if (lg.T == 4)
-        filter_band_inplace<K, 4, ONE ? 1 : kMaxRounds4>(region0, stride, lg, q, np, w, lane);
+        filter_band_inplace<K, 4, ONE ? 1 : kMaxRounds4, GRAD>(region0, aux0, stride, lg, q, np, w, gacc, lane);
     else if (lg.T == 2)
-        filter_band_inplace<K, 2, ONE ? 1 : kMaxRounds2>(region0, stride, lg, q, np, w, lane);
+        filter_band_inplace<K, 2, ONE ? 1 : kMaxRounds2, GRAD>(region0, aux0, stride, lg, q, np, w, gacc, lane);
     else
-        filter_band_inplace<K, 1, ONE ? 1 : kMaxRounds1>(region0, stride, lg, q, np, w, lane);
+        filter_band_inplace<K, 1, ONE ? 1 : kMaxRounds1, GRAD>(region0, aux0, stride, lg, q, np, w, gacc, lane);
 }
 
 // Kernel-gradient correlation of one subband over all resident planes with
@@ -401,32 +462,84 @@ DEV void corr_band(const float* dz0, const float* y0, int stride, const LevelGeo
         corr_band_tiles<K, 1>(dz0, y0, stride, lg, q, np, acc, lane);
 }
 
-// Kernel-gradient correlation of one small (coarse) subband, one tap per lane:
-// lane (half hf, tap tt) sums dZ(site) * Y(site + offset(tt)) over the rows of
-// its half. Returns the lane's running sum (kept in LDS between planes).
-template <int K>
-DEV float corr_band_taps(const float* __restrict__ dz0, const float* __restrict__ y0, int stride,
-                         const LevelGeom& lg, int q, int np, float acc, int lane)
+// Kernel-gradient correlation of one coarse subband, by rows: lane (tap row p,
+// row group rg) keeps the K sums G[p][0..K-1] for the site rows j = rg, rg+NG,
+// ... and walks each row in CW-site chunks read with 16-byte loads:
+//   G[p][t] += sum_i dZ[j][i] * Y[j+p-R][i+t-R].
+// Reads past the grid width hit zeros (ragged sites / halo), which contribute
+// nothing. The row groups are then summed with a fixed xor tree and added to
+// one LDS slot per tap, so the result does not depend on timing.
+template <int K, int CW>
+DEV void corr_row_chunk(const float* __restrict__ dzr, const float* __restrict__ yr, float (&acc)[K])
 {
-    constexpr int R = K / 2, KK = K * K;
-    constexpr bool two = KK <= 32;
-    const int hf = two ? (lane >> 5) : 0;
-    const int tt = two ? (lane & 31) : lane;
-    const bool active = tt < KK;
-    const int tp = active ? tt / K : R, tq = active ? tt - (tt / K) * K : R;
-    const int off = (tp - R) * lg.pitch + (tq - R);
-    for (int p = 0; p < np; ++p) {
-        const int boff = p * stride + lg.off + q * lg.band;
-        const float* dz = dz0 + boff;
-        const float* yy = y0 + boff + off;
-        for (int j = hf; j < lg.h; j += (two ? 2 : 1)) {
-            const float* dzr = dz + (j + R) * lg.pitch + R;
-            const float* yyr = yy + (j + R) * lg.pitch + R;
-#pragma unroll 4
-            for (int i = 0; i < lg.w; ++i) acc = __builtin_fmaf(dzr[i], yyr[i], acc);
+    constexpr int R = K / 2;
+    constexpr int ND = ceil4c(CW + R), NY = ceil4c(CW + 2 * R);
+    float d[ND], y[NY];
+#pragma unroll
+    for (int v = 0; v < ND / 4; ++v) {
+        const float4 f = reinterpret_cast<const float4*>(dzr)[v];
+        d[4 * v] = f.x, d[4 * v + 1] = f.y, d[4 * v + 2] = f.z, d[4 * v + 3] = f.w;
+    }
+#pragma unroll
+    for (int v = 0; v < NY / 4; ++v) {
+        const float4 f = reinterpret_cast<const float4*>(yr)[v];
+        y[4 * v] = f.x, y[4 * v + 1] = f.y, y[4 * v + 2] = f.z, y[4 * v + 3] = f.w;
+    }
+#pragma unroll
+    for (int i = 0; i < CW; ++i)
+#pragma unroll
+        for (int t = 0; t < K; ++t) acc[t] = __builtin_fmaf(d[R + i], y[i + t], acc[t]);
+}
+
+template <int K>
+DEV void corr_band_rows(const float* __restrict__ dz0, const float* __restrict__ y0, int stride,
+                        const LevelGeom& lg, int q, int np, float* __restrict__ slot, int lane)
+{
+    constexpr int R = K / 2;
+    constexpr int PS = K <= 1 ? 1 : (K <= 2 ? 2 : (K <= 4 ? 4 : 8));  // lanes per row group
+    constexpr int NG = 64 / PS;                                        // row groups
+    const int p = lane & (PS - 1), rg = lane / PS;
+    const bool active = p < K;
+    const int prow = active ? p : R;  // inactive lanes read a valid row and are dropped below
+    float acc[K];
+#pragma unroll
+    for (int t = 0; t < K; ++t) acc[t] = 0.f;
+    for (int pp = 0; pp < np; ++pp) {
+        const float* dzb = dz0 + pp * stride + lg.off + q * lg.band;
+        const float* yb = y0 + pp * stride + lg.off + q * lg.band;
+        for (int j = rg; j < lg.h; j += NG) {
+            const float* dzr = dzb + (j + R) * lg.pitch;  // array column 0 of site row j
+            const float* yr = yb + (j + prow) * lg.pitch;  // site row j + p - R
+            if (lg.w <= 8) {
+                corr_row_chunk<K, 8>(dzr, yr, acc);
+            } else {
+                for (int i0 = 0; i0 < lg.w; i0 += 16) corr_row_chunk<K, 16>(dzr + i0, yr + i0, acc);
+            }
         }
     }
-    return active ? acc : 0.f;
+#pragma unroll
+    for (int t = 0; t < K; ++t)
+#pragma unroll
+        for (int m = PS; m < 64; m <<= 1) acc[t] += __shfl_xor(acc[t], m, 64);
+    if (rg == 0 && active) {
+#pragma unroll
+        for (int t = 0; t < K; ++t) slot[p * K + t] += acc[t];
+    }
+}
+
+// Backward, one band of one level: kernel gradient into `gl` and, if dx is
+// wanted, the rotated-kernel filter for dx; one pass over the tiles when every
+// level fits a single register-tile round.
+template <int K, bool ONE>
+DEV void grad_and_filter(float* side_in, const float* side_aux, int stride, const LevelGeom& lg, int q, int np,
+                         const float (&w)[K * K], float (&gl)[K * K], bool have_out, int lane)
+{
+    if (ONE && have_out) {
+        filter_band<K, ONE, true>(side_in, side_aux, stride, lg, q, np, w, gl, lane);
+    } else {
+        corr_band<K>(side_in, side_aux, stride, lg, q, np, gl, lane);
+        if (have_out) filter_band<K, ONE, false>(side_in, side_aux, stride, lg, q, np, w, gl, lane);
+    }
 }
 
 // ----------------------------------------------------------------------------
@@ -584,7 +697,7 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(const FusedArgs a)
 
     // LDS: [folded weights][coarse kernel-gradient sums (backward)][planes]
     const int wt_floats = ceil4c((1 + 4 * L) * KK);
-    const int gc_floats = BWD ? L * kWaves * 64 : 0;
+    const int gc_floats = BWD ? ceil4c(L * 4 * KK) : 0;
     float* wtab = lds;
     float* gco = lds + wt_floats;
     float* planes = lds + wt_floats + gc_floats;
@@ -608,9 +721,10 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(const FusedArgs a)
     }
     __syncthreads();
 
-    float g0[KK], g1[KK];  // backward: per-lane kernel-gradient sums (base, level 1 band `wave`)
+    // backward: per-lane kernel-gradient sums (base; levels 1 and 2 of band `wave`)
+    float g0[KK], g1[KK], g2[KK];
 #pragma unroll
-    for (int t = 0; t < KK; ++t) g0[t] = g1[t] = 0.f;
+    for (int t = 0; t < KK; ++t) g0[t] = g1[t] = g2[t] = 0.f;
 
     const ST* in = reinterpret_cast<const ST*>(a.in);
     const ST* aux = reinterpret_cast<const ST*>(a.aux);
@@ -646,22 +760,28 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(const FusedArgs a)
             __syncthreads();
         }
 
-        // 3. subband filtering, one band per wavefront
+        // 3. subband filtering, one band per wavefront. In the backward pass the
+        //    kernel gradient of each band is accumulated on the way: for levels
+        //    1..3 in per-lane registers (in the same pass over the tiles as the
+        //    dx filter when every level fits one tile round), for deeper levels
+        //    row by row into LDS.
         for (int l = 1; l <= L; ++l) {
             const LevelGeom& lg = g.lv[l];
+            float w[KK];
+            fetch_weights<K>(wtab, wrow(l, q), BWD, lane, w);
             if constexpr (BWD) {
-                // kernel gradient of level l band q: dZ_l (the dy pyramid) against Y_l(x)
-                if (l == 1) {
-                    corr_band<K>(side_in, side_aux, stride, lg, q, np, g1, lane);
+                if (l <= reg_levels<ONE>()) {
+                    // static choice of the accumulator array keeps it in registers
+                    if (l == 1)
+                        grad_and_filter<K, ONE>(side_in, side_aux, stride, lg, q, np, w, g1, have_out, lane);
+                    else
+                        grad_and_filter<K, ONE>(side_in, side_aux, stride, lg, q, np, w, g2, have_out, lane);
                 } else {
-                    float* slot = gco + ((l - 1) * kWaves + q) * 64 + lane;
-                    *slot = corr_band_taps<K>(side_in, side_aux, stride, lg, q, np, *slot, lane);
+                    corr_band_rows<K>(side_in, side_aux, stride, lg, q, np, gco + ((l - 1) * 4 + q) * KK, lane);
+                    if (have_out) filter_band<K, ONE, false>(side_in, side_aux, stride, lg, q, np, w, g1, lane);
                 }
-            }
-            if (!BWD || have_out) {
-                float w[KK];
-                fetch_weights<K>(wtab, wrow(l, q), BWD, lane, w);
-                filter_band<K, ONE>(side_in, stride, lg, q, np, w, lane);
+            } else {
+                filter_band<K, ONE, false>(side_in, side_aux, stride, lg, q, np, w, g1, lane);
             }
         }
         __syncthreads();
@@ -697,23 +817,20 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(const FusedArgs a)
         for (int t = 0; t < KK; ++t) {
             const float v0 = wave_sum(g0[t]);
             const float v1 = wave_sum(g1[t]);
+            const float v2 = wave_sum(g2[t]);
             if (lane == 0) {
                 red[wave * KK + t] = v0;
                 red[(kWaves + wave) * KK + t] = v1;
+                red[(2 * kWaves + wave) * KK + t] = v2;
             }
         }
         __syncthreads();
         float* dst = a.partial + ((long)chunk * C + c) * NP;
         for (int t = tid; t < KK; t += kThreads)
             dst[t] = ((red[t] + red[KK + t]) + red[2 * KK + t]) + red[3 * KK + t];
-        if (L >= 1)
-            for (int i = tid; i < 4 * KK; i += kThreads) dst[KK + i] = red[kWaves * KK + i];
-        for (int l = 2; l <= L; ++l)
-            for (int i = tid; i < 4 * KK; i += kThreads) {
-                const int qq = i / KK, t = i - qq * KK;
-                const float* s = gco + ((l - 1) * kWaves + qq) * 64;
-                dst[KK + ((l - 1) * 4 + qq) * KK + t] = (KK <= 32) ? s[t] + s[32 + t] : s[t];
-            }
+        // register-held levels: band q's sums came from wavefront q
+        for (int i = tid; i < 4 * KK * min(L, reg_levels<ONE>()); i += kThreads) dst[KK + i] = red[kWaves * KK + i];
+        for (int i = 4 * KK * reg_levels<ONE>() + tid; i < 4 * L * KK; i += kThreads) dst[KK + i] = gco[i];
     }
 }
 
