@@ -44,8 +44,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="only run a plain device-to-device copy of this many MiB (profiler counter calibration)")
-    ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "traffic_counters.json"),
-                    help="measured HBM bytes of the dominant kernel (from rocprofv3 counters)")
+    ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "hbm_traffic_wtconv_convnext_t_stage1.txt"),
+                    help="counter summary with the measured HBM bytes of the dominant kernel")
     return ap.parse_args()
 
 
@@ -69,20 +69,33 @@ def cpu_baseline(inp, work_bytes, seconds):
                       f"{reps} repetitions in {el:.1f} s, float64; {el / reps * 1e3:.1f} ms per step"}
 
 
-def load_traffic(path, kernel, work):
-    """Measured HBM bytes per launch of `kernel`, if a counter summary for the
-    current kernel build is present; else None."""
+def kernel_source_hash():
+    """sha256 of the HIP sources the library is built from."""
+    import hashlib
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2608_10805_amd", "csrc")
+    for name in sorted(os.listdir(csrc)):
+        with open(os.path.join(csrc, name), "rb") as f:
+            h.update(name.encode() + b"\0" + f.read())
+    return h.hexdigest()
+
+
+def load_traffic(path, kernel):
+    """Measured HBM bytes per launch of `kernel` from a counter summary under
+    profiles/ ("key: value" lines), if it was taken on the current kernel
+    sources and workload; else None."""
     if not os.path.exists(path):
         return None
-    try:
-        with open(path) as f:
-            t = json.load(f)
-    except (OSError, ValueError):
+    rec = {}
+    with open(path) as f:
+        for line in f:
+            if ":" in line and not line.startswith("#"):
+                k, v = line.split(":", 1)
+                rec[k.strip()] = v.strip()
+    if rec.get("kernel_source_sha256") != kernel_source_hash() or rec.get("workload") != WORKLOAD["workload"]:
         return None
-    rec = t.get(kernel)
-    if not rec or rec.get("workload") != WORKLOAD["workload"]:
-        return None
-    return rec.get("bytes_per_launch")
+    key = f"{kernel}_hbm_bytes_per_launch"
+    return float(rec[key]) if key in rec else None
 
 
 def main():
@@ -163,12 +176,12 @@ def main():
     work = iomodel.single_pass_work(B, C, H, W, k, L, "f32")
     value = work.bytes_fwdbwd / (ms_step * 1e-3) / 1e9
     if bwd_ms >= fwd_ms:
-        dom, dom_ms, dom_fma, dom_bytes = "fused_kernel<5,float,bwd>", bwd_ms, work.fma_bwd, work.bytes_bwd
+        dom, dom_ms, dom_fma, dom_bytes = "backward_fused", bwd_ms, work.fma_bwd, work.bytes_bwd
     else:
-        dom, dom_ms, dom_fma, dom_bytes = "fused_kernel<5,float,fwd>", fwd_ms, work.fma_fwd, work.bytes_fwd
+        dom, dom_ms, dom_fma, dom_bytes = "forward", fwd_ms, work.fma_fwd, work.bytes_fwd
     achieved = 2.0 * dom_fma / (dom_ms * 1e-3) / 1e12
     peak = iomodel.FP32_FLOPS / 1e12
-    traffic = load_traffic(args.traffic, dom, work)
+    traffic = load_traffic(args.traffic, dom)
     roofline = {"bound": "alu", "achieved": round(achieved, 3), "peak": round(peak, 1), "unit": "TFLOP/s",
                 "frac": round(achieved / peak, 4), "traffic": traffic, "kernel": dom,
                 "kernel_ms": round(dom_ms, 5),
