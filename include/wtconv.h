@@ -37,7 +37,7 @@
  *   - level_w / level_scale (and their gradients) are HOST arrays of L DEVICE
  *     pointers: level_w[l-1] -> [4C][k][k], level_scale[l-1] -> [4C].
  *   - The caller owns every buffer. The library allocates no device memory;
- *     the backward pass takes a caller-provided workspace.
+ *     scratch space comes from a caller-provided workspace.
  *   - Work is enqueued on `stream` and is asynchronous. Argument errors are
  *     detected on the host before any HIP call and returned synchronously;
  *     launch errors are returned as WTCONV_ERR_HIP; device faults surface at
@@ -45,10 +45,10 @@
  *   - Gradient outputs are overwritten, not accumulated into.
  *   - Entry points are reentrant; the library keeps no mutable global state.
  *     Results are bitwise reproducible for identical inputs and shapes.
- *   - Supported: B, C, H, W >= 1; k in {1, 3, 5, 7}; 0 <= L <= 8; planes whose
- *     fused working set fits in one compute unit's 160 KB of LDS (for float32
- *     k = 5: forward up to about 120 x 120, backward up to about 84 x 84
- *     pixels per plane). Larger planes return WTCONV_ERR_UNSUPPORTED.
+ *   - Supported: B, C, H, W >= 1; k in {1, 3, 5, 7}; 0 <= L <= 8. Planes whose
+ *     fused working set fits one compute unit's 160 KB of LDS (float32, k = 5:
+ *     forward up to about 120 x 120 pixels, backward up to about 84 x 84) run
+ *     in one pass; larger planes use a split with a workspace.
  */
 #ifndef WTCONV_H
 #define WTCONV_H
@@ -78,7 +78,7 @@ typedef enum {
     WTCONV_ERR_DTYPE = 5,       /* unknown dtype                                  */
     WTCONV_ERR_ALIAS = 6,       /* an output overlaps an input or another output  */
     WTCONV_ERR_WORKSPACE = 7,   /* workspace NULL or smaller than required        */
-    WTCONV_ERR_UNSUPPORTED = 8, /* plane too large for the on-chip working set    */
+    WTCONV_ERR_UNSUPPORTED = 8, /* no execution plan for this shape               */
     WTCONV_ERR_HIP = 9          /* a HIP runtime call or kernel launch failed     */
 } wtconv_status;
 
@@ -90,18 +90,29 @@ typedef struct {
     wtconv_dtype dtype;
 } wtconv_desc;
 
+/* Bytes of device workspace wtconv_forward needs for `desc` (0 when the planes
+ * are processed on chip in one pass, or on a bad desc). */
+size_t wtconv_forward_workspace_bytes(const wtconv_desc* desc);
+
 /*
  * Forward pass, Algorithm 1 (Section 2.1).
- *   x            [B][C][H][W] dtype, read once
+ *   x            [B][C][H][W] dtype
  *   base_w       [C][k][k] float32           base_scale [C] float32
  *   level_w      host array of L device ptrs, each [4C][k][k] float32
  *   level_scale  host array of L device ptrs, each [4C] float32
- *   y            [B][C][H][W] dtype, written once; must not overlap x
- * level_w / level_scale may be NULL when L = 0.
+ *   y            [B][C][H][W] dtype; must not overlap x
+ *   workspace    device memory of at least wtconv_forward_workspace_bytes(desc)
+ *                bytes, 16-byte aligned; may be NULL when that size is 0. Its
+ *                contents are scratch.
+ * level_w / level_scale may be NULL when L = 0. Planes whose working set fits
+ * one compute unit's LDS are read once and written once; larger planes are
+ * split (the coarse levels run on the quarter-size level-1 carrier held in the
+ * workspace, the base path and level 1 run on tiles with a halo).
  */
 wtconv_status wtconv_forward(const wtconv_desc* desc, const void* x, const float* base_w,
                              const float* base_scale, const float* const* level_w,
-                             const float* const* level_scale, void* y, hipStream_t stream);
+                             const float* const* level_scale, void* y, void* workspace,
+                             size_t workspace_bytes, hipStream_t stream);
 
 /* Bytes of device workspace wtconv_backward needs for `desc` (0 on a bad desc). */
 size_t wtconv_backward_workspace_bytes(const wtconv_desc* desc);

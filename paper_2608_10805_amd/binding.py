@@ -17,8 +17,8 @@ STATUS = {
     4: "WTCONV_ERR_LEVELS", 5: "WTCONV_ERR_DTYPE", 6: "WTCONV_ERR_ALIAS", 7: "WTCONV_ERR_WORKSPACE",
     8: "WTCONV_ERR_UNSUPPORTED", 9: "WTCONV_ERR_HIP",
 }
-EXPORTS = ["wtconv_forward", "wtconv_backward", "wtconv_backward_workspace_bytes", "wtconv_backward_partials",
-           "wtconv_backward_finalize", "wtconv_status_string", "wtconv_version"]
+EXPORTS = ["wtconv_forward_workspace_bytes", "wtconv_forward", "wtconv_backward", "wtconv_backward_workspace_bytes",
+           "wtconv_backward_partials", "wtconv_backward_finalize", "wtconv_status_string", "wtconv_version"]
 MAX_LEVELS = 8
 
 
@@ -47,7 +47,9 @@ def load():
         from . import build
         build.build()
     lib = ctypes.CDLL(LIB_PATH)
-    lib.wtconv_forward.argtypes = [ctypes.POINTER(Desc), _P, _P, _P, _PP, _PP, _P, _P]
+    lib.wtconv_forward_workspace_bytes.argtypes = [ctypes.POINTER(Desc)]
+    lib.wtconv_forward_workspace_bytes.restype = ctypes.c_size_t
+    lib.wtconv_forward.argtypes = [ctypes.POINTER(Desc), _P, _P, _P, _PP, _PP, _P, _P, ctypes.c_size_t, _P]
     lib.wtconv_forward.restype = ctypes.c_int
     lib.wtconv_backward_workspace_bytes.argtypes = [ctypes.POINTER(Desc)]
     lib.wtconv_backward_workspace_bytes.restype = ctypes.c_size_t
@@ -90,10 +92,15 @@ def _ptr_array(ptrs):
 # raw entry points (integers as device addresses)
 # ----------------------------------------------------------------------------
 
-def wtconv_forward(desc: Desc, x, base_w, base_scale, level_w, level_scale, y, stream) -> int:
+def wtconv_forward_workspace_bytes(desc: Desc) -> int:
+    return int(load().wtconv_forward_workspace_bytes(ctypes.byref(desc)))
+
+
+def wtconv_forward(desc: Desc, x, base_w, base_scale, level_w, level_scale, y, workspace, workspace_bytes,
+                   stream) -> int:
     """Raw call: pointers are integers (device addresses); level_* are lists of addresses."""
     return load().wtconv_forward(ctypes.byref(desc), x, base_w, base_scale, _ptr_array(level_w),
-                                 _ptr_array(level_scale), y, stream)
+                                 _ptr_array(level_scale), y, workspace, ctypes.c_size_t(workspace_bytes), stream)
 
 
 def wtconv_backward_workspace_bytes(desc: Desc) -> int:
@@ -150,9 +157,10 @@ def _stream(device):
     return torch.cuda.current_stream(device).cuda_stream
 
 
-def forward(x, base_w, base_scale, level_w, level_scale, out=None):
+def forward(x, base_w, base_scale, level_w, level_scale, out=None, workspace=None):
     """y = WTConv(x) on the current stream. x: [B,C,H,W] fp32/bf16/fp16 on the GPU;
-    base_w [C,k,k], base_scale [C], level_w list of [4C,k,k], level_scale list of [4C] (fp32)."""
+    base_w [C,k,k], base_scale [C], level_w list of [4C,k,k], level_scale list of [4C] (fp32).
+    Large planes need a device workspace; one is allocated if `workspace` is None or too small."""
     import torch
     _require(x, "x")
     B, C, H, W = x.shape
@@ -164,9 +172,15 @@ def forward(x, base_w, base_scale, level_w, level_scale, out=None):
         _require(t, name, torch.float32)
     y = torch.empty_like(x) if out is None else out
     desc = make_desc(B, C, H, W, k, L, _dtype_code(x))
+    nbytes = wtconv_forward_workspace_bytes(desc)
+    ws_ptr = None
+    if nbytes:
+        if workspace is None or workspace.numel() * workspace.element_size() < nbytes:
+            workspace = torch.empty(nbytes, dtype=torch.uint8, device=x.device)
+        ws_ptr = workspace.data_ptr()
     _check(wtconv_forward(desc, x.data_ptr(), base_w.data_ptr(), base_scale.data_ptr(),
                           [t.data_ptr() for t in level_w], [t.data_ptr() for t in level_scale], y.data_ptr(),
-                          _stream(x.device)))
+                          ws_ptr, nbytes, _stream(x.device)))
     return y
 
 

@@ -165,13 +165,14 @@ bool overlaps(const void* a, size_t na, const void* b, size_t nb)
 }
 
 size_t elem_size(wtconv_dtype dt) { return dt == WTCONV_F32 ? 4 : 2; }
+size_t align256(size_t n) { return (n + 255) / 256 * 256; }
 
 wtconv_status check_desc(const wtconv_desc* d)
 {
     if (!d) return WTCONV_ERR_NULL;
     if (d->B < 1 || d->C < 1 || d->H < 1 || d->W < 1) return WTCONV_ERR_SHAPE;
     if ((long)d->H * d->W > (1L << 30) || (long)d->B * d->C > (1L << 30) ||
-        (long)d->C * 4 * 49 > (1L << 30))
+        (long)d->C * 4 * 49 > (1L << 30) || (long)d->B * d->C * d->H * d->W > (1L << 40))
         return WTCONV_ERR_SHAPE;
     if (d->k != 1 && d->k != 3 && d->k != 5 && d->k != 7) return WTCONV_ERR_KSIZE;
     if (d->L < 0 || d->L > WTCONV_MAX_LEVELS) return WTCONV_ERR_LEVELS;
@@ -200,79 +201,280 @@ void fill_params(wtc::ParamPtrs& p, int L, const float* w0, const float* s0, con
     }
 }
 
-int vec_ok(wtconv_dtype dt, const void* a, const void* b, const void* c)
+// Parameter gradient destinations (device pointers).
+struct Grads {
+    float* dw0;
+    float* ds0;
+    float* dlw[kMaxLevels];
+    float* dls[kMaxLevels];
+};
+
+// The same parameters, levels shifted by one: the coarse sub-problem's level
+// l is the full problem's level l + 1.
+wtc::ParamPtrs shift_params(const wtc::ParamPtrs& p)
+{
+    wtc::ParamPtrs s = p;
+    for (int l = 0; l + 1 < kMaxLevels; ++l) {
+        s.lw[l] = p.lw[l + 1];
+        s.ls[l] = p.ls[l + 1];
+    }
+    s.lw[kMaxLevels - 1] = s.ls[kMaxLevels - 1] = nullptr;
+    return s;
+}
+
+Grads shift_grads(const Grads& g)
+{
+    Grads s = g;
+    for (int l = 0; l + 1 < kMaxLevels; ++l) {
+        s.dlw[l] = g.dlw[l + 1];
+        s.dls[l] = g.dls[l + 1];
+    }
+    s.dlw[kMaxLevels - 1] = s.dls[kMaxLevels - 1] = nullptr;
+    return s;
+}
+
+int vec_ok(const void* a, const void* b, const void* c)
 {
     const uintptr_t m = 15;  // 16-byte loads of the input planes
-    (void)dt;
     return (((uintptr_t)a & m) == 0 && ((uintptr_t)b & m) == 0 && ((uintptr_t)c & m) == 0) ? 1 : 0;
 }
 
-}  // namespace
+// ----------------------------------------------------------------------------
+// Large planes. A plane whose working set does not fit one CU's LDS is split:
+// the coarse branch (levels 2..L) is exactly the WTConv, without base path, of
+// the level-1 raw LL carrier X1 (a quarter-size plane), whose output is the
+// coarse levels' contribution at the level-1 grid; in the backward pass that
+// sub-problem's input gradient is the same contribution for dx, and its kernel
+// gradients are those of levels 2..L. The sub-problem recurses until it fits.
+// The full-resolution part (base path and level 1) then runs in region mode:
+// each workgroup computes one T x T output tile from a region with a halo of
+// 2R pixels (the level-1 receptive field), adding the carry at level 1.
+// ----------------------------------------------------------------------------
+struct RegionPlan {
+    Plan pl;
+    int T = 0, h = 0, ntx = 0, nty = 0;
+};
 
-extern "C" {
-
-int wtconv_version(void) { return 100; }
-
-const char* wtconv_status_string(wtconv_status s)
+bool make_region_plan(const wtconv_desc& d, bool bwd, RegionPlan& rp)
 {
-    switch (s) {
-        case WTCONV_OK: return "ok";
-        case WTCONV_ERR_NULL: return "a required pointer is NULL";
-        case WTCONV_ERR_SHAPE: return "invalid shape (B, C, H, W must be >= 1 and sizes must fit)";
-        case WTCONV_ERR_KSIZE: return "unsupported kernel size (k must be 1, 3, 5 or 7)";
-        case WTCONV_ERR_LEVELS: return "unsupported number of levels (0 <= L <= 8)";
-        case WTCONV_ERR_DTYPE: return "unknown dtype";
-        case WTCONV_ERR_ALIAS: return "an output overlaps an input or another output";
-        case WTCONV_ERR_WORKSPACE: return "workspace missing or too small";
-        case WTCONV_ERR_UNSUPPORTED: return "plane too large for the on-chip working set";
-        case WTCONV_ERR_HIP: return "HIP runtime error";
+    const int R = d.k / 2;
+    const int m = d.L > 0 ? 1 : 0;
+    rp.h = ceil_to(m ? 2 * R : R, 4);
+    for (int T : {56, 48, 40, 32, 24, 16, 8}) {
+        wtconv_desc rd = d;
+        rd.B = 1;  // one region resident at a time
+        rd.H = rd.W = T + 2 * rp.h;
+        rd.L = m;
+        Plan pl;
+        if (!make_plan(rd, bwd, pl) || pl.PP != 1) continue;
+        rp.T = T;
+        rp.ntx = cdiv(d.W, T);
+        rp.nty = cdiv(d.H, T);
+        const long ntiles = (long)rp.ntx * rp.nty;
+        const int target = bwd ? kBackwardTargetWorkgroups : kForwardTargetWorkgroups;
+        const long chunks_target = std::max(1L, (target + d.C * ntiles - 1) / (d.C * ntiles));
+        pl.nb = (int)((d.B + chunks_target - 1) / chunks_target);
+        pl.nchunks = cdiv(d.B, pl.nb);
+        pl.one_round = 0;
+        if ((long)pl.nchunks * ntiles * d.C > INT32_MAX) return false;  // grid size
+        rp.pl = pl;
+        return true;
     }
-    return "unknown status";
+    return false;
 }
 
-wtconv_status wtconv_forward(const wtconv_desc* desc, const void* x, const float* base_w,
-                             const float* base_scale, const float* const* level_w,
-                             const float* const* level_scale, void* y, hipStream_t stream)
-{
-    wtconv_status st = check_desc(desc);
-    if (st != WTCONV_OK) return st;
-    const wtconv_desc& d = *desc;
-    if (!x || !y || !base_w || !base_scale) return WTCONV_ERR_NULL;
-    if ((st = check_levels(d.L, level_w, level_scale)) != WTCONV_OK) return st;
-    const size_t bytes = (size_t)d.B * d.C * d.H * d.W * elem_size(d.dtype);
-    if (overlaps(x, bytes, y, bytes)) return WTCONV_ERR_ALIAS;
-    Plan pl;
-    if (!make_plan(d, false, pl)) return WTCONV_ERR_UNSUPPORTED;
+long level1_floats(const wtconv_desc& d) { return (long)d.B * d.C * ((d.H + 1) / 2) * ((d.W + 1) / 2); }
 
+wtconv_desc coarse_desc(const wtconv_desc& d)
+{
+    wtconv_desc s = d;
+    s.H = (d.H + 1) / 2;
+    s.W = (d.W + 1) / 2;
+    s.L = d.L - 1;
+    s.dtype = WTCONV_F32;
+    return s;
+}
+
+const size_t kUnsupported = ~(size_t)0;
+
+size_t forward_ws(const wtconv_desc& d)
+{
+    Plan pl;
+    if (make_plan(d, false, pl)) return 0;
+    RegionPlan rp;
+    if (!make_region_plan(d, false, rp)) return kUnsupported;
+    if (d.L < 2) return 0;
+    const size_t sub = forward_ws(coarse_desc(d));
+    if (sub == kUnsupported) return kUnsupported;
+    return 2 * align256(level1_floats(d) * 4) + sub;
+}
+
+size_t backward_ws(const wtconv_desc& d)
+{
+    const int NP = wtc::partial_floats_per_channel(d.k, d.L);
+    Plan pl;
+    if (make_plan(d, true, pl)) return align256((size_t)pl.nchunks * d.C * NP * 4);
+    RegionPlan rp;
+    if (!make_region_plan(d, true, rp)) return kUnsupported;
+    const int m = d.L > 0 ? 1 : 0;
+    const size_t part = align256((size_t)rp.pl.nchunks * rp.ntx * rp.nty * d.C *
+                                 wtc::partial_floats_per_channel(d.k, m) * 4);
+    if (d.L < 2) return part;
+    const size_t sub = backward_ws(coarse_desc(d));
+    if (sub == kUnsupported) return kUnsupported;
+    return part + 3 * align256(level1_floats(d) * 4) + sub;
+}
+
+FusedArgs base_args(const wtconv_desc& d, const Plan& pl, const void* in, const void* aux, void* out,
+                    const wtc::ParamPtrs& p, int skip_base)
+{
     FusedArgs a;
     memset(&a, 0, sizeof(a));
-    a.in = x;
-    a.aux = nullptr;
-    a.out = y;
-    a.partial = nullptr;
-    fill_params(a.p, d.L, base_w, base_scale, level_w, level_scale);
+    a.in = in;
+    a.aux = aux;
+    a.out = out;
+    a.p = p;
     a.B = d.B;
     a.C = d.C;
     a.nb = pl.nb;
     a.PP = pl.PP;
-    a.vec_ok = vec_ok(d.dtype, x, y, x);
+    a.vec_ok = vec_ok(in, aux ? aux : in, out ? out : in);
     a.lds_floats = pl.lds_floats;
     a.one_round = pl.one_round;
+    a.skip_base = skip_base;
     a.g = pl.g;
-    const hipError_t e = wtc::launch_forward(d.k, d.dtype, a, pl.nchunks * d.C, stream);
-    return e == hipSuccess ? WTCONV_OK : WTCONV_ERR_HIP;
+    return a;
 }
 
-size_t wtconv_backward_workspace_bytes(const wtconv_desc* desc)
+void set_region(FusedArgs& a, const wtconv_desc& d, const RegionPlan& rp, const float* carry)
 {
-    if (check_desc(desc) != WTCONV_OK) return 0;
-    Plan pl;
-    if (!make_plan(*desc, true, pl)) return 0;
-    const size_t n = (size_t)pl.nchunks * desc->C * wtc::partial_floats_per_channel(desc->k, desc->L);
-    return (n * sizeof(float) + 255) / 256 * 256;
+    a.rg_ntx = rp.ntx;
+    a.rg_nty = rp.nty;
+    a.rg_T = rp.T;
+    a.rg_h = rp.h;
+    a.real_H = d.H;
+    a.real_W = d.W;
+    a.rg_r_itx = 1.0f / (float)(rp.T / 4);
+    a.rg_r_itiles = 1.0f / (float)((rp.T / 4) * (rp.T / 4));
+    a.carry = carry;
+    a.carry_H = (d.H + 1) / 2;
+    a.carry_W = (d.W + 1) / 2;
 }
 
-namespace {
+wtconv_status hip_status(hipError_t e) { return e == hipSuccess ? WTCONV_OK : WTCONV_ERR_HIP; }
+
+wtconv_status carrier(const wtconv_desc& d, const void* in, float* out, hipStream_t stream)
+{
+    wtc::CarrierArgs c;
+    c.in = in;
+    c.out = out;
+    c.planes = (long)d.B * d.C;
+    c.H = d.H;
+    c.W = d.W;
+    c.H1 = (d.H + 1) / 2;
+    c.W1 = (d.W + 1) / 2;
+    c.vec_ok = 0;
+    return hip_status(wtc::launch_carrier(d.dtype, c, stream));
+}
+
+wtconv_status forward_impl(const wtconv_desc& d, const void* x, const wtc::ParamPtrs& p, void* y, char* ws,
+                           int skip_base, hipStream_t stream)
+{
+    Plan pl;
+    if (make_plan(d, false, pl)) {
+        const FusedArgs a = base_args(d, pl, x, nullptr, y, p, skip_base);
+        return hip_status(wtc::launch_forward(d.k, d.dtype, a, pl.nchunks * d.C, stream));
+    }
+    RegionPlan rp;
+    if (!make_region_plan(d, false, rp)) return WTCONV_ERR_UNSUPPORTED;
+    const float* carry = nullptr;
+    if (d.L >= 2) {
+        const size_t n1 = align256(level1_floats(d) * 4);
+        float* x1 = reinterpret_cast<float*>(ws);
+        float* c1 = reinterpret_cast<float*>(ws + n1);
+        wtconv_status st = carrier(d, x, x1, stream);
+        if (st != WTCONV_OK) return st;
+        st = forward_impl(coarse_desc(d), x1, shift_params(p), c1, ws + 2 * n1, 1, stream);
+        if (st != WTCONV_OK) return st;
+        carry = c1;
+    }
+    FusedArgs a = base_args(d, rp.pl, x, nullptr, y, p, skip_base);
+    set_region(a, d, rp, carry);
+    return hip_status(wtc::launch_forward(d.k, d.dtype, a, rp.pl.nchunks * rp.ntx * rp.nty * d.C, stream));
+}
+
+wtconv_status partials_impl(const wtconv_desc& d, const void* x, const void* dy, const wtc::ParamPtrs& p,
+                            void* dx, char* ws, int skip_base, hipStream_t stream)
+{
+    Plan pl;
+    if (make_plan(d, true, pl)) {
+        FusedArgs a = base_args(d, pl, dy, x, dx, p, skip_base);
+        a.partial = reinterpret_cast<float*>(ws);
+        return hip_status(wtc::launch_backward(d.k, d.dtype, a, pl.nchunks * d.C, stream));
+    }
+    RegionPlan rp;
+    if (!make_region_plan(d, true, rp)) return WTCONV_ERR_UNSUPPORTED;
+    const int m = d.L > 0 ? 1 : 0;
+    const size_t part = align256((size_t)rp.pl.nchunks * rp.ntx * rp.nty * d.C *
+                                 wtc::partial_floats_per_channel(d.k, m) * 4);
+    const float* carry = nullptr;
+    if (d.L >= 2) {
+        const size_t n1 = align256(level1_floats(d) * 4);
+        float* x1 = reinterpret_cast<float*>(ws + part);
+        float* dy1 = reinterpret_cast<float*>(ws + part + n1);
+        float* dx1 = dx ? reinterpret_cast<float*>(ws + part + 2 * n1) : nullptr;
+        wtconv_status st = carrier(d, x, x1, stream);
+        if (st == WTCONV_OK) st = carrier(d, dy, dy1, stream);
+        if (st == WTCONV_OK)
+            st = partials_impl(coarse_desc(d), x1, dy1, shift_params(p), dx1, ws + part + 3 * n1, 1, stream);
+        if (st != WTCONV_OK) return st;
+        carry = dx1;
+    }
+    FusedArgs a = base_args(d, rp.pl, dy, x, dx, p, skip_base);
+    set_region(a, d, rp, carry);
+    a.partial = reinterpret_cast<float*>(ws);
+    return hip_status(wtc::launch_backward(d.k, d.dtype, a, rp.pl.nchunks * rp.ntx * rp.nty * d.C, stream));
+}
+
+wtconv_status reduce(const wtconv_desc& d, int L, int nchunks, const wtc::ParamPtrs& p, const Grads& gr,
+                     const char* ws, int skip_base, hipStream_t stream)
+{
+    wtc::ReduceArgs r;
+    memset(&r, 0, sizeof(r));
+    r.partial = reinterpret_cast<const float*>(ws);
+    r.nchunks = nchunks;
+    r.C = d.C;
+    r.k = d.k;
+    r.L = L;
+    r.skip_base = skip_base;
+    r.p = p;
+    r.dw0 = gr.dw0;
+    r.ds0 = gr.ds0;
+    for (int l = 0; l < L; ++l) {
+        r.dlw[l] = gr.dlw[l];
+        r.dls[l] = gr.dls[l];
+    }
+    return hip_status(wtc::launch_reduce(r, stream));
+}
+
+wtconv_status finalize_impl(const wtconv_desc& d, const wtc::ParamPtrs& p, const Grads& gr, const char* ws,
+                            int skip_base, hipStream_t stream)
+{
+    Plan pl;
+    if (make_plan(d, true, pl)) return reduce(d, d.L, pl.nchunks, p, gr, ws, skip_base, stream);
+    RegionPlan rp;
+    if (!make_region_plan(d, true, rp)) return WTCONV_ERR_UNSUPPORTED;
+    const int m = d.L > 0 ? 1 : 0;
+    if (d.L >= 2) {
+        const size_t part = align256((size_t)rp.pl.nchunks * rp.ntx * rp.nty * d.C *
+                                     wtc::partial_floats_per_channel(d.k, m) * 4);
+        const size_t n1 = align256(level1_floats(d) * 4);
+        const wtconv_status st =
+            finalize_impl(coarse_desc(d), shift_params(p), shift_grads(gr), ws + part + 3 * n1, 1, stream);
+        if (st != WTCONV_OK) return st;
+    }
+    return reduce(d, m, rp.pl.nchunks * rp.ntx * rp.nty, p, gr, ws, skip_base, stream);
+}
 
 struct Range {
     const void* p;
@@ -304,24 +506,28 @@ int param_ranges(const wtconv_desc& d, const float* w0, const float* s0, const f
     return n;
 }
 
-wtconv_status partials_impl(const wtconv_desc* desc, const void* x, const void* dy, const float* base_w,
-                            const float* base_scale, const float* const* level_w,
-                            const float* const* level_scale, void* dx, void* workspace, size_t workspace_bytes,
-                            hipStream_t stream, const Plan* plan_in, const Range* extra_outs, int n_extra)
+wtconv_status check_workspace(size_t need, const void* ws, size_t bytes)
+{
+    if (need == kUnsupported) return WTCONV_ERR_UNSUPPORTED;
+    if (need == 0) return WTCONV_OK;
+    if (!ws || bytes < need || ((uintptr_t)ws & 15)) return WTCONV_ERR_WORKSPACE;
+    return WTCONV_OK;
+}
+
+// Shared argument checks of the backward entry points.
+wtconv_status backward_checks(const wtconv_desc* desc, const void* x, const void* dy, const float* base_w,
+                              const float* base_scale, const float* const* level_w,
+                              const float* const* level_scale, const void* dx, const void* workspace,
+                              size_t workspace_bytes, const Range* extra_outs, int n_extra, size_t* need_out)
 {
     wtconv_status st = check_desc(desc);
     if (st != WTCONV_OK) return st;
     const wtconv_desc& d = *desc;
     if (!x || !dy || !base_w || !base_scale) return WTCONV_ERR_NULL;
     if ((st = check_levels(d.L, level_w, level_scale)) != WTCONV_OK) return st;
-    Plan pl;
-    if (plan_in)
-        pl = *plan_in;
-    else if (!make_plan(d, true, pl))
-        return WTCONV_ERR_UNSUPPORTED;
-    const size_t need = wtconv_backward_workspace_bytes(desc);
-    if (!workspace || workspace_bytes < need || ((uintptr_t)workspace & 15)) return WTCONV_ERR_WORKSPACE;
-
+    const size_t need = backward_ws(d);
+    if ((st = check_workspace(need, workspace, workspace_bytes)) != WTCONV_OK) return st;
+    if (need == 0) return WTCONV_ERR_WORKSPACE;  // the backward always writes partials
     const size_t act = (size_t)d.B * d.C * d.H * d.W * elem_size(d.dtype);
     Range ins[4 + 2 * kMaxLevels];
     int ni = 0;
@@ -334,71 +540,80 @@ wtconv_status partials_impl(const wtconv_desc* desc, const void* x, const void* 
     outs[no++] = {workspace, need};
     for (int i = 0; i < n_extra; ++i) outs[no++] = extra_outs[i];
     if (any_overlap(outs, no, ins, ni)) return WTCONV_ERR_ALIAS;
-
-    FusedArgs a;
-    memset(&a, 0, sizeof(a));
-    a.in = dy;
-    a.aux = x;
-    a.out = dx;
-    a.partial = reinterpret_cast<float*>(workspace);
-    fill_params(a.p, d.L, base_w, base_scale, level_w, level_scale);
-    a.B = d.B;
-    a.C = d.C;
-    a.nb = pl.nb;
-    a.PP = pl.PP;
-    a.vec_ok = vec_ok(d.dtype, x, dy, dx ? dx : x);
-    a.lds_floats = pl.lds_floats;
-    a.one_round = pl.one_round;
-    a.g = pl.g;
-    const hipError_t e = wtc::launch_backward(d.k, d.dtype, a, pl.nchunks * d.C, stream);
-    return e == hipSuccess ? WTCONV_OK : WTCONV_ERR_HIP;
+    *need_out = need;
+    return WTCONV_OK;
 }
 
-wtconv_status finalize_impl(const wtconv_desc* desc, const float* base_w, const float* base_scale,
-                            const float* const* level_w, const float* const* level_scale, float* d_base_w,
-                            float* d_base_scale, float* const* d_level_w, float* const* d_level_scale,
-                            const void* workspace, size_t workspace_bytes, hipStream_t stream,
-                            bool checked_alias)
+Grads grads_of(int L, float* d_base_w, float* d_base_scale, float* const* d_level_w, float* const* d_level_scale)
+{
+    Grads gr;
+    memset(&gr, 0, sizeof(gr));
+    gr.dw0 = d_base_w;
+    gr.ds0 = d_base_scale;
+    for (int l = 0; l < L; ++l) {
+        gr.dlw[l] = d_level_w[l];
+        gr.dls[l] = d_level_scale[l];
+    }
+    return gr;
+}
+
+}  // namespace
+
+extern "C" {
+
+int wtconv_version(void) { return 200; }
+
+const char* wtconv_status_string(wtconv_status s)
+{
+    switch (s) {
+        case WTCONV_OK: return "ok";
+        case WTCONV_ERR_NULL: return "a required pointer is NULL";
+        case WTCONV_ERR_SHAPE: return "invalid shape (B, C, H, W must be >= 1 and sizes must fit)";
+        case WTCONV_ERR_KSIZE: return "unsupported kernel size (k must be 1, 3, 5 or 7)";
+        case WTCONV_ERR_LEVELS: return "unsupported number of levels (0 <= L <= 8)";
+        case WTCONV_ERR_DTYPE: return "unknown dtype";
+        case WTCONV_ERR_ALIAS: return "an output overlaps an input or another output";
+        case WTCONV_ERR_WORKSPACE: return "workspace missing, misaligned or too small";
+        case WTCONV_ERR_UNSUPPORTED: return "no execution plan for this shape";
+        case WTCONV_ERR_HIP: return "HIP runtime error";
+    }
+    return "unknown status";
+}
+
+size_t wtconv_forward_workspace_bytes(const wtconv_desc* desc)
+{
+    if (check_desc(desc) != WTCONV_OK) return 0;
+    const size_t n = forward_ws(*desc);
+    return n == kUnsupported ? 0 : n;
+}
+
+wtconv_status wtconv_forward(const wtconv_desc* desc, const void* x, const float* base_w,
+                             const float* base_scale, const float* const* level_w,
+                             const float* const* level_scale, void* y, void* workspace,
+                             size_t workspace_bytes, hipStream_t stream)
 {
     wtconv_status st = check_desc(desc);
     if (st != WTCONV_OK) return st;
     const wtconv_desc& d = *desc;
-    if (!base_w || !base_scale || !d_base_w || !d_base_scale) return WTCONV_ERR_NULL;
+    if (!x || !y || !base_w || !base_scale) return WTCONV_ERR_NULL;
     if ((st = check_levels(d.L, level_w, level_scale)) != WTCONV_OK) return st;
-    if ((st = check_levels(d.L, (const float* const*)d_level_w, (const float* const*)d_level_scale)) != WTCONV_OK)
-        return st;
-    Plan pl;
-    if (!make_plan(d, true, pl)) return WTCONV_ERR_UNSUPPORTED;
-    const size_t need = wtconv_backward_workspace_bytes(desc);
-    if (!workspace || workspace_bytes < need || ((uintptr_t)workspace & 15)) return WTCONV_ERR_WORKSPACE;
-    if (!checked_alias) {
-        Range ins[3 + 2 * kMaxLevels];
-        int ni = param_ranges(d, base_w, base_scale, level_w, level_scale, ins);
-        ins[ni++] = {workspace, need};
-        Range outs[2 + 2 * kMaxLevels];
-        const int no = param_ranges(d, d_base_w, d_base_scale, (const float* const*)d_level_w,
-                                    (const float* const*)d_level_scale, outs);
-        if (any_overlap(outs, no, ins, ni)) return WTCONV_ERR_ALIAS;
-    }
-    wtc::ReduceArgs r;
-    memset(&r, 0, sizeof(r));
-    r.partial = reinterpret_cast<const float*>(workspace);
-    r.nchunks = pl.nchunks;
-    r.C = d.C;
-    r.k = d.k;
-    r.L = d.L;
-    fill_params(r.p, d.L, base_w, base_scale, level_w, level_scale);
-    r.dw0 = d_base_w;
-    r.ds0 = d_base_scale;
-    for (int l = 0; l < d.L; ++l) {
-        r.dlw[l] = d_level_w[l];
-        r.dls[l] = d_level_scale[l];
-    }
-    const hipError_t e = wtc::launch_reduce(r, stream);
-    return e == hipSuccess ? WTCONV_OK : WTCONV_ERR_HIP;
+    const size_t need = forward_ws(d);
+    if ((st = check_workspace(need, workspace, workspace_bytes)) != WTCONV_OK) return st;
+    const size_t bytes = (size_t)d.B * d.C * d.H * d.W * elem_size(d.dtype);
+    if (overlaps(x, bytes, y, bytes)) return WTCONV_ERR_ALIAS;
+    if (need && (overlaps(workspace, need, x, bytes) || overlaps(workspace, need, y, bytes)))
+        return WTCONV_ERR_ALIAS;
+    wtc::ParamPtrs p;
+    fill_params(p, d.L, base_w, base_scale, level_w, level_scale);
+    return forward_impl(d, x, p, y, reinterpret_cast<char*>(workspace), 0, stream);
 }
 
-}  // namespace
+size_t wtconv_backward_workspace_bytes(const wtconv_desc* desc)
+{
+    if (check_desc(desc) != WTCONV_OK) return 0;
+    const size_t n = backward_ws(*desc);
+    return n == kUnsupported ? 0 : n;
+}
 
 wtconv_status wtconv_backward_partials(const wtconv_desc* desc, const void* x, const void* dy,
                                        const float* base_w, const float* base_scale,
@@ -406,8 +621,13 @@ wtconv_status wtconv_backward_partials(const wtconv_desc* desc, const void* x, c
                                        void* dx, void* workspace, size_t workspace_bytes,
                                        hipStream_t stream)
 {
-    return partials_impl(desc, x, dy, base_w, base_scale, level_w, level_scale, dx, workspace, workspace_bytes,
-                         stream, nullptr, nullptr, 0);
+    size_t need = 0;
+    const wtconv_status st = backward_checks(desc, x, dy, base_w, base_scale, level_w, level_scale, dx, workspace,
+                                             workspace_bytes, nullptr, 0, &need);
+    if (st != WTCONV_OK) return st;
+    wtc::ParamPtrs p;
+    fill_params(p, desc->L, base_w, base_scale, level_w, level_scale);
+    return partials_impl(*desc, x, dy, p, dx, reinterpret_cast<char*>(workspace), 0, stream);
 }
 
 wtconv_status wtconv_backward_finalize(const wtconv_desc* desc, const float* base_w, const float* base_scale,
@@ -416,8 +636,27 @@ wtconv_status wtconv_backward_finalize(const wtconv_desc* desc, const float* bas
                                        float* const* d_level_scale, const void* workspace,
                                        size_t workspace_bytes, hipStream_t stream)
 {
-    return finalize_impl(desc, base_w, base_scale, level_w, level_scale, d_base_w, d_base_scale, d_level_w,
-                         d_level_scale, workspace, workspace_bytes, stream, false);
+    wtconv_status st = check_desc(desc);
+    if (st != WTCONV_OK) return st;
+    const wtconv_desc& d = *desc;
+    if (!base_w || !base_scale || !d_base_w || !d_base_scale) return WTCONV_ERR_NULL;
+    if ((st = check_levels(d.L, level_w, level_scale)) != WTCONV_OK) return st;
+    if ((st = check_levels(d.L, (const float* const*)d_level_w, (const float* const*)d_level_scale)) != WTCONV_OK)
+        return st;
+    const size_t need = backward_ws(d);
+    if ((st = check_workspace(need, workspace, workspace_bytes)) != WTCONV_OK) return st;
+    if (need == 0) return WTCONV_ERR_WORKSPACE;
+    Range ins[3 + 2 * kMaxLevels];
+    int ni = param_ranges(d, base_w, base_scale, level_w, level_scale, ins);
+    ins[ni++] = {workspace, need};
+    Range outs[2 + 2 * kMaxLevels];
+    const int no = param_ranges(d, d_base_w, d_base_scale, (const float* const*)d_level_w,
+                                (const float* const*)d_level_scale, outs);
+    if (any_overlap(outs, no, ins, ni)) return WTCONV_ERR_ALIAS;
+    wtc::ParamPtrs p;
+    fill_params(p, d.L, base_w, base_scale, level_w, level_scale);
+    return finalize_impl(d, p, grads_of(d.L, d_base_w, d_base_scale, d_level_w, d_level_scale),
+                         reinterpret_cast<const char*>(workspace), 0, stream);
 }
 
 wtconv_status wtconv_backward(const wtconv_desc* desc, const void* x, const void* dy,
@@ -439,11 +678,16 @@ wtconv_status wtconv_backward(const wtconv_desc* desc, const void* x, const void
     Range grads[2 + 2 * kMaxLevels];
     const int ng = param_ranges(d, d_base_w, d_base_scale, (const float* const*)d_level_w,
                                 (const float* const*)d_level_scale, grads);
-    st = partials_impl(desc, x, dy, base_w, base_scale, level_w, level_scale, dx, workspace, workspace_bytes,
-                       stream, nullptr, grads, ng);
+    size_t need = 0;
+    st = backward_checks(desc, x, dy, base_w, base_scale, level_w, level_scale, dx, workspace, workspace_bytes,
+                         grads, ng, &need);
     if (st != WTCONV_OK) return st;
-    return finalize_impl(desc, base_w, base_scale, level_w, level_scale, d_base_w, d_base_scale, d_level_w,
-                         d_level_scale, workspace, workspace_bytes, stream, true);
+    wtc::ParamPtrs p;
+    fill_params(p, d.L, base_w, base_scale, level_w, level_scale);
+    char* ws = reinterpret_cast<char*>(workspace);
+    st = partials_impl(d, x, dy, p, dx, ws, 0, stream);
+    if (st != WTCONV_OK) return st;
+    return finalize_impl(d, p, grads_of(d.L, d_base_w, d_base_scale, d_level_w, d_level_scale), ws, 0, stream);
 }
 
 }  // extern "C"

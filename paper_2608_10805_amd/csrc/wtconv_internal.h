@@ -68,12 +68,35 @@ struct FusedArgs {
     int vec_ok;          // 1 if plane bases allow 16-byte (f32) / 8-byte (16-bit) vector access
     int lds_floats;      // dynamic LDS of the workgroup, in floats
     int one_round;       // 1 if every level is filtered in a single register-tile round
+    int skip_base;       // 1: no base path and no base-kernel gradient (coarse sub-problem)
+    // Region mode (planes too large for LDS): each workgroup processes an
+    // rg_T x rg_T output tile of a real_H x real_W plane through a region with
+    // a halo of rg_h pixels on every side; g describes the region. `carry` is
+    // the level-1 contribution of the coarser levels ([B][C][carry_H][carry_W]).
+    int rg_ntx, rg_nty;  // tiles per plane row / column
+    int rg_T, rg_h;
+    int real_H, real_W;
+    float rg_r_itx;      // 1 / (rg_T / 4): inner output tiles per tile row
+    float rg_r_itiles;   // 1 / (rg_T / 4)^2
+    const float* carry;
+    int carry_H, carry_W;
     PlaneGeom g;
+};
+
+// Level-1 raw LL carrier of every plane: out = (a + b + c + d) / 2 per 2x2
+// block of the zero-extended input, an fp32 [planes][H1][W1] array.
+struct CarrierArgs {
+    const void* in;
+    float* out;
+    long planes;
+    int H, W, H1, W1;
+    int vec_ok;
 };
 
 struct ReduceArgs {
     const float* partial;
     int nchunks, C, k, L;
+    int skip_base;  // do not write the base gradients
     ParamPtrs p;
     float* dw0;
     float* ds0;
@@ -88,5 +111,6 @@ inline int partial_floats_per_channel(int k, int L) { return k * k * (1 + 4 * L)
 hipError_t launch_forward(int k, wtconv_dtype dt, const FusedArgs& a, int grid, hipStream_t s);
 hipError_t launch_backward(int k, wtconv_dtype dt, const FusedArgs& a, int grid, hipStream_t s);
 hipError_t launch_reduce(const ReduceArgs& a, hipStream_t s);
+hipError_t launch_carrier(wtconv_dtype dt, const CarrierArgs& a, hipStream_t s);
 
 }  // namespace wtc

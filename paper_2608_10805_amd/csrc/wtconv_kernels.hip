@@ -170,11 +170,12 @@ DEV void butterfly(float a, float b, float c, float d, float (&o)[4])
 //    Pixels outside the plane are zero (zero extension). Ragged sites beyond
 //    the level grids are written as the zeros they are.
 // ----------------------------------------------------------------------------
+// A 4x4 pixel block whose top-left pixel is (y0, x0) of an H x W plane; pixels
+// outside the plane (including negative coordinates) read as zero.
 template <typename T>
-DEV void fetch_block(const T* __restrict__ src, const PlaneGeom& g, int y0, int x0, bool vec, float (&v)[4][4])
+DEV void fetch_block(const T* __restrict__ src, int H, int W, int y0, int x0, bool vec, float (&v)[4][4])
 {
-    const int H = g.H, W = g.W;
-    if (vec && y0 + 4 <= H) {  // vec implies W % 4 == 0: the 4 columns are inside
+    if (vec && y0 >= 0 && x0 >= 0 && y0 + 4 <= H && x0 + 4 <= W) {  // vec: W % 4 == 0 and x0 % 4 == 0
 #pragma unroll
         for (int r = 0; r < 4; ++r) load4(src + (long)(y0 + r) * W + x0, v[r]);
     } else {
@@ -183,7 +184,7 @@ DEV void fetch_block(const T* __restrict__ src, const PlaneGeom& g, int y0, int 
 #pragma unroll
             for (int c = 0; c < 4; ++c) {
                 const int y = y0 + r, x = x0 + c;
-                v[r][c] = (y < H && x < W) ? to_f32(src[(long)y * W + x]) : 0.f;
+                v[r][c] = (y >= 0 && y < H && x >= 0 && x < W) ? to_f32(src[(long)y * W + x]) : 0.f;
             }
     }
 }
@@ -228,7 +229,7 @@ DEV void load_block(const T* __restrict__ src, float* __restrict__ reg, const Pl
                     bool vec)
 {
     float v[4][4];
-    fetch_block<T>(src, g, y0, x0, vec, v);
+    fetch_block<T>(src, g.H, g.W, y0, x0, vec, v);
     store_block<K>(v, reg, g, y0, x0);
 }
 
@@ -434,9 +435,15 @@ DEV void filter_band(float* region0, const float* aux0, int stride, const LevelG
 
 // Kernel-gradient correlation of one subband over all resident planes with
 // tiles: acc += sum over sites of dZ(site) * Y(site + tap offset).
+// Sites counted by a kernel-gradient correlation: [m0, m1) in both grid
+// directions (region mode counts only its own tile's sites; otherwise all).
+struct SiteMask {
+    int m0, m1;
+};
+
 template <int K, int T>
 DEV void corr_band_tiles(const float* __restrict__ dz0, const float* __restrict__ y0, int stride,
-                         const LevelGeom& lg, int q, int np, float (&acc)[K * K], int lane)
+                         const LevelGeom& lg, int q, int np, float (&acc)[K * K], int lane, SiteMask mk)
 {
     const int tx = lg.ew / T;
     const int per = tx * (lg.eh / T);
@@ -446,20 +453,27 @@ DEV void corr_band_tiles(const float* __restrict__ dz0, const float* __restrict_
         const int boff = ti.p * stride + lg.off + q * lg.band;
         float ctr[T][T];
         load_center<K, T>(dz0 + boff, lg.pitch, ti.j0, ti.i0, ctr);
+#pragma unroll
+        for (int oy = 0; oy < T; ++oy)
+#pragma unroll
+            for (int ox = 0; ox < T; ++ox) {
+                const int j = ti.j0 + oy, i = ti.i0 + ox;
+                if (j < mk.m0 || j >= mk.m1 || i < mk.m0 || i >= mk.m1) ctr[oy][ox] = 0.f;
+            }
         corr_tile<K, T>(y0 + boff, lg.pitch, ti.j0, ti.i0, ctr, acc);
     }
 }
 
 template <int K>
 DEV void corr_band(const float* dz0, const float* y0, int stride, const LevelGeom& lg, int q, int np,
-                   float (&acc)[K * K], int lane)
+                   float (&acc)[K * K], int lane, SiteMask mk)
 {
     if (lg.T == 4)
-        corr_band_tiles<K, 4>(dz0, y0, stride, lg, q, np, acc, lane);
+        corr_band_tiles<K, 4>(dz0, y0, stride, lg, q, np, acc, lane, mk);
     else if (lg.T == 2)
-        corr_band_tiles<K, 2>(dz0, y0, stride, lg, q, np, acc, lane);
+        corr_band_tiles<K, 2>(dz0, y0, stride, lg, q, np, acc, lane, mk);
     else
-        corr_band_tiles<K, 1>(dz0, y0, stride, lg, q, np, acc, lane);
+        corr_band_tiles<K, 1>(dz0, y0, stride, lg, q, np, acc, lane, mk);
 }
 
 // Kernel-gradient correlation of one coarse subband, by rows: lane (tap row p,
@@ -532,12 +546,12 @@ DEV void corr_band_rows(const float* __restrict__ dz0, const float* __restrict__
 // level fits a single register-tile round.
 template <int K, bool ONE>
 DEV void grad_and_filter(float* side_in, const float* side_aux, int stride, const LevelGeom& lg, int q, int np,
-                         const float (&w)[K * K], float (&gl)[K * K], bool have_out, int lane)
+                         const float (&w)[K * K], float (&gl)[K * K], bool have_out, int lane, SiteMask mk)
 {
     if (ONE && have_out) {
         filter_band<K, ONE, true>(side_in, side_aux, stride, lg, q, np, w, gl, lane);
     } else {
-        corr_band<K>(side_in, side_aux, stride, lg, q, np, gl, lane);
+        corr_band<K>(side_in, side_aux, stride, lg, q, np, gl, lane, mk);
         if (have_out) filter_band<K, ONE, false>(side_in, side_aux, stride, lg, q, np, w, gl, lane);
     }
 }
@@ -584,8 +598,17 @@ DEV void base_tile(const float* __restrict__ xa, int xpitch, int y0, int x0, con
 // per 2x2 quadrant; level 1 has a tuple per quadrant and a sign pair per pixel.
 // Because the LL term of every level enters with sign +, the coarser levels'
 // sum for a quadrant is simply added to that quadrant's level-1 LL.
+// `carry` (nullable) is the coarser levels' contribution at the level-1 grid,
+// in orthonormal units: it enters each level-1 LL with the factor 1/2 of one
+// synthesis step; (cy, cx) is the tile's first level-1 site in it.
+struct Carry {
+    const float* p;
+    int H, W, cy, cx;
+};
+
 template <int K>
-DEV void synth_tile(const float* __restrict__ reg, const PlaneGeom& g, int y0, int x0, float (&acc)[4][4])
+DEV void synth_tile(const float* __restrict__ reg, const PlaneGeom& g, int y0, int x0, float (&acc)[4][4],
+                    const Carry& cr)
 {
     constexpr int R = K / 2;
     const int L = g.L;
@@ -613,6 +636,15 @@ DEV void synth_tile(const float* __restrict__ reg, const PlaneGeom& g, int y0, i
     } else {
         quad[0][0] = quad[0][1] = quad[1][0] = quad[1][1] = coarse;
     }
+    if (cr.p) {
+#pragma unroll
+        for (int a = 0; a < 2; ++a)
+#pragma unroll
+            for (int b = 0; b < 2; ++b) {
+                const int j = cr.cy + a, i = cr.cx + b;
+                if (j < cr.H && i < cr.W) quad[a][b] += 0.5f * cr.p[(long)j * cr.W + i];
+            }
+    }
     const LevelGeom& lg = g.lv[1];
 #pragma unroll
     for (int a = 0; a < 2; ++a)
@@ -634,7 +666,7 @@ DEV void store_tile(T* __restrict__ plane, int H, int W, int y0, int x0, const f
 #pragma unroll
     for (int oy = 0; oy < 4; ++oy) {
         const int y = y0 + oy;
-        if (y >= H) break;
+        if (y >= H || x0 >= W) break;
         T* row = plane + (long)y * W + x0;
         if (vec && x0 + 4 <= W) {
             if constexpr (sizeof(T) == 4) {
@@ -678,22 +710,29 @@ DEV void fetch_weights(const float* __restrict__ wtab, int row, bool rot, int la
 // ----------------------------------------------------------------------------
 // the fused kernel
 // ----------------------------------------------------------------------------
-template <int K, typename ST, bool BWD, bool ONE>
+template <int K, typename ST, bool BWD, bool ONE, bool RGN>
 __global__ void __launch_bounds__(kThreads) fused_kernel(const FusedArgs a)
 {
     constexpr int R = K / 2, KK = K * K;
     extern __shared__ float4 lds4[];
     float* lds = reinterpret_cast<float*>(lds4);
 
-    const PlaneGeom& g = a.g;
+    const PlaneGeom& g = a.g;  // the plane (or, in region mode, the region) held on chip
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int C = a.C;
     const int c = blockIdx.x % C;
-    const int chunk = blockIdx.x / C;
+    const int ntiles = RGN ? a.rg_ntx * a.rg_nty : 1;
+    const int chunk = (blockIdx.x / C) / ntiles;
+    const int tile = (blockIdx.x / C) - chunk * ntiles;
     const int b_begin = chunk * a.nb;
     const int b_end = min(a.B, b_begin + a.nb);
     const int L = g.L;
-    const long HW = (long)g.H * g.W;
+    // region mode: origin of the region in the real plane (multiples of 4)
+    const int oy = RGN ? (tile / a.rg_ntx) * a.rg_T - a.rg_h : 0;
+    const int ox = RGN ? (tile % a.rg_ntx) * a.rg_T - a.rg_h : 0;
+    const int PH = RGN ? a.real_H : g.H, PW = RGN ? a.real_W : g.W;  // the real plane
+    const long HW = (long)PH * PW;
+    const bool skip_base = a.skip_base != 0;
 
     // LDS: [folded weights][coarse kernel-gradient sums (backward)][planes]
     const int wt_floats = ceil4c((1 + 4 * L) * KK);
@@ -731,7 +770,7 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(const FusedArgs a)
     ST* out = reinterpret_cast<ST*>(a.out);
     const bool have_out = out != nullptr;
     const bool vec_ok = a.vec_ok != 0;
-    const bool vec_store = vec_ok && (g.W % 4) == 0;
+    const bool vec_store = vec_ok && (PW % 4) == 0;
     const bool vec_load = vec_store;
     const int q = wave;  // the subband this wavefront filters
 
@@ -744,9 +783,13 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(const FusedArgs a)
             for (int it = tid; it < np * per; it += kThreads) {
                 const TileIdx ti = tile_at(it, per, g.r_tiles, tx, g.r_tiles_x, 4);
                 const long plane = (long)(b0 + ti.p) * C + c;
-                load_block<K, ST>(in + plane * HW, side_in + ti.p * stride, g, ti.j0, ti.i0, vec_load);
-                if constexpr (BWD)
-                    load_block<K, ST>(aux + plane * HW, side_aux + ti.p * stride, g, ti.j0, ti.i0, vec_load);
+                float v[4][4];
+                fetch_block<ST>(in + plane * HW, PH, PW, oy + ti.j0, ox + ti.i0, vec_load, v);
+                store_block<K>(v, side_in + ti.p * stride, g, ti.j0, ti.i0);
+                if constexpr (BWD) {
+                    fetch_block<ST>(aux + plane * HW, PH, PW, oy + ti.j0, ox + ti.i0, vec_load, v);
+                    store_block<K>(v, side_aux + ti.p * stride, g, ti.j0, ti.i0);
+                }
             }
         }
         __syncthreads();
@@ -770,12 +813,14 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(const FusedArgs a)
             float w[KK];
             fetch_weights<K>(wtab, wrow(l, q), BWD, lane, w);
             if constexpr (BWD) {
+                // region mode counts only the sites of its own tile
+                const SiteMask mk = RGN ? SiteMask{a.rg_h >> l, (a.rg_h + a.rg_T) >> l} : SiteMask{0, 1 << 30};
                 if (l <= reg_levels<ONE>()) {
                     // static choice of the accumulator array keeps it in registers
                     if (l == 1)
-                        grad_and_filter<K, ONE>(side_in, side_aux, stride, lg, q, np, w, g1, have_out, lane);
+                        grad_and_filter<K, ONE>(side_in, side_aux, stride, lg, q, np, w, g1, have_out, lane, mk);
                     else
-                        grad_and_filter<K, ONE>(side_in, side_aux, stride, lg, q, np, w, g2, have_out, lane);
+                        grad_and_filter<K, ONE>(side_in, side_aux, stride, lg, q, np, w, g2, have_out, lane, mk);
                 } else {
                     corr_band_rows<K>(side_in, side_aux, stride, lg, q, np, gco + ((l - 1) * 4 + q) * KK, lane);
                     if (have_out) filter_band<K, ONE, false>(side_in, side_aux, stride, lg, q, np, w, g1, lane);
@@ -786,24 +831,47 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(const FusedArgs a)
         }
         __syncthreads();
 
-        // 4. output tiles
+        // 4. output tiles (region mode: the tiles of the region's inner rg_T x rg_T square)
         {
             float w[KK];
             fetch_weights<K>(wtab, 0, BWD, lane, w);
-            const int tx = g.tiles_x, per = g.tiles_x * g.tiles_y;
+            const int tx = RGN ? a.rg_T / 4 : g.tiles_x;
+            const int per = RGN ? tx * tx : g.tiles_x * g.tiles_y;
             for (int it = tid; it < np * per; it += kThreads) {
-                const TileIdx ti = tile_at(it, per, g.r_tiles, tx, g.r_tiles_x, 4);
+                TileIdx ti = RGN ? tile_at(it, per, a.rg_r_itiles, tx, a.rg_r_itx, 4)
+                                 : tile_at(it, per, g.r_tiles, tx, g.r_tiles_x, 4);
+                if (RGN) {
+                    ti.j0 += a.rg_h;
+                    ti.i0 += a.rg_h;
+                }
                 const float* reg = side_in + ti.p * stride;
+                const long plane = (long)(b0 + ti.p) * C + c;
                 float acc[4][4], ctr[4][4];
                 if (!BWD || have_out) {
-                    base_tile<K>(reg, g.xpitch, ti.j0, ti.i0, w, acc, ctr);
-                    synth_tile<K>(reg, g, ti.j0, ti.i0, acc);
-                    const long plane = (long)(b0 + ti.p) * C + c;
-                    store_tile<ST>(out + plane * HW, g.H, g.W, ti.j0, ti.i0, acc, vec_store);
-                } else {
+                    if (skip_base) {
+#pragma unroll
+                        for (int oy2 = 0; oy2 < 4; ++oy2)
+#pragma unroll
+                            for (int ox2 = 0; ox2 < 4; ++ox2) acc[oy2][ox2] = 0.f;
+                    } else {
+                        base_tile<K>(reg, g.xpitch, ti.j0, ti.i0, w, acc, ctr);
+                    }
+                    Carry cr = {nullptr, 0, 0, 0, 0};
+                    if (RGN && a.carry) {
+                        cr.p = a.carry + plane * a.carry_H * a.carry_W;
+                        cr.H = a.carry_H;
+                        cr.W = a.carry_W;
+                        cr.cy = (oy + ti.j0) >> 1;
+                        cr.cx = (ox + ti.i0) >> 1;
+                    }
+                    synth_tile<K>(reg, g, ti.j0, ti.i0, acc, cr);
+                    store_tile<ST>(out + plane * HW, PH, PW, oy + ti.j0, ox + ti.i0, acc, vec_store);
+                } else if (!skip_base) {
                     load_center<K, 4>(reg, g.xpitch, ti.j0, ti.i0, ctr);
                 }
-                if constexpr (BWD) corr_tile<K, 4>(side_aux + ti.p * stride, g.xpitch, ti.j0, ti.i0, ctr, g0);
+                if constexpr (BWD) {
+                    if (!skip_base) corr_tile<K, 4>(side_aux + ti.p * stride, g.xpitch, ti.j0, ti.i0, ctr, g0);
+                }
             }
         }
         __syncthreads();
@@ -825,7 +893,7 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(const FusedArgs a)
             }
         }
         __syncthreads();
-        float* dst = a.partial + ((long)chunk * C + c) * NP;
+        float* dst = a.partial + ((long)(chunk * ntiles + tile) * C + c) * NP;
         for (int t = tid; t < KK; t += kThreads)
             dst[t] = ((red[t] + red[KK + t]) + red[2 * KK + t]) + red[3 * KK + t];
         // register-held levels: band q's sums came from wavefront q
@@ -846,6 +914,7 @@ __global__ void __launch_bounds__(64) reduce_kernel(const ReduceArgs a)
     const int c = blockIdx.x;
     const int band = blockIdx.y;  // 0 = base, else 1 + (l-1)*4 + q
     const int t = threadIdx.x;
+    if (band == 0 && a.skip_base) return;
     float scale, norm;
     const float* w;
     float* dw;
@@ -879,21 +948,43 @@ __global__ void __launch_bounds__(64) reduce_kernel(const ReduceArgs a)
     if (t == 0) *ds = prod;
 }
 
-template <int K, typename ST, bool BWD, bool ONE>
+template <int K, typename ST, bool BWD, bool ONE, bool RGN>
 hipError_t launch_variant(const FusedArgs& a, int grid, hipStream_t s)
 {
     const size_t bytes = (size_t)a.lds_floats * sizeof(float);
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&fused_kernel<K, ST, BWD, ONE>),
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&fused_kernel<K, ST, BWD, ONE, RGN>),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((fused_kernel<K, ST, BWD, ONE>), dim3(grid), dim3(kThreads), bytes, s, a);
+    hipLaunchKernelGGL((fused_kernel<K, ST, BWD, ONE, RGN>), dim3(grid), dim3(kThreads), bytes, s, a);
     return hipGetLastError();
 }
 
 template <int K, typename ST, bool BWD>
 hipError_t launch_one(const FusedArgs& a, int grid, hipStream_t s)
 {
-    return a.one_round ? launch_variant<K, ST, BWD, true>(a, grid, s) : launch_variant<K, ST, BWD, false>(a, grid, s);
+    if (a.rg_ntx > 0) return launch_variant<K, ST, BWD, false, true>(a, grid, s);
+    return a.one_round ? launch_variant<K, ST, BWD, true, false>(a, grid, s)
+                       : launch_variant<K, ST, BWD, false, false>(a, grid, s);
+}
+
+// Level-1 raw LL carrier: one thread per level-1 site.
+template <typename T>
+__global__ void __launch_bounds__(256) carrier_kernel(const CarrierArgs a)
+{
+    const long n = a.planes * a.H1 * a.W1;
+    const T* in = reinterpret_cast<const T*>(a.in);
+    for (long e = blockIdx.x * 256L + threadIdx.x; e < n; e += (long)gridDim.x * 256) {
+        const long p = e / ((long)a.H1 * a.W1);
+        const int r = (int)(e - p * a.H1 * a.W1);
+        const int j = r / a.W1, i = r - (r / a.W1) * a.W1;
+        const T* src = in + p * a.H * a.W;
+        const int y = 2 * j, x = 2 * i;
+        const float v00 = to_f32(src[(long)y * a.W + x]);
+        const float v01 = x + 1 < a.W ? to_f32(src[(long)y * a.W + x + 1]) : 0.f;
+        const float v10 = y + 1 < a.H ? to_f32(src[(long)(y + 1) * a.W + x]) : 0.f;
+        const float v11 = (x + 1 < a.W && y + 1 < a.H) ? to_f32(src[(long)(y + 1) * a.W + x + 1]) : 0.f;
+        a.out[e] = 0.5f * ((v00 + v01) + (v10 + v11));
+    }
 }
 
 template <bool BWD>
@@ -927,6 +1018,18 @@ hipError_t launch_forward(int k, wtconv_dtype dt, const FusedArgs& a, int grid, 
 hipError_t launch_backward(int k, wtconv_dtype dt, const FusedArgs& a, int grid, hipStream_t s)
 {
     return dispatch<true>(k, dt, a, grid, s);
+}
+
+hipError_t launch_carrier(wtconv_dtype dt, const CarrierArgs& a, hipStream_t s)
+{
+    const long n = a.planes * a.H1 * a.W1;
+    const int grid = (int)((n + 255) / 256 < 65536 ? (n + 255) / 256 : 65536);
+    switch (dt) {
+        case WTCONV_F32: hipLaunchKernelGGL(carrier_kernel<float>, dim3(grid), dim3(256), 0, s, a); break;
+        case WTCONV_BF16: hipLaunchKernelGGL(carrier_kernel<uint16_t>, dim3(grid), dim3(256), 0, s, a); break;
+        case WTCONV_F16: hipLaunchKernelGGL(carrier_kernel<_Float16>, dim3(grid), dim3(256), 0, s, a); break;
+    }
+    return hipGetLastError();
 }
 
 hipError_t launch_reduce(const ReduceArgs& a, hipStream_t s)

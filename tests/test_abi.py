@@ -41,13 +41,13 @@ def test_status_strings():
     assert binding.status_string(99) == "unknown status"
 
 
-def fwd(desc, x=FAKE, bw=FAKE + 4096, bs=FAKE + 8192, lw=None, ls=None, y=FAKE + (1 << 36)):
+def fwd(desc, x=FAKE, bw=FAKE + 4096, bs=FAKE + 8192, lw=None, ls=None, y=FAKE + (1 << 36), ws=None, ws_bytes=0):
     L = desc.L if desc is not None else 0
     lw = [FAKE + 16384 + 64 * i for i in range(L)] if lw is None else lw
     ls = [FAKE + 32768 + 64 * i for i in range(L)] if ls is None else ls
     lib = binding.load()
     return lib.wtconv_forward(ctypes.byref(desc) if desc is not None else None, x, bw, bs,
-                              binding._ptr_array(lw), binding._ptr_array(ls), y, None)
+                              binding._ptr_array(lw), binding._ptr_array(ls), y, ws, ctypes.c_size_t(ws_bytes), None)
 
 
 @pytest.mark.parametrize("shape,code", [
@@ -71,7 +71,7 @@ def test_forward_rejects_nulls():
     assert fwd(d, bw=None) == 1
     assert fwd(d, bs=None) == 1
     lib = binding.load()
-    assert lib.wtconv_forward(ctypes.byref(d), FAKE, FAKE, FAKE, None, None, FAKE + (1 << 36), None) == 1
+    assert lib.wtconv_forward(ctypes.byref(d), FAKE, FAKE, FAKE, None, None, FAKE + (1 << 36), None, 0, None) == 1
     assert fwd(d, lw=[FAKE, 0]) == 1
 
 
@@ -81,9 +81,29 @@ def test_forward_rejects_alias():
     assert fwd(d, x=FAKE + 64, y=FAKE) == 6
 
 
-def test_forward_rejects_unsupported_plane():
-    # a 512 x 512 fp32 plane plus its pyramid cannot be resident in 160 KB of LDS
-    assert fwd(make_desc(1, 1, 512, 512, 5, 3)) == 8
+def test_forward_workspace_query():
+    # planes that fit one compute unit's LDS need no forward workspace
+    assert binding.wtconv_forward_workspace_bytes(make_desc(64, 96, 56, 56, 5, 3)) == 0
+    assert binding.wtconv_forward_workspace_bytes(make_desc(1, 1, 8, 8, 4, 1)) == 0
+    assert binding.load().wtconv_forward_workspace_bytes(None) == 0
+    # large planes: the level-1 carrier and the coarse output live in the workspace
+    n = binding.wtconv_forward_workspace_bytes(make_desc(16, 64, 224, 224, 5, 3))
+    assert n >= 2 * 16 * 64 * 112 * 112 * 4 and n % 256 == 0
+    # a single Haar level (or none) needs no carrier
+    assert binding.wtconv_forward_workspace_bytes(make_desc(16, 64, 224, 224, 5, 1)) == 0
+    assert binding.wtconv_forward_workspace_bytes(make_desc(16, 64, 224, 224, 5, 0)) == 0
+
+
+def test_forward_large_plane_workspace_checks():
+    d = make_desc(1, 1, 512, 512, 5, 3)
+    need = binding.wtconv_forward_workspace_bytes(d)
+    assert need > 0
+    ws = FAKE + (1 << 38)
+    assert fwd(d) == 7                                       # no workspace
+    assert fwd(d, ws=ws, ws_bytes=need - 1) == 7             # too small
+    assert fwd(d, ws=ws + 4, ws_bytes=need) == 7             # misaligned
+    assert fwd(d, ws=FAKE + 64, ws_bytes=need) == 6          # overlaps x
+    assert fwd(d, ws=FAKE + (1 << 36) - 16, ws_bytes=need) == 6  # overlaps y
 
 
 def bwd(desc, ws=FAKE + (1 << 38), ws_bytes=1 << 30, dx=FAKE + (1 << 37), **kw):
@@ -105,6 +125,9 @@ def test_backward_workspace_query():
     d = make_desc(64, 96, 56, 56, 5, 3)
     n = binding.wtconv_backward_workspace_bytes(d)
     assert n > 0 and n % 256 == 0
+    # large planes add the level-1 carriers of x and dy and the coarse dx
+    big = binding.wtconv_backward_workspace_bytes(make_desc(16, 64, 224, 224, 5, 3))
+    assert big >= 3 * 16 * 64 * 112 * 112 * 4 and big % 256 == 0
     assert binding.wtconv_backward_workspace_bytes(make_desc(1, 1, 8, 8, 4, 1)) == 0
     assert binding.load().wtconv_backward_workspace_bytes(None) == 0
 

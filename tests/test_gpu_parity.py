@@ -211,12 +211,51 @@ def test_autograd_module_matches_binding():
         assert rel_err(to_np(m.level_scale[l].grad), ref["d_level_scale"][l]) < 1e-5
 
 
-def test_large_plane_reports_unsupported():
-    """Planes whose working set exceeds one compute unit's LDS are rejected with
-    WTCONV_ERR_UNSUPPORTED (no silent fallback)."""
-    from paper_2608_10805_amd.binding import WTConvError
+# Planes whose working set does not fit one compute unit's LDS take the split
+# path: the coarse levels run on the level-1 carrier (recursively, if that is
+# still too large) and the base path plus level 1 run on halo tiles. Every
+# element is checked; the cases cover a split in the backward pass only, in
+# both passes, k = 1 (no halo), k = 7, L = 0 and 1 (no carrier), a two-deep
+# recursion, ragged tiles and 16-bit storage.
+LARGE = [
+    (2, 2, 100, 100, 5, 3, "f32"),
+    (1, 2, 130, 126, 5, 3, "f32"),
+    (1, 3, 130, 70, 1, 2, "f32"),
+    (2, 3, 90, 90, 7, 1, "f32"),
+    (1, 2, 150, 130, 3, 0, "f32"),
+    (1, 2, 224, 224, 5, 5, "f32"),
+    (1, 1, 300, 300, 7, 4, "f32"),
+    (1, 2, 190, 170, 5, 4, "f32"),
+    (1, 2, 224, 224, 5, 3, "bf16"),
+    (1, 2, 190, 170, 5, 4, "f16"),
+]
 
-    inp, dev = setup(1, 1, 224, 224, 5, 5, "f32")
-    with pytest.raises(WTConvError) as ei:
-        dev.backward()
-    assert ei.value.status == 8
+
+@pytest.mark.parametrize("B,C,H,W,k,L,dtype", LARGE)
+def test_large_plane_forward(B, C, H, W, k, L, dtype):
+    check_forward(B, C, H, W, k, L, dtype)
+
+
+@pytest.mark.parametrize("B,C,H,W,k,L,dtype", LARGE)
+def test_large_plane_backward(B, C, H, W, k, L, dtype):
+    check_backward(B, C, H, W, k, L, dtype)
+
+
+def test_large_plane_backward_without_dx():
+    check_backward(2, 2, 100, 100, 5, 3, "f32", need_dx=False)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("L", [1, 2, 3, 4, 5])
+def test_large_224_fwdbwd_full(L, dtype):
+    """B=16 C=64 224x224, k=5, L sweep (the large entry of the shape sweep)."""
+    check_full_size(16, 64, 224, 224, 5, L, dtype, backward=True, n_planes=6, n_channels=2)
+
+
+def test_large_plane_determinism_bitwise():
+    inp, dev = setup(2, 3, 150, 150, 5, 3, "f32", seed=5)
+    y1, y2 = dev.forward(), dev.forward()
+    assert torch.equal(y1, y2)
+    g1, g2 = dev.backward(), dev.backward()
+    for a, b in zip([g1[0], g1[1], g1[2]] + g1[3] + g1[4], [g2[0], g2[1], g2[2]] + g2[3] + g2[4]):
+        assert torch.equal(a, b)
