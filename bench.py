@@ -46,15 +46,109 @@ def parse():
                     help="only run a plain device-to-device copy of this many MiB (profiler counter calibration)")
     ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "hbm_traffic_wtconv_convnext_t_stage1.txt"),
                     help="counter summary with the measured HBM bytes of the dominant kernel")
+    ap.add_argument("--no-config-table", action="store_true",
+                    help="skip the per-configuration fwd / fwd+bwd timing table")
+    ap.add_argument("--table-steps", type=int, default=10)
     return ap.parse_args()
+
+
+# Every benchmarked configuration of the operator (fwd and fwd+bwd timed for each):
+# (name, B, C, H, W, k, L, dtype)
+def table_configs():
+    out = [("small_fwd", 2, 16, 32, 32, 5, 1, "f32"),
+           ("convnext_s1", 64, 96, 56, 56, 5, 3, "f32")]
+    out += [(f"convnext_s2_L{L}", 64, 192, 28, 28, 5, L, "f32") for L in range(1, 6)]
+    out += [("convnext_s1_bf16_L5", 128, 96, 56, 56, 5, 5, "bf16")]
+    for (B, C, H, W) in [(128, 96, 56, 56), (128, 192, 28, 28), (128, 384, 14, 14), (128, 768, 7, 7),
+                         (32, 128, 63, 95), (16, 64, 224, 224)]:
+        for dt in ("f32", "bf16"):
+            for L in (1, 3, 5):
+                out.append((f"sweep_{H}x{W}_c{C}_L{L}_{dt}", B, C, H, W, 5, L, dt))
+    return out
+
+
+def config_table(steps, dev):
+    """ms, algorithmic GB/s and roofline fractions of fwd and fwd+bwd for every
+    configuration. Timing-only inputs are drawn on the device (seeded, with the
+    distributions of the parity inputs); buffer sets rotate so that one step's
+    tensors do not stay in the 256 MB Infinity Cache."""
+    import torch
+
+    from paper_2608_10805_amd import binding, iomodel
+
+    tdt = {"f32": torch.float32, "bf16": torch.bfloat16, "f16": torch.float16}
+    gen = torch.Generator(device=dev)
+    rows = []
+    for name, B, C, H, W, k, L, dt in table_configs():
+        gen.manual_seed(0)
+        f32 = dict(device=dev, dtype=torch.float32)
+        bw = (torch.rand(C, k, k, generator=gen, **f32) * 0.4 - 0.2)
+        bs = torch.rand(C, generator=gen, **f32) + 0.5
+        lw = [torch.rand(4 * C, k, k, generator=gen, **f32) * 0.4 - 0.2 for _ in range(L)]
+        ls = [torch.rand(4 * C, generator=gen, **f32) * 0.15 + 0.05 for _ in range(L)]
+        act = B * C * H * W * iomodel.elem_bytes(dt)
+        nsets = max(1, min(8, -(-600 * 2 ** 20 // (4 * act))))
+        sets = []
+        for _ in range(nsets):
+            x = torch.randn(B, C, H, W, generator=gen, **f32).to(tdt[dt])
+            dy = torch.randn(B, C, H, W, generator=gen, **f32).to(tdt[dt])
+            sets.append((x, dy, torch.empty_like(x), torch.empty_like(x)))
+        fws = torch.empty(max(1, binding.wtconv_forward_workspace_bytes(
+            binding.make_desc(B, C, H, W, k, L, binding._dtype_code(sets[0][0])))), dtype=torch.uint8, device=dev)
+        bk = binding.Backward(sets[0][0], bw, bs, lw, ls, need_dx=True)
+
+        def run(n, with_bwd):
+            for i in range(n):
+                x, dy, y, dx = sets[i % nsets]
+                binding.forward(x, bw, bs, lw, ls, out=y, workspace=fws)
+                if with_bwd:
+                    bk.partials(x, dy, dx)
+                    bk.finalize()
+
+        res = {}
+        for with_bwd in (False, True):
+            run(3, with_bwd)
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            torch.cuda.synchronize()
+            a.record()
+            run(steps, with_bwd)
+            b.record()
+            torch.cuda.synchronize()
+            res[with_bwd] = a.elapsed_time(b) / steps
+        work = iomodel.single_pass_work(B, C, H, W, k, L, dt)
+        fwd_ms, fb_ms = res[False], res[True]
+        row = {"name": name, "B": B, "C": C, "H": H, "W": W, "k": k, "L": L, "dtype": dt,
+               "fwd_ms": round(fwd_ms, 4), "fwdbwd_ms": round(fb_ms, 4),
+               "fwd_GBps": round(work.bytes_fwd / (fwd_ms * 1e-3) / 1e9, 1),
+               "fwdbwd_GBps": round(work.bytes_fwdbwd / (fb_ms * 1e-3) / 1e9, 1)}
+        row["fwd_hbm_frac"] = round(row["fwd_GBps"] / iomodel.HBM_PEAK_GBPS, 4)
+        row["fwdbwd_hbm_frac"] = round(row["fwdbwd_GBps"] / iomodel.HBM_PEAK_GBPS, 4)
+        row["fwdbwd_fma_frac"] = round(iomodel.fma_floor_s(work.fma_fwdbwd) / (fb_ms * 1e-3), 4)
+        log(f"table: {name:28s} fwd {fwd_ms * 1e3:8.1f} us  fwd+bwd {fb_ms * 1e3:8.1f} us  "
+            f"{row['fwdbwd_GBps']:7.1f} GB/s  fma {row['fwdbwd_fma_frac']:.3f}")
+        rows.append(row)
+        del sets, bk, fws
+        torch.cuda.empty_cache()
+    return rows
+
+
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
 
 
 def cpu_baseline(inp, work_bytes, seconds):
     import oracle
 
     planes = WORKLOAD["B"] * WORKLOAD["C"]
-    log(f"cpu_baseline: float64 oracle fwd+bwd over the whole workload ({planes} planes), "
-        f"{oracle.num_threads()} threads")
+    threads = oracle.num_threads()
+    log(f"cpu_baseline: float64 oracle fwd+bwd over the whole workload ({planes} planes), {threads} threads")
     reps, t0 = 0, time.perf_counter()
     while True:
         oracle.forward(inp.x, inp.base_w, inp.base_scale, inp.level_w, inp.level_scale)
@@ -63,10 +157,71 @@ def cpu_baseline(inp, work_bytes, seconds):
         el = time.perf_counter() - t0
         if el >= seconds:
             break
-    return {"value": round(work_bytes * reps / el / 1e9, 4), "unit": "GB/s", "cores": oracle.num_threads(),
-            "kind": "oracle",
+    # single-thread forward on a 4-image slice of the same workload, scaled to the whole batch
+    nb = 4
+    oracle.set_num_threads(1)
+    t1 = time.perf_counter()
+    oracle.forward(inp.x[:nb], inp.base_w, inp.base_scale, inp.level_w, inp.level_scale)
+    el1 = time.perf_counter() - t1
+    oracle.set_num_threads(threads)
+    fwd1_s = el1 * WORKLOAD["B"] / nb
+    return {"value": round(work_bytes * reps / el / 1e9, 4), "unit": "GB/s", "cores": threads,
+            "kind": "oracle", "cpu_model": cpu_model(),
             "sample": f"the full workload ({planes} planes of 56x56, k=5, L=3), forward and backward, "
-                      f"{reps} repetitions in {el:.1f} s, float64; {el / reps * 1e3:.1f} ms per step"}
+                      f"{reps} repetitions in {el:.1f} s, float64; {el / reps * 1e3:.1f} ms per step",
+            "fwd_1thread_s": round(fwd1_s, 3),
+            "fwd_1thread_sample": f"forward of {nb} of {WORKLOAD['B']} images ({nb * WORKLOAD['C']} planes) on one "
+                                  f"thread in {el1:.2f} s, scaled to the whole batch"}
+
+
+def copy_ceiling_gbps(dev, gib=1):
+    """Device-to-device copy of `gib` GiB: bytes read + written per second."""
+    import torch
+    n = gib * (1 << 30) // 4
+    a, b = torch.ones(n, device=dev), torch.empty(n, device=dev)
+    for _ in range(2):
+        b.copy_(a)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    reps = 5
+    for _ in range(reps):
+        b.copy_(a)
+    e1.record()
+    torch.cuda.synchronize()
+    s = e0.elapsed_time(e1) * 1e-3 / reps
+    del a, b
+    torch.cuda.empty_cache()
+    return 2.0 * n * 4 / s / 1e9
+
+
+def valu_probe(dev):
+    """Sustained non-packed fp32 FMA rate from the probe kernel (TFLOP/s and implied clock)."""
+    import ctypes
+
+    import torch
+    from paper_2608_10805_amd import build
+
+    lib = ctypes.CDLL(build.PROBE_LIB)
+    lib.valu_probe_fmas.restype = ctypes.c_longlong
+    lib.valu_probe_fmas.argtypes = [ctypes.c_int, ctypes.c_int]
+    lib.valu_probe_launch.argtypes = [ctypes.c_void_p, ctypes.c_int, ctypes.c_int, ctypes.c_void_p]
+    blocks, iters = 8192, 256
+    out = torch.empty(blocks * 256, device=dev)
+    stream = torch.cuda.current_stream(dev).cuda_stream
+    for _ in range(2):
+        assert lib.valu_probe_launch(out.data_ptr(), blocks, iters, stream) == 0
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    reps = 3
+    for _ in range(reps):
+        assert lib.valu_probe_launch(out.data_ptr(), blocks, iters, stream) == 0
+    e1.record()
+    torch.cuda.synchronize()
+    s = e0.elapsed_time(e1) * 1e-3 / reps
+    fma_s = lib.valu_probe_fmas(blocks, iters) / s
+    return {"fp32_TFLOPs": round(2 * fma_s / 1e12, 2), "implied_clock_GHz": round(fma_s / (256 * 64) / 1e9, 3)}
 
 
 def kernel_source_hash():
@@ -167,6 +322,7 @@ def main():
     end.record()
     torch.cuda.synchronize()
     ms_step = start.elapsed_time(end) / args.steps
+    per_step = [e[0].elapsed_time(e[3]) for e in evs]
     fwd_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
     bwd_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
     fin_ms = float(np.mean([e[2].elapsed_time(e[3]) for e in evs]))
@@ -182,12 +338,18 @@ def main():
     achieved = 2.0 * dom_fma / (dom_ms * 1e-3) / 1e12
     peak = iomodel.FP32_FLOPS / 1e12
     traffic = load_traffic(args.traffic, dom)
+    copy_gbps = copy_ceiling_gbps(dev)
+    probe = valu_probe(dev)
+    log(f"bench: copy ceiling {copy_gbps:.0f} GB/s, VALU probe {probe}")
     roofline = {"bound": "alu", "achieved": round(achieved, 3), "peak": round(peak, 1), "unit": "TFLOP/s",
                 "frac": round(achieved / peak, 4), "traffic": traffic, "kernel": dom,
                 "kernel_ms": round(dom_ms, 5),
                 "hbm_view": {"algorithmic_bytes": dom_bytes,
                              "achieved_GBps": round(dom_bytes / (dom_ms * 1e-3) / 1e9, 1),
                              "frac": round(dom_bytes / (dom_ms * 1e-3) / 1e9 / iomodel.HBM_PEAK_GBPS, 4)}}
+    table = None
+    if not args.no_config_table:
+        table = config_table(args.table_steps, dev)
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(inp, work.bytes_fwdbwd, args.cpu_seconds)
@@ -198,15 +360,23 @@ def main():
         "vs_baseline": None, "dtype": "f32", "data": "synthetic (seeded; x, dy ~ N(0,1), weights U(-0.2,0.2))",
         "config": dict(WORKLOAD),
         "hbm_frac": round(value / iomodel.HBM_PEAK_GBPS, 4),
+        "ms_mean": round(ms_step, 5), "ms_median": round(float(np.median(per_step)), 5),
+        "ms_min": round(float(np.min(per_step)), 5),
+        "copy_ceiling_GBps": round(copy_gbps, 1), "hbm_frac_of_copy": round(value / copy_gbps, 4),
+        "valu_probe": probe,
+        "fma_frac": round(iomodel.fma_floor_s(work.fma_fwdbwd) / (ms_step * 1e-3), 4),
         "fwd_ms": round(fwd_ms, 5), "bwd_fused_ms": round(bwd_ms, 5), "bwd_finalize_ms": round(fin_ms, 5),
         "algorithmic_bytes_per_step": work.bytes_fwdbwd,
         "floors_us": {"hbm": round(iomodel.hbm_floor_s(work.bytes_fwdbwd) * 1e6, 2),
                       "fp32_fma": round(iomodel.fma_floor_s(work.fma_fwdbwd) * 1e6, 2)},
         "paper_io_model_elems_per_N": {"Q_ref": round(iomodel.q_ref(L), 3), "Q_fused": round(iomodel.q_fused(L), 3),
-                                       "single_pass_fwd": 2, "single_pass_fwdbwd": 5},
+                                       "single_pass_fwd": 2, "single_pass_fwdbwd": 5,
+                                       "rocprof_dominant_kernel": (round(traffic / (N * 4), 3)
+                                                                   if traffic is not None else None)},
         "roofline": roofline,
         "cpu_baseline": cpu,
         "N": N,
+        "configs": table,
     }
     print(json.dumps(out), flush=True)
 

@@ -42,6 +42,7 @@ def _load():
     lib.oracle_forward.argtypes = [i] * 6 + [_D] * 6
     lib.oracle_backward.argtypes = [i] * 6 + [_D] * 11
     lib.oracle_num_threads.restype = i
+    lib.oracle_set_num_threads.argtypes = [i]
     _lib = lib
     return lib
 
@@ -61,6 +62,11 @@ def _check(rc, what):
 
 def num_threads() -> int:
     return int(_load().oracle_num_threads())
+
+
+def set_num_threads(n: int) -> None:
+    """OpenMP thread count of the whole-tensor entry points."""
+    _load().oracle_set_num_threads(int(n))
 
 
 def level_shape(H: int, W: int, l: int):

@@ -13,6 +13,9 @@ CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libwtconv.so")
 SOURCES = ["wtconv_api.cpp", "wtconv_kernels.hip"]
+# measurement helper used only by the benchmark (sustained VALU rate)
+PROBE_LIB = os.path.join(HERE, "libvalu_probe.so")
+PROBE_SOURCES = ["valu_probe.hip"]
 ARCH = os.environ.get("WTCONV_OFFLOAD_ARCH", "gfx950")
 
 
@@ -22,15 +25,21 @@ def hipcc_flags():
             "-I", INCLUDE, "-I", CSRC]
 
 
-def build(verbose: bool = False, extra=None) -> str:
-    """Compile every HIP source into libwtconv.so and return its path."""
+def _compile(sources, lib, extra, verbose):
     hipcc = os.path.join(os.environ.get("ROCM_PATH", "/opt/rocm"), "bin", "hipcc")
-    srcs = [os.path.join(CSRC, s) for s in SOURCES]
-    cmd = [hipcc] + hipcc_flags() + list(extra or []) + ["-shared", "-x", "hip"] + srcs + ["-o", LIB + ".tmp"]
+    srcs = [os.path.join(CSRC, s) for s in sources]
+    cmd = [hipcc] + hipcc_flags() + list(extra or []) + ["-shared", "-x", "hip"] + srcs + ["-o", lib + ".tmp"]
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)
-    os.replace(LIB + ".tmp", LIB)
+    os.replace(lib + ".tmp", lib)
+
+
+def build(verbose: bool = False, extra=None) -> str:
+    """Compile every HIP source (libwtconv.so and the benchmark's VALU probe)
+    and return the path of libwtconv.so."""
+    _compile(SOURCES, LIB, extra, verbose)
+    _compile(PROBE_SOURCES, PROBE_LIB, extra, verbose)
     return LIB
 
 
