@@ -42,29 +42,36 @@ int round_cap(int T)
     return T == 4 ? wtc::kMaxRounds4 : (T == 2 ? wtc::kMaxRounds2 : wtc::kMaxRounds1);
 }
 
-// Tile edge for filtering an h x w level with PP resident planes: the fewest
-// register-tile rounds per wavefront, preferring larger tiles (more reuse of
-// every LDS read) when they cost at most 25% more issue slots.
-int pick_tile(int h, int w, int PP)
+// Tile edge for filtering an h x w level with PP resident planes. Each of the
+// four wavefronts filters one band; a round gives every lane one T x T tile.
+// Per round a wavefront issues T*T*k*k FMAs on its SIMD (4 cycles each) and
+// reads a (T+k-1)-row window per lane from LDS, which all four wavefronts
+// share at 128 bytes per cycle (the backward pass reads two windows). The
+// tile with the smallest estimated time max(FMA, LDS) wins, larger tiles on
+// ties; rounds are capped by the registers that hold in-place results.
+int pick_tile(int h, int w, int PP, int k, bool bwd)
 {
-    int rounds[5] = {0, 0, 0, 0, 0};
-    int cost[5] = {0, 0, 0, 0, 0};
-    int best = 1 << 30;
+    const int R = k / 2;
+    long best_cost = -1;
+    int best = 0;
     for (int T : {4, 2, 1}) {
         const long tiles = (long)PP * (ceil_to(h, T) / T) * (ceil_to(w, T) / T);
-        rounds[T] = cdiv(tiles, 64);
-        cost[T] = rounds[T] * T * T;
-        if (rounds[T] <= round_cap(T)) best = std::min(best, cost[T]);
+        const long rounds = cdiv(tiles, 64);
+        if (rounds > round_cap(T)) continue;
+        const long fma_cycles = rounds * T * T * k * k * 4;
+        const long lds_bytes = rounds * wtc::kWaves * (bwd ? 2 : 1) * (T + 2 * R) * window_floats(T, R) * 4 * 64;
+        const long cost = std::max(fma_cycles, lds_bytes / 128);
+        if (best_cost < 0 || cost < best_cost) {
+            best_cost = cost;
+            best = T;
+        }
     }
-    if (best == (1 << 30)) return 0;
-    for (int T : {4, 2, 1})
-        if (rounds[T] <= round_cap(T) && cost[T] * 4 <= best * 5) return T;
-    return 0;
+    return best;
 }
 
 // Lay out one plane's input array and pyramid for a given number of resident
 // planes. Returns false if a level cannot be tiled within the register caps.
-bool layout(const wtconv_desc& d, int PP, PlaneGeom& g)
+bool layout(const wtconv_desc& d, int PP, bool bwd, PlaneGeom& g)
 {
     const int R = d.k / 2;
     memset(&g, 0, sizeof(g));
@@ -83,7 +90,7 @@ bool layout(const wtconv_desc& d, int PP, PlaneGeom& g)
         LevelGeom& lg = g.lv[l];
         lg.h = h;
         lg.w = w;
-        lg.T = pick_tile(h, w, PP);
+        lg.T = pick_tile(h, w, PP, d.k, bwd);
         if (lg.T == 0) return false;
         lg.eh = ceil_to(h, lg.T);
         lg.ew = ceil_to(w, lg.T);
@@ -130,7 +137,7 @@ bool make_plan(const wtconv_desc& d, bool bwd, Plan& pl)
     int PP = 0;
     for (int pp = want; pp >= 1; --pp) {
         PlaneGeom g;
-        if (!layout(d, pp, g)) continue;
+        if (!layout(d, pp, bwd, g)) continue;
         const int lds = lds_floats_for(d, bwd, pp, g);
         if (lds <= kLdsFloatsShared || (pp == 1 && lds <= kLdsFloatsMax)) {
             PP = pp;

@@ -63,11 +63,6 @@ DEV uint16_t from_f32<uint16_t>(float v)  // bf16, round to nearest even
 template <>
 DEV _Float16 from_f32<_Float16>(float v) { return (_Float16)v; }
 
-DEV float readlane_f(float v, int lane)
-{
-    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), lane));
-}
-
 // n / d for 0 <= n < 2^20 from rinv = fp32(1 / d): the exact quotient
 // (n + 0.5) / d lies at least 0.5 / d away from an integer, while the two
 // fp32 roundings perturb it by at most about (n / d) * 2^-23, far less.
@@ -283,7 +278,9 @@ DEV void conv_tile(const float* __restrict__ band, int pitch, int j0, int i0, co
 #pragma unroll
             for (int ox = 0; ox < T; ++ox)
 #pragma unroll
-                for (int t = 0; t < K; ++t) out[oy][ox] = __builtin_fmaf(w[p * K + t], row[ox + t], out[oy][ox]);
+                for (int t = 0; t < K; ++t)  // the first term is a product (no zeroed accumulator)
+                    out[oy][ox] = (p == 0 && t == 0) ? w[0] * row[ox]
+                                                     : __builtin_fmaf(w[p * K + t], row[ox + t], out[oy][ox]);
         }
     }
 }
@@ -313,7 +310,9 @@ DEV void conv_tile_ctr(const float* __restrict__ band, int pitch, int j0, int i0
 #pragma unroll
             for (int ox = 0; ox < T; ++ox)
 #pragma unroll
-                for (int t = 0; t < K; ++t) out[oy][ox] = __builtin_fmaf(w[p * K + t], row[ox + t], out[oy][ox]);
+                for (int t = 0; t < K; ++t)  // the first term is a product (no zeroed accumulator)
+                    out[oy][ox] = (p == 0 && t == 0) ? w[0] * row[ox]
+                                                     : __builtin_fmaf(w[p * K + t], row[ox + t], out[oy][ox]);
         }
     }
 }
@@ -585,7 +584,9 @@ DEV void base_tile(const float* __restrict__ xa, int xpitch, int y0, int x0, con
 #pragma unroll
             for (int ox = 0; ox < 4; ++ox)
 #pragma unroll
-                for (int t = 0; t < K; ++t) acc[oy][ox] = __builtin_fmaf(w[p * K + t], row[ox + t], acc[oy][ox]);
+                for (int t = 0; t < K; ++t)  // the first term is a product (no zeroed accumulator)
+                    acc[oy][ox] = (p == 0 && t == 0) ? w[0] * row[ox]
+                                                     : __builtin_fmaf(w[p * K + t], row[ox + t], acc[oy][ox]);
         }
     }
 }
@@ -696,15 +697,17 @@ DEV float wave_sum(float v)
 // Index of the folded-weight row for the base kernel (0) or level l band q.
 DEV int wrow(int l, int q) { return l == 0 ? 0 : 1 + (l - 1) * 4 + q; }
 
-// Fetch one folded kernel into scalar registers: lane i of `packed` holds tap
-// i; `rot` reverses the tap order (180-degree rotation, used for dx).
+// Fetch one folded kernel into registers (the same value in every lane, read
+// with broadcast LDS loads, so the FMAs take it as a VGPR operand without any
+// cross-lane moves); `rot` reverses the tap order (180-degree rotation, used
+// for dx).
 template <int K>
 DEV void fetch_weights(const float* __restrict__ wtab, int row, bool rot, int lane, float (&w)[K * K])
 {
     constexpr int KK = K * K;
-    const float packed = lane < KK ? wtab[row * KK + lane] : 0.f;
+    (void)lane;
 #pragma unroll
-    for (int i = 0; i < KK; ++i) w[i] = readlane_f(packed, rot ? KK - 1 - i : i);
+    for (int i = 0; i < KK; ++i) w[i] = wtab[row * KK + (rot ? KK - 1 - i : i)];
 }
 
 // ----------------------------------------------------------------------------
