@@ -302,10 +302,35 @@ wtconv_desc coarse_desc(const wtconv_desc& d)
     return s;
 }
 
+// Planes of at most 8 x 8 pixels run in the tiny-plane kernels: one lane per
+// batch entry, so the batch is covered in groups of 64.
+bool use_tiny(const wtconv_desc& d) { return d.H <= wtc::kTinyMaxEdge && d.W <= wtc::kTinyMaxEdge; }
+int tiny_groups(const wtconv_desc& d) { return cdiv(d.B, 64); }
+
+wtc::TinyArgs tiny_args(const wtconv_desc& d, const void* in, const void* aux, void* out, float* partial,
+                        const wtc::ParamPtrs& p, int skip_base)
+{
+    wtc::TinyArgs t;
+    memset(&t, 0, sizeof(t));
+    t.in = in;
+    t.aux = aux;
+    t.out = out;
+    t.partial = partial;
+    t.p = p;
+    t.B = d.B;
+    t.C = d.C;
+    t.H = d.H;
+    t.W = d.W;
+    t.L = d.L;
+    t.skip_base = skip_base;
+    return t;
+}
+
 const size_t kUnsupported = ~(size_t)0;
 
 size_t forward_ws(const wtconv_desc& d)
 {
+    if (use_tiny(d)) return 0;
     Plan pl;
     if (make_plan(d, false, pl)) return 0;
     RegionPlan rp;
@@ -319,6 +344,7 @@ size_t forward_ws(const wtconv_desc& d)
 size_t backward_ws(const wtconv_desc& d)
 {
     const int NP = wtc::partial_floats_per_channel(d.k, d.L);
+    if (use_tiny(d)) return align256((size_t)tiny_groups(d) * d.C * NP * 4);
     Plan pl;
     if (make_plan(d, true, pl)) return align256((size_t)pl.nchunks * d.C * NP * 4);
     RegionPlan rp;
@@ -387,6 +413,9 @@ wtconv_status carrier(const wtconv_desc& d, const void* in, float* out, hipStrea
 wtconv_status forward_impl(const wtconv_desc& d, const void* x, const wtc::ParamPtrs& p, void* y, char* ws,
                            int skip_base, hipStream_t stream)
 {
+    if (use_tiny(d))
+        return hip_status(
+            wtc::launch_tiny(d.k, d.dtype, false, tiny_args(d, x, nullptr, y, nullptr, p, skip_base), stream));
     Plan pl;
     if (make_plan(d, false, pl)) {
         const FusedArgs a = base_args(d, pl, x, nullptr, y, p, skip_base);
@@ -413,6 +442,9 @@ wtconv_status forward_impl(const wtconv_desc& d, const void* x, const wtc::Param
 wtconv_status partials_impl(const wtconv_desc& d, const void* x, const void* dy, const wtc::ParamPtrs& p,
                             void* dx, char* ws, int skip_base, hipStream_t stream)
 {
+    if (use_tiny(d))
+        return hip_status(wtc::launch_tiny(
+            d.k, d.dtype, true, tiny_args(d, dy, x, dx, reinterpret_cast<float*>(ws), p, skip_base), stream));
     Plan pl;
     if (make_plan(d, true, pl)) {
         FusedArgs a = base_args(d, pl, dy, x, dx, p, skip_base);
@@ -467,6 +499,7 @@ wtconv_status reduce(const wtconv_desc& d, int L, int nchunks, const wtc::ParamP
 wtconv_status finalize_impl(const wtconv_desc& d, const wtc::ParamPtrs& p, const Grads& gr, const char* ws,
                             int skip_base, hipStream_t stream)
 {
+    if (use_tiny(d)) return reduce(d, d.L, tiny_groups(d), p, gr, ws, skip_base, stream);
     Plan pl;
     if (make_plan(d, true, pl)) return reduce(d, d.L, pl.nchunks, p, gr, ws, skip_base, stream);
     RegionPlan rp;

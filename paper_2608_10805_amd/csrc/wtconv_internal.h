@@ -93,6 +93,19 @@ struct CarrierArgs {
     int vec_ok;
 };
 
+// Planes of at most 8 x 8 pixels (wtconv_tiny.hip): one workgroup per four
+// channels and 64 batch entries, one lane per batch entry.
+struct TinyArgs {
+    const void* in;   // forward: x; backward: dy
+    const void* aux;  // backward: x
+    void* out;        // forward: y; backward: dx (may be null)
+    float* partial;   // backward: [ceil(B / 64)][C][NP] kernel-gradient partials
+    ParamPtrs p;
+    int B, C, H, W, L;
+    int skip_base;    // 1: no base path and no base-kernel gradient (coarse sub-problem)
+};
+constexpr int kTinyMaxEdge = 8;
+
 struct ReduceArgs {
     const float* partial;
     int nchunks, C, k, L;
@@ -112,5 +125,7 @@ hipError_t launch_forward(int k, wtconv_dtype dt, const FusedArgs& a, int grid, 
 hipError_t launch_backward(int k, wtconv_dtype dt, const FusedArgs& a, int grid, hipStream_t s);
 hipError_t launch_reduce(const ReduceArgs& a, hipStream_t s);
 hipError_t launch_carrier(wtconv_dtype dt, const CarrierArgs& a, hipStream_t s);
+hipError_t launch_tiny(int k, wtconv_dtype dt, bool bwd, const TinyArgs& a, hipStream_t s);
+size_t tiny_lds_bytes(int k, int L, bool bwd);
 
 }  // namespace wtc

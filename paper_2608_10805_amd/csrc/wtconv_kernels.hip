@@ -28,40 +28,17 @@
 // order and unfolds them into dW and d(scale).
 #include <stdint.h>
 
+#include "wtconv_device.h"
 #include "wtconv_internal.h"
 
 namespace wtc {
 namespace {
-
-#define DEV __device__ __forceinline__
 
 // Levels whose kernel gradient is accumulated in per-lane registers across a
 // workgroup's planes (two in the single-round variant, which has the register
 // room, one otherwise); deeper levels accumulate row by row in LDS.
 template <bool ONE>
 constexpr int reg_levels() { return ONE ? 2 : 1; }
-
-// ----------------------------------------------------------------------------
-// storage types
-// ----------------------------------------------------------------------------
-DEV float to_f32(float v) { return v; }
-DEV float to_f32(uint16_t v) { return __uint_as_float(((uint32_t)v) << 16); }  // bf16
-DEV float to_f32(_Float16 v) { return (float)v; }
-
-template <typename T>
-DEV T from_f32(float v);
-template <>
-DEV float from_f32<float>(float v) { return v; }
-template <>
-DEV uint16_t from_f32<uint16_t>(float v)  // bf16, round to nearest even
-{
-    uint32_t u = __float_as_uint(v);
-    if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x0040u);
-    u += 0x7fffu + ((u >> 16) & 1u);
-    return (uint16_t)(u >> 16);
-}
-template <>
-DEV _Float16 from_f32<_Float16>(float v) { return (_Float16)v; }
 
 // n / d for 0 <= n < 2^20 from rinv = fp32(1 / d): the exact quotient
 // (n + 0.5) / d lies at least 0.5 / d away from an integer, while the two
@@ -145,18 +122,6 @@ DEV void st_row(float* __restrict__ p, const float* v)
 #pragma unroll
         for (int i = 0; i < N; ++i) p[i] = v[i];
     }
-}
-
-// Unnormalised Haar butterfly of the 2x2 patch [[a, b], [c, d]]:
-// (LL, LH, HL, HH) = (a+b+c+d, a+b-c-d, a-b+c-d, a-b-c+d), eq. (butterfly)
-// without its factor 1/2.
-DEV void butterfly(float a, float b, float c, float d, float (&o)[4])
-{
-    const float ab = a + b, cd = c + d, amb = a - b, cmd = c - d;
-    o[0] = ab + cd;
-    o[1] = ab - cd;
-    o[2] = amb + cmd;
-    o[3] = amb - cmd;
 }
 
 // ----------------------------------------------------------------------------

@@ -211,6 +211,34 @@ def test_autograd_module_matches_binding():
         assert rel_err(to_np(m.level_scale[l].grad), ref["d_level_scale"][l]) < 1e-5
 
 
+# Planes of at most 8 x 8 pixels run in the tiny-plane kernels (one lane per
+# batch entry, groups of 64): ragged batch groups, channel counts that are not
+# multiples of four, every kernel size, L up to 8 and 16-bit storage.
+TINY = [
+    (70, 3, 7, 6, 5, 4, "f32"),
+    (2, 5, 8, 8, 7, 8, "f32"),
+    (65, 2, 5, 3, 1, 2, "f32"),
+    (3, 4, 4, 7, 3, 3, "bf16"),
+    (128, 9, 7, 7, 5, 5, "f16"),
+    (1, 1, 2, 2, 5, 1, "f32"),
+    (64, 4, 7, 7, 5, 0, "f32"),
+]
+
+
+@pytest.mark.parametrize("B,C,H,W,k,L,dtype", TINY)
+def test_tiny_plane_forward(B, C, H, W, k, L, dtype):
+    check_forward(B, C, H, W, k, L, dtype)
+
+
+@pytest.mark.parametrize("B,C,H,W,k,L,dtype", TINY)
+def test_tiny_plane_backward(B, C, H, W, k, L, dtype):
+    check_backward(B, C, H, W, k, L, dtype)
+
+
+def test_tiny_plane_backward_without_dx():
+    check_backward(70, 3, 7, 6, 5, 4, "f32", need_dx=False)
+
+
 # Planes whose working set does not fit one compute unit's LDS take the split
 # path: the coarse levels run on the level-1 carrier (recursively, if that is
 # still too large) and the base path plus level 1 run on halo tiles. Every
