@@ -216,27 +216,25 @@ struct Grads {
     float* dls[kMaxLevels];
 };
 
-// The same parameters, levels shifted by one: the coarse sub-problem's level
-// l is the full problem's level l + 1.
-wtc::ParamPtrs shift_params(const wtc::ParamPtrs& p)
+// The same parameters, levels shifted by m: the coarse sub-problem's level l
+// is the full problem's level l + m.
+wtc::ParamPtrs shift_params(const wtc::ParamPtrs& p, int m)
 {
     wtc::ParamPtrs s = p;
-    for (int l = 0; l + 1 < kMaxLevels; ++l) {
-        s.lw[l] = p.lw[l + 1];
-        s.ls[l] = p.ls[l + 1];
+    for (int l = 0; l < kMaxLevels; ++l) {
+        s.lw[l] = l + m < kMaxLevels ? p.lw[l + m] : nullptr;
+        s.ls[l] = l + m < kMaxLevels ? p.ls[l + m] : nullptr;
     }
-    s.lw[kMaxLevels - 1] = s.ls[kMaxLevels - 1] = nullptr;
     return s;
 }
 
-Grads shift_grads(const Grads& g)
+Grads shift_grads(const Grads& g, int m)
 {
     Grads s = g;
-    for (int l = 0; l + 1 < kMaxLevels; ++l) {
-        s.dlw[l] = g.dlw[l + 1];
-        s.dls[l] = g.dls[l + 1];
+    for (int l = 0; l < kMaxLevels; ++l) {
+        s.dlw[l] = l + m < kMaxLevels ? g.dlw[l + m] : nullptr;
+        s.dls[l] = l + m < kMaxLevels ? g.dls[l + m] : nullptr;
     }
-    s.dlw[kMaxLevels - 1] = s.dls[kMaxLevels - 1] = nullptr;
     return s;
 }
 
@@ -247,15 +245,26 @@ int vec_ok(const void* a, const void* b, const void* c)
 }
 
 // ----------------------------------------------------------------------------
-// Large planes. A plane whose working set does not fit one CU's LDS is split:
-// the coarse branch (levels 2..L) is exactly the WTConv, without base path, of
-// the level-1 raw LL carrier X1 (a quarter-size plane), whose output is the
-// coarse levels' contribution at the level-1 grid; in the backward pass that
-// sub-problem's input gradient is the same contribution for dx, and its kernel
-// gradients are those of levels 2..L. The sub-problem recurses until it fits.
-// The full-resolution part (base path and level 1) then runs in region mode:
-// each workgroup computes one T x T output tile from a region with a halo of
-// 2R pixels (the level-1 receptive field), adding the carry at level 1.
+// Execution choice. A problem runs in one of four ways:
+//   tiny     planes of at most 8 x 8 pixels: wtconv_tiny.hip, one lane per
+//            batch entry, every level in registers;
+//   resident one fused pass per plane resident in LDS (wtconv_kernels.hip);
+//   split    resident, but the levels above m (the first level whose grid is
+//            at most 8 x 8) are a coarse sub-problem: the coarse branch is
+//            exactly the WTConv, without base path, of the level-m raw LL
+//            carrier X_m (2^-m times each 2^m x 2^m block sum), whose output
+//            is the coarse levels' contribution at the level-m grid and whose
+//            input gradient is the same contribution for dx; its kernel
+//            gradients are those of levels m+1..L. The carrier is tiny, and
+//            the fused pass then runs levels 1..m only and adds the carry at
+//            level m. The deepest levels are the least efficient part of the
+//            fused pass (a few sites per band, one barrier-separated step each,
+//            and the largest LDS footprint), so this trades one extra read of
+//            the input for them;
+//   region   planes too large for LDS: the same split at m = 1 (the sub-
+//            problem recurses until it fits), with the base path and level 1
+//            run on 56 x 56 (or smaller) output tiles with a halo of 2R pixels
+//            (the level-1 receptive field).
 // ----------------------------------------------------------------------------
 struct RegionPlan {
     Plan pl;
@@ -264,6 +273,8 @@ struct RegionPlan {
 
 bool make_region_plan(const wtconv_desc& d, bool bwd, RegionPlan& rp)
 {
+    // the carrier kernel decomposes small offsets with fp32 reciprocals
+    if (d.H >= (1 << 19) || d.W >= (1 << 19)) return false;
     const int R = d.k / 2;
     const int m = d.L > 0 ? 1 : 0;
     rp.h = ceil_to(m ? 2 * R : R, 4);
@@ -290,22 +301,100 @@ bool make_region_plan(const wtconv_desc& d, bool bwd, RegionPlan& rp)
     return false;
 }
 
-long level1_floats(const wtconv_desc& d) { return (long)d.B * d.C * ((d.H + 1) / 2) * ((d.W + 1) / 2); }
+enum class Mode { Tiny, Resident, Split, Region, None };
 
-wtconv_desc coarse_desc(const wtconv_desc& d)
+struct Exec {
+    Mode mode = Mode::None;
+    Plan pl;         // resident / split: the fused pass (split: levels 1..m)
+    RegionPlan rp;   // region
+    int m = 0;       // split / region: levels run by the fused pass
+    bool coarse = false;  // split / region: a coarse sub-problem exists (L > m)
+};
+
+bool use_tiny(const wtconv_desc& d) { return d.H <= wtc::kTinyMaxEdge && d.W <= wtc::kTinyMaxEdge; }
+int tiny_groups(const wtconv_desc& d) { return cdiv(d.B, 64); }
+
+// The first level whose grid is at most 8 x 8.
+int tiny_level(const wtconv_desc& d)
+{
+    int m = 0, h = d.H, w = d.W;
+    while (h > wtc::kTinyMaxEdge || w > wtc::kTinyMaxEdge) {
+        h = (h + 1) / 2;
+        w = (w + 1) / 2;
+        ++m;
+    }
+    return m;
+}
+
+// Whether a resident problem runs its levels above m as a tiny sub-problem
+// (measured on MI355X at the ConvNeXt-T shapes). The split costs one extra
+// read of the input per pass (two in the backward) plus the tiny kernel; it
+// pays when the fused pass loses at least two deep levels (one when those
+// start at level 2, where the fused pass is least efficient), or in the
+// backward pass when it brings the workgroup's LDS under the two-per-CU mark.
+bool want_split(const wtconv_desc& d, bool bwd, int m, int full_lds, int split_lds)
+{
+    if (m < 1 || m > 6 || d.L <= m) return false;
+    const int deep = d.L - m;
+    if (!bwd) return deep >= (m == 1 ? 2 : 3);
+    const int two_per_cu = kLdsFloatsMax / 2;
+    return m == 1 || deep >= 2 || (full_lds > two_per_cu && split_lds <= two_per_cu);
+}
+
+Exec choose(const wtconv_desc& d, bool bwd)
+{
+    Exec ex;
+    if (use_tiny(d)) {
+        ex.mode = Mode::Tiny;
+        return ex;
+    }
+    if (make_plan(d, bwd, ex.pl)) {
+        const int m = tiny_level(d);
+        if (m >= 1 && d.L > m) {
+            wtconv_desc f = d;
+            f.L = m;
+            Plan sp;
+            if (make_plan(f, bwd, sp) && want_split(d, bwd, m, ex.pl.lds_floats, sp.lds_floats)) {
+                ex.pl = sp;
+                ex.mode = Mode::Split;
+                ex.m = m;
+                ex.coarse = true;
+                return ex;
+            }
+        }
+        ex.mode = Mode::Resident;
+        return ex;
+    }
+    if (make_region_plan(d, bwd, ex.rp)) {
+        ex.mode = Mode::Region;
+        ex.m = d.L > 0 ? 1 : 0;
+        ex.coarse = d.L >= 2;
+    }
+    return ex;
+}
+
+// Sites of the level-m grid over the whole tensor.
+long level_floats(const wtconv_desc& d, int m)
+{
+    long h = d.H, w = d.W;
+    for (int l = 0; l < m; ++l) {
+        h = (h + 1) / 2;
+        w = (w + 1) / 2;
+    }
+    return (long)d.B * d.C * h * w;
+}
+
+wtconv_desc coarse_desc(const wtconv_desc& d, int m)
 {
     wtconv_desc s = d;
-    s.H = (d.H + 1) / 2;
-    s.W = (d.W + 1) / 2;
-    s.L = d.L - 1;
+    for (int l = 0; l < m; ++l) {
+        s.H = (s.H + 1) / 2;
+        s.W = (s.W + 1) / 2;
+    }
+    s.L = d.L - m;
     s.dtype = WTCONV_F32;
     return s;
 }
-
-// Planes of at most 8 x 8 pixels run in the tiny-plane kernels: one lane per
-// batch entry, so the batch is covered in groups of 64.
-bool use_tiny(const wtconv_desc& d) { return d.H <= wtc::kTinyMaxEdge && d.W <= wtc::kTinyMaxEdge; }
-int tiny_groups(const wtconv_desc& d) { return cdiv(d.B, 64); }
 
 wtc::TinyArgs tiny_args(const wtconv_desc& d, const void* in, const void* aux, void* out, float* partial,
                         const wtc::ParamPtrs& p, int skip_base)
@@ -328,34 +417,46 @@ wtc::TinyArgs tiny_args(const wtconv_desc& d, const void* in, const void* aux, v
 
 const size_t kUnsupported = ~(size_t)0;
 
+// Kernel-gradient partials written by the fused (or tiny) pass of `ex`.
+size_t pass_partial_bytes(const wtconv_desc& d, const Exec& ex)
+{
+    switch (ex.mode) {
+        case Mode::Tiny:
+            return align256((size_t)tiny_groups(d) * d.C * wtc::partial_floats_per_channel(d.k, d.L) * 4);
+        case Mode::Resident:
+            return align256((size_t)ex.pl.nchunks * d.C * wtc::partial_floats_per_channel(d.k, d.L) * 4);
+        case Mode::Split:
+            return align256((size_t)ex.pl.nchunks * d.C * wtc::partial_floats_per_channel(d.k, ex.m) * 4);
+        case Mode::Region:
+            return align256((size_t)ex.rp.pl.nchunks * ex.rp.ntx * ex.rp.nty * d.C *
+                            wtc::partial_floats_per_channel(d.k, ex.m) * 4);
+        case Mode::None: break;
+    }
+    return kUnsupported;
+}
+
+// Workspace layouts.
+//   forward:  [X_m][carry][sub-problem]                   (split / region with a coarse part)
+//   backward: [partials][X_m][dY_m][dX_m][sub-problem]
 size_t forward_ws(const wtconv_desc& d)
 {
-    if (use_tiny(d)) return 0;
-    Plan pl;
-    if (make_plan(d, false, pl)) return 0;
-    RegionPlan rp;
-    if (!make_region_plan(d, false, rp)) return kUnsupported;
-    if (d.L < 2) return 0;
-    const size_t sub = forward_ws(coarse_desc(d));
+    const Exec ex = choose(d, false);
+    if (ex.mode == Mode::None) return kUnsupported;
+    if (!ex.coarse) return 0;
+    const size_t sub = forward_ws(coarse_desc(d, ex.m));
     if (sub == kUnsupported) return kUnsupported;
-    return 2 * align256(level1_floats(d) * 4) + sub;
+    return 2 * align256(level_floats(d, ex.m) * 4) + sub;
 }
 
 size_t backward_ws(const wtconv_desc& d)
 {
-    const int NP = wtc::partial_floats_per_channel(d.k, d.L);
-    if (use_tiny(d)) return align256((size_t)tiny_groups(d) * d.C * NP * 4);
-    Plan pl;
-    if (make_plan(d, true, pl)) return align256((size_t)pl.nchunks * d.C * NP * 4);
-    RegionPlan rp;
-    if (!make_region_plan(d, true, rp)) return kUnsupported;
-    const int m = d.L > 0 ? 1 : 0;
-    const size_t part = align256((size_t)rp.pl.nchunks * rp.ntx * rp.nty * d.C *
-                                 wtc::partial_floats_per_channel(d.k, m) * 4);
-    if (d.L < 2) return part;
-    const size_t sub = backward_ws(coarse_desc(d));
+    const Exec ex = choose(d, true);
+    if (ex.mode == Mode::None) return kUnsupported;
+    const size_t part = pass_partial_bytes(d, ex);
+    if (!ex.coarse) return part;
+    const size_t sub = backward_ws(coarse_desc(d, ex.m));
     if (sub == kUnsupported) return kUnsupported;
-    return part + 3 * align256(level1_floats(d) * 4) + sub;
+    return part + 3 * align256(level_floats(d, ex.m) * 4) + sub;
 }
 
 FusedArgs base_args(const wtconv_desc& d, const Plan& pl, const void* in, const void* aux, void* out,
@@ -379,7 +480,7 @@ FusedArgs base_args(const wtconv_desc& d, const Plan& pl, const void* in, const 
     return a;
 }
 
-void set_region(FusedArgs& a, const wtconv_desc& d, const RegionPlan& rp, const float* carry)
+void set_region(FusedArgs& a, const wtconv_desc& d, const RegionPlan& rp)
 {
     a.rg_ntx = rp.ntx;
     a.rg_nty = rp.nty;
@@ -389,90 +490,103 @@ void set_region(FusedArgs& a, const wtconv_desc& d, const RegionPlan& rp, const 
     a.real_W = d.W;
     a.rg_r_itx = 1.0f / (float)(rp.T / 4);
     a.rg_r_itiles = 1.0f / (float)((rp.T / 4) * (rp.T / 4));
+}
+
+void set_carry(FusedArgs& a, const wtconv_desc& d, int m, const float* carry)
+{
+    const wtconv_desc c = coarse_desc(d, m);
     a.carry = carry;
-    a.carry_H = (d.H + 1) / 2;
-    a.carry_W = (d.W + 1) / 2;
+    a.carry_H = c.H;
+    a.carry_W = c.W;
+    a.carry_level = m;
 }
 
 wtconv_status hip_status(hipError_t e) { return e == hipSuccess ? WTCONV_OK : WTCONV_ERR_HIP; }
 
-wtconv_status carrier(const wtconv_desc& d, const void* in, float* out, hipStream_t stream)
+wtconv_status carrier(const wtconv_desc& d, int m, const void* in, float* out, hipStream_t stream)
 {
+    const wtconv_desc cd = coarse_desc(d, m);
     wtc::CarrierArgs c;
     c.in = in;
     c.out = out;
     c.planes = (long)d.B * d.C;
     c.H = d.H;
     c.W = d.W;
-    c.H1 = (d.H + 1) / 2;
-    c.W1 = (d.W + 1) / 2;
-    c.vec_ok = 0;
+    c.H1 = cd.H;
+    c.W1 = cd.W;
+    c.m = m;
+    c.vec_ok = (d.W % 4 == 0 && ((uintptr_t)in & (d.dtype == WTCONV_F32 ? 15 : 7)) == 0) ? 1 : 0;
     return hip_status(wtc::launch_carrier(d.dtype, c, stream));
+}
+
+// The fused pass of a resident / split / region execution (grid and plan).
+struct FusedPass {
+    const Plan* pl;
+    int grid;
+};
+
+FusedPass fused_pass(const wtconv_desc& d, const Exec& ex)
+{
+    if (ex.mode == Mode::Region)
+        return {&ex.rp.pl, ex.rp.pl.nchunks * ex.rp.ntx * ex.rp.nty * d.C};
+    return {&ex.pl, ex.pl.nchunks * d.C};
 }
 
 wtconv_status forward_impl(const wtconv_desc& d, const void* x, const wtc::ParamPtrs& p, void* y, char* ws,
                            int skip_base, hipStream_t stream)
 {
-    if (use_tiny(d))
+    const Exec ex = choose(d, false);
+    if (ex.mode == Mode::None) return WTCONV_ERR_UNSUPPORTED;
+    if (ex.mode == Mode::Tiny)
         return hip_status(
             wtc::launch_tiny(d.k, d.dtype, false, tiny_args(d, x, nullptr, y, nullptr, p, skip_base), stream));
-    Plan pl;
-    if (make_plan(d, false, pl)) {
-        const FusedArgs a = base_args(d, pl, x, nullptr, y, p, skip_base);
-        return hip_status(wtc::launch_forward(d.k, d.dtype, a, pl.nchunks * d.C, stream));
-    }
-    RegionPlan rp;
-    if (!make_region_plan(d, false, rp)) return WTCONV_ERR_UNSUPPORTED;
     const float* carry = nullptr;
-    if (d.L >= 2) {
-        const size_t n1 = align256(level1_floats(d) * 4);
+    if (ex.coarse) {
+        const size_t n1 = align256(level_floats(d, ex.m) * 4);
         float* x1 = reinterpret_cast<float*>(ws);
         float* c1 = reinterpret_cast<float*>(ws + n1);
-        wtconv_status st = carrier(d, x, x1, stream);
+        wtconv_status st = carrier(d, ex.m, x, x1, stream);
         if (st != WTCONV_OK) return st;
-        st = forward_impl(coarse_desc(d), x1, shift_params(p), c1, ws + 2 * n1, 1, stream);
+        st = forward_impl(coarse_desc(d, ex.m), x1, shift_params(p, ex.m), c1, ws + 2 * n1, 1, stream);
         if (st != WTCONV_OK) return st;
         carry = c1;
     }
-    FusedArgs a = base_args(d, rp.pl, x, nullptr, y, p, skip_base);
-    set_region(a, d, rp, carry);
-    return hip_status(wtc::launch_forward(d.k, d.dtype, a, rp.pl.nchunks * rp.ntx * rp.nty * d.C, stream));
+    const FusedPass fp = fused_pass(d, ex);
+    FusedArgs a = base_args(d, *fp.pl, x, nullptr, y, p, skip_base);
+    if (ex.mode == Mode::Region) set_region(a, d, ex.rp);
+    if (carry) set_carry(a, d, ex.m, carry);
+    return hip_status(wtc::launch_forward(d.k, d.dtype, a, fp.grid, stream));
 }
 
 wtconv_status partials_impl(const wtconv_desc& d, const void* x, const void* dy, const wtc::ParamPtrs& p,
                             void* dx, char* ws, int skip_base, hipStream_t stream)
 {
-    if (use_tiny(d))
+    const Exec ex = choose(d, true);
+    if (ex.mode == Mode::None) return WTCONV_ERR_UNSUPPORTED;
+    if (ex.mode == Mode::Tiny)
         return hip_status(wtc::launch_tiny(
             d.k, d.dtype, true, tiny_args(d, dy, x, dx, reinterpret_cast<float*>(ws), p, skip_base), stream));
-    Plan pl;
-    if (make_plan(d, true, pl)) {
-        FusedArgs a = base_args(d, pl, dy, x, dx, p, skip_base);
-        a.partial = reinterpret_cast<float*>(ws);
-        return hip_status(wtc::launch_backward(d.k, d.dtype, a, pl.nchunks * d.C, stream));
-    }
-    RegionPlan rp;
-    if (!make_region_plan(d, true, rp)) return WTCONV_ERR_UNSUPPORTED;
-    const int m = d.L > 0 ? 1 : 0;
-    const size_t part = align256((size_t)rp.pl.nchunks * rp.ntx * rp.nty * d.C *
-                                 wtc::partial_floats_per_channel(d.k, m) * 4);
+    const size_t part = pass_partial_bytes(d, ex);
     const float* carry = nullptr;
-    if (d.L >= 2) {
-        const size_t n1 = align256(level1_floats(d) * 4);
+    if (ex.coarse) {
+        const size_t n1 = align256(level_floats(d, ex.m) * 4);
         float* x1 = reinterpret_cast<float*>(ws + part);
         float* dy1 = reinterpret_cast<float*>(ws + part + n1);
         float* dx1 = dx ? reinterpret_cast<float*>(ws + part + 2 * n1) : nullptr;
-        wtconv_status st = carrier(d, x, x1, stream);
-        if (st == WTCONV_OK) st = carrier(d, dy, dy1, stream);
+        wtconv_status st = carrier(d, ex.m, x, x1, stream);
+        if (st == WTCONV_OK) st = carrier(d, ex.m, dy, dy1, stream);
         if (st == WTCONV_OK)
-            st = partials_impl(coarse_desc(d), x1, dy1, shift_params(p), dx1, ws + part + 3 * n1, 1, stream);
+            st = partials_impl(coarse_desc(d, ex.m), x1, dy1, shift_params(p, ex.m), dx1, ws + part + 3 * n1, 1,
+                               stream);
         if (st != WTCONV_OK) return st;
         carry = dx1;
     }
-    FusedArgs a = base_args(d, rp.pl, dy, x, dx, p, skip_base);
-    set_region(a, d, rp, carry);
+    const FusedPass fp = fused_pass(d, ex);
+    FusedArgs a = base_args(d, *fp.pl, dy, x, dx, p, skip_base);
+    if (ex.mode == Mode::Region) set_region(a, d, ex.rp);
+    if (carry) set_carry(a, d, ex.m, carry);
     a.partial = reinterpret_cast<float*>(ws);
-    return hip_status(wtc::launch_backward(d.k, d.dtype, a, rp.pl.nchunks * rp.ntx * rp.nty * d.C, stream));
+    return hip_status(wtc::launch_backward(d.k, d.dtype, a, fp.grid, stream));
 }
 
 wtconv_status reduce(const wtconv_desc& d, int L, int nchunks, const wtc::ParamPtrs& p, const Grads& gr,
@@ -499,21 +613,22 @@ wtconv_status reduce(const wtconv_desc& d, int L, int nchunks, const wtc::ParamP
 wtconv_status finalize_impl(const wtconv_desc& d, const wtc::ParamPtrs& p, const Grads& gr, const char* ws,
                             int skip_base, hipStream_t stream)
 {
-    if (use_tiny(d)) return reduce(d, d.L, tiny_groups(d), p, gr, ws, skip_base, stream);
-    Plan pl;
-    if (make_plan(d, true, pl)) return reduce(d, d.L, pl.nchunks, p, gr, ws, skip_base, stream);
-    RegionPlan rp;
-    if (!make_region_plan(d, true, rp)) return WTCONV_ERR_UNSUPPORTED;
-    const int m = d.L > 0 ? 1 : 0;
-    if (d.L >= 2) {
-        const size_t part = align256((size_t)rp.pl.nchunks * rp.ntx * rp.nty * d.C *
-                                     wtc::partial_floats_per_channel(d.k, m) * 4);
-        const size_t n1 = align256(level1_floats(d) * 4);
-        const wtconv_status st =
-            finalize_impl(coarse_desc(d), shift_params(p), shift_grads(gr), ws + part + 3 * n1, 1, stream);
+    const Exec ex = choose(d, true);
+    switch (ex.mode) {
+        case Mode::None: return WTCONV_ERR_UNSUPPORTED;
+        case Mode::Tiny: return reduce(d, d.L, tiny_groups(d), p, gr, ws, skip_base, stream);
+        case Mode::Resident: return reduce(d, d.L, ex.pl.nchunks, p, gr, ws, skip_base, stream);
+        default: break;
+    }
+    if (ex.coarse) {
+        const size_t part = pass_partial_bytes(d, ex);
+        const size_t n1 = align256(level_floats(d, ex.m) * 4);
+        const wtconv_status st = finalize_impl(coarse_desc(d, ex.m), shift_params(p, ex.m), shift_grads(gr, ex.m),
+                                               ws + part + 3 * n1, 1, stream);
         if (st != WTCONV_OK) return st;
     }
-    return reduce(d, m, rp.pl.nchunks * rp.ntx * rp.nty, p, gr, ws, skip_base, stream);
+    const int nchunks = ex.mode == Mode::Region ? ex.rp.pl.nchunks * ex.rp.ntx * ex.rp.nty : ex.pl.nchunks;
+    return reduce(d, ex.m, nchunks, p, gr, ws, skip_base, stream);
 }
 
 struct Range {

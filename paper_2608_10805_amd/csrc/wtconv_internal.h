@@ -71,26 +71,30 @@ struct FusedArgs {
     int skip_base;       // 1: no base path and no base-kernel gradient (coarse sub-problem)
     // Region mode (planes too large for LDS): each workgroup processes an
     // rg_T x rg_T output tile of a real_H x real_W plane through a region with
-    // a halo of rg_h pixels on every side; g describes the region. `carry` is
-    // the level-1 contribution of the coarser levels ([B][C][carry_H][carry_W]).
+    // a halo of rg_h pixels on every side; g describes the region. `carry`
+    // (nullable, any mode) is the contribution of the levels above
+    // carry_level, on the level-carry_level grid ([B][C][carry_H][carry_W]).
     int rg_ntx, rg_nty;  // tiles per plane row / column
     int rg_T, rg_h;
     int real_H, real_W;
     float rg_r_itx;      // 1 / (rg_T / 4): inner output tiles per tile row
     float rg_r_itiles;   // 1 / (rg_T / 4)^2
     const float* carry;
-    int carry_H, carry_W;
+    int carry_H, carry_W, carry_level;
     PlaneGeom g;
 };
 
-// Level-1 raw LL carrier of every plane: out = (a + b + c + d) / 2 per 2x2
-// block of the zero-extended input, an fp32 [planes][H1][W1] array.
+// Level-m raw LL carrier of every plane: 2^-m times the sum of each 2^m x 2^m
+// block of the zero-extended input, an fp32 [planes][H1][W1] array (H1, W1 =
+// ceil(H / 2^m), ceil(W / 2^m)).
 struct CarrierArgs {
     const void* in;
     float* out;
     long planes;
     int H, W, H1, W1;
-    int vec_ok;
+    int m;
+    int vec_ok;  // 1 if W % 4 == 0 and the input base allows 4-element vector loads
+                 // (2-element loads for m = 1, 4-element ones beyond)
 };
 
 // Planes of at most 8 x 8 pixels (wtconv_tiny.hip): one workgroup per four

@@ -84,6 +84,28 @@ DEV void load_row(const float* __restrict__ p, float (&row)[Win<K, T>::NA])
     }
 }
 
+// Two consecutive storage elements -> fp32 (one 8-byte or 4-byte load).
+DEV void load2(const float* __restrict__ p, float (&v)[2])
+{
+    const float2 f = *reinterpret_cast<const float2*>(p);
+    v[0] = f.x;
+    v[1] = f.y;
+}
+DEV void load2(const uint16_t* __restrict__ p, float (&v)[2])
+{
+    const uint32_t u = *reinterpret_cast<const uint32_t*>(p);
+    v[0] = __uint_as_float(u << 16);
+    v[1] = __uint_as_float(u & 0xffff0000u);
+}
+DEV void load2(const _Float16* __restrict__ p, float (&v)[2])
+{
+    const uint32_t u = *reinterpret_cast<const uint32_t*>(p);
+    _Float16 h[2];
+    __builtin_memcpy(h, &u, 4);
+    v[0] = (float)h[0];
+    v[1] = (float)h[1];
+}
+
 // Four consecutive storage elements -> fp32 (one 16-byte or 8-byte load).
 DEV void load4(const float* __restrict__ p, float (&v)[4])
 {
@@ -564,12 +586,14 @@ DEV void base_tile(const float* __restrict__ xa, int xpitch, int y0, int x0, con
 // per 2x2 quadrant; level 1 has a tuple per quadrant and a sign pair per pixel.
 // Because the LL term of every level enters with sign +, the coarser levels'
 // sum for a quadrant is simply added to that quadrant's level-1 LL.
-// `carry` (nullable) is the coarser levels' contribution at the level-1 grid,
-// in orthonormal units: it enters each level-1 LL with the factor 1/2 of one
-// synthesis step; (cy, cx) is the tile's first level-1 site in it.
+// `carry` (nullable) is the contribution of the levels above m = cr.m (the
+// synthesis of a coarse sub-problem, in orthonormal units, on the level-m
+// grid); it enters level m's LL, i.e. with the factor 2^-m of m synthesis
+// steps: per quadrant for m = 1, tile-wide for m >= 2 (a 4x4 tile lies inside
+// one level-2 site). (cy, cx) is the tile's first level-m site in it.
 struct Carry {
     const float* p;
-    int H, W, cy, cx;
+    int H, W, cy, cx, m;
 };
 
 template <int K>
@@ -580,6 +604,8 @@ DEV void synth_tile(const float* __restrict__ reg, const PlaneGeom& g, int y0, i
     const int L = g.L;
     if (L < 1) return;
     float coarse = 0.f;
+    if (cr.p && cr.m >= 2 && cr.cy < cr.H && cr.cx < cr.W)
+        coarse = __builtin_ldexpf(cr.p[(long)cr.cy * cr.W + cr.cx], -cr.m);
     for (int l = 3; l <= L; ++l) {
         const LevelGeom& lg = g.lv[l];
         const float* z = reg + lg.off + ((y0 >> l) + R) * lg.pitch + (x0 >> l) + R;
@@ -602,7 +628,7 @@ DEV void synth_tile(const float* __restrict__ reg, const PlaneGeom& g, int y0, i
     } else {
         quad[0][0] = quad[0][1] = quad[1][0] = quad[1][1] = coarse;
     }
-    if (cr.p) {
+    if (cr.p && cr.m == 1) {
 #pragma unroll
         for (int a = 0; a < 2; ++a)
 #pragma unroll
@@ -824,13 +850,14 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(const FusedArgs a)
                     } else {
                         base_tile<K>(reg, g.xpitch, ti.j0, ti.i0, w, acc, ctr);
                     }
-                    Carry cr = {nullptr, 0, 0, 0, 0};
-                    if (RGN && a.carry) {
+                    Carry cr = {nullptr, 0, 0, 0, 0, 0};
+                    if (a.carry) {
                         cr.p = a.carry + plane * a.carry_H * a.carry_W;
                         cr.H = a.carry_H;
                         cr.W = a.carry_W;
-                        cr.cy = (oy + ti.j0) >> 1;
-                        cr.cx = (ox + ti.i0) >> 1;
+                        cr.m = a.carry_level;
+                        cr.cy = (oy + ti.j0) >> cr.m;
+                        cr.cx = (ox + ti.i0) >> cr.m;
                     }
                     synth_tile<K>(reg, g, ti.j0, ti.i0, acc, cr);
                     store_tile<ST>(out + plane * HW, PH, PW, oy + ti.j0, ox + ti.i0, acc, vec_store);
@@ -935,24 +962,78 @@ hipError_t launch_one(const FusedArgs& a, int grid, hipStream_t s)
                        : launch_variant<K, ST, BWD, false, false>(a, grid, s);
 }
 
-// Level-1 raw LL carrier: one thread per level-1 site.
-template <typename T>
+// Raw LL carrier of level M (1 <= M <= 6): M levels of the orthonormal
+// butterfly's LL compose to 2^-M times the sum of each 2^M x 2^M pixel block
+// (zero outside the plane). One thread per output site. A workgroup covers
+// 256 consecutive sites: the (plane, row, column) of its first site is
+// computed once (uniformly), and each thread steps from there with fp32
+// reciprocals of small offsets (exact below 2^20). The block's loads are all
+// independent (fully unrolled), vectorised along rows when the plane allows.
+template <typename T, int M>
 __global__ void __launch_bounds__(256) carrier_kernel(const CarrierArgs a)
 {
+    constexpr int E = 1 << M;
     const long n = a.planes * a.H1 * a.W1;
     const T* in = reinterpret_cast<const T*>(a.in);
-    for (long e = blockIdx.x * 256L + threadIdx.x; e < n; e += (long)gridDim.x * 256) {
-        const long p = e / ((long)a.H1 * a.W1);
-        const int r = (int)(e - p * a.H1 * a.W1);
-        const int j = r / a.W1, i = r - (r / a.W1) * a.W1;
-        const T* src = in + p * a.H * a.W;
-        const int y = 2 * j, x = 2 * i;
-        const float v00 = to_f32(src[(long)y * a.W + x]);
-        const float v01 = x + 1 < a.W ? to_f32(src[(long)y * a.W + x + 1]) : 0.f;
-        const float v10 = y + 1 < a.H ? to_f32(src[(long)(y + 1) * a.W + x]) : 0.f;
-        const float v11 = (x + 1 < a.W && y + 1 < a.H) ? to_f32(src[(long)(y + 1) * a.W + x + 1]) : 0.f;
-        a.out[e] = 0.5f * ((v00 + v01) + (v10 + v11));
+    const bool vec = a.vec_ok != 0;
+    const float r_w1 = 1.0f / (float)a.W1, r_h1 = 1.0f / (float)a.H1;
+    for (long e0 = (long)blockIdx.x * 256; e0 < n; e0 += (long)gridDim.x * 256) {
+        const long pj0 = e0 / a.W1;  // uniform
+        const int i0 = (int)(e0 - pj0 * a.W1);
+        const long p0 = pj0 / a.H1;
+        const int j0 = (int)(pj0 - p0 * a.H1);
+        const long e = e0 + threadIdx.x;
+        if (e >= n) continue;
+        const int qi = fdiv(i0 + (int)threadIdx.x, r_w1);  // rows advanced
+        const int i = i0 + (int)threadIdx.x - qi * a.W1;
+        const int qj = fdiv(j0 + qi, r_h1);                 // planes advanced
+        const int j = j0 + qi - qj * a.H1;
+        const long p = p0 + qj;
+        const int y0 = j << M, x0 = i << M;
+        const T* base = in + (p * a.H + y0) * a.W + x0;
+        const bool full = vec && x0 + E <= a.W;
+        float s = 0.f;
+#pragma unroll
+        for (int r = 0; r < E; ++r) {
+            const T* row = base + (long)r * a.W;
+            float rs = 0.f;
+            if (y0 + r >= a.H) {
+                // rows below the plane are zero
+            } else if (full && M == 1) {
+                float v[2];
+                load2(row, v);
+                rs = v[0] + v[1];
+            } else if (full) {
+#pragma unroll
+                for (int c = 0; c < E; c += 4) {
+                    float v[4];
+                    load4(row + c, v);
+                    rs += (v[0] + v[1]) + (v[2] + v[3]);
+                }
+            } else {
+#pragma unroll
+                for (int c = 0; c < E; ++c)
+                    if (x0 + c < a.W) rs += to_f32(row[c]);
+            }
+            s += rs;
+        }
+        a.out[e] = __builtin_ldexpf(s, -M);
     }
+}
+
+template <typename T>
+hipError_t launch_carrier_t(const CarrierArgs& a, int grid, hipStream_t s)
+{
+    switch (a.m) {
+        case 1: hipLaunchKernelGGL((carrier_kernel<T, 1>), dim3(grid), dim3(256), 0, s, a); break;
+        case 2: hipLaunchKernelGGL((carrier_kernel<T, 2>), dim3(grid), dim3(256), 0, s, a); break;
+        case 3: hipLaunchKernelGGL((carrier_kernel<T, 3>), dim3(grid), dim3(256), 0, s, a); break;
+        case 4: hipLaunchKernelGGL((carrier_kernel<T, 4>), dim3(grid), dim3(256), 0, s, a); break;
+        case 5: hipLaunchKernelGGL((carrier_kernel<T, 5>), dim3(grid), dim3(256), 0, s, a); break;
+        case 6: hipLaunchKernelGGL((carrier_kernel<T, 6>), dim3(grid), dim3(256), 0, s, a); break;
+        default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
 }
 
 template <bool BWD>
@@ -990,14 +1071,16 @@ hipError_t launch_backward(int k, wtconv_dtype dt, const FusedArgs& a, int grid,
 
 hipError_t launch_carrier(wtconv_dtype dt, const CarrierArgs& a, hipStream_t s)
 {
+    if (a.m < 1 || a.m > 6) return hipErrorInvalidValue;
     const long n = a.planes * a.H1 * a.W1;
-    const int grid = (int)((n + 255) / 256 < 65536 ? (n + 255) / 256 : 65536);
+    const long blocks = (n + 255) / 256;
+    const int grid = (int)(blocks < 16384 ? blocks : 16384);
     switch (dt) {
-        case WTCONV_F32: hipLaunchKernelGGL(carrier_kernel<float>, dim3(grid), dim3(256), 0, s, a); break;
-        case WTCONV_BF16: hipLaunchKernelGGL(carrier_kernel<uint16_t>, dim3(grid), dim3(256), 0, s, a); break;
-        case WTCONV_F16: hipLaunchKernelGGL(carrier_kernel<_Float16>, dim3(grid), dim3(256), 0, s, a); break;
+        case WTCONV_F32: return launch_carrier_t<float>(a, grid, s);
+        case WTCONV_BF16: return launch_carrier_t<uint16_t>(a, grid, s);
+        case WTCONV_F16: return launch_carrier_t<_Float16>(a, grid, s);
     }
-    return hipGetLastError();
+    return hipErrorInvalidValue;
 }
 
 hipError_t launch_reduce(const ReduceArgs& a, hipStream_t s)

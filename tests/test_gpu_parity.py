@@ -239,6 +239,39 @@ def test_tiny_plane_backward_without_dx():
     check_backward(70, 3, 7, 6, 5, 4, "f32", need_dx=False)
 
 
+# Resident planes with levels beyond the first 8 x 8 grid (level m) may run
+# the coarse levels as a tiny sub-problem on the level-m carrier and the fused
+# pass on levels 1..m with the coarse contribution added at level m (the
+# backward pass splits more often than the forward): m = 1, 2, 3 and 4 in both
+# passes, every kernel size, B above 64, 16-bit storage.
+SPLIT = [
+    (2, 3, 14, 14, 5, 3, "f32"),
+    (3, 2, 28, 28, 5, 4, "f32"),
+    (2, 2, 20, 12, 3, 4, "f32"),
+    (2, 2, 56, 56, 5, 5, "f32"),
+    (1, 2, 63, 95, 5, 5, "f32"),
+    (2, 3, 28, 28, 7, 3, "bf16"),
+    (66, 2, 14, 14, 1, 2, "f16"),
+    (2, 2, 28, 28, 5, 5, "f32"),
+    (1, 2, 56, 56, 5, 6, "f32"),
+    (1, 1, 63, 95, 3, 7, "f32"),
+]
+
+
+@pytest.mark.parametrize("B,C,H,W,k,L,dtype", SPLIT)
+def test_split_forward(B, C, H, W, k, L, dtype):
+    check_forward(B, C, H, W, k, L, dtype)
+
+
+@pytest.mark.parametrize("B,C,H,W,k,L,dtype", SPLIT)
+def test_split_backward(B, C, H, W, k, L, dtype):
+    check_backward(B, C, H, W, k, L, dtype)
+
+
+def test_split_backward_without_dx():
+    check_backward(3, 2, 28, 28, 5, 4, "f32", need_dx=False)
+
+
 # Planes whose working set does not fit one compute unit's LDS take the split
 # path: the coarse levels run on the level-1 carrier (recursively, if that is
 # still too large) and the base path plus level 1 run on halo tiles. Every
