@@ -64,6 +64,40 @@ def table_configs():
         for dt in ("f32", "bf16"):
             for L in (1, 3, 5):
                 out.append((f"sweep_{H}x{W}_c{C}_L{L}_{dt}", B, C, H, W, 5, L, dt))
+    # the paper's own layer sweep: B=8, C in {32, 64, 128}, H=W in {128, 256, 512},
+    # L = 1..5, fp32 and fp16, k = 5 (its latency tables report the geometric
+    # mean over the nine shapes)
+    for dt in ("f32", "f16"):
+        for L in range(1, 6):
+            for C in (32, 64, 128):
+                for H in (128, 256, 512):
+                    out.append((f"paper_{H}x{H}_c{C}_L{L}_{dt}", 8, C, H, H, 5, L, dt))
+    return out
+
+
+# The paper's fused-kernel latencies on its RTX A6000 (geometric mean over its
+# nine layer shapes, k = 5, L = 1..5), for context next to the MI355X figures.
+PAPER_A6000_MS = {
+    "f32": {"fwd": [2.312, 2.552, 2.634, 2.681, 2.703], "fwdbwd": [7.800, 8.693, 8.995, 9.154, 9.277]},
+    "f16": {"fwd": [1.389, 1.592, 1.668, 1.710, 1.748], "fwdbwd": [5.365, 6.148, 6.442, 6.600, 6.733]},
+}
+
+
+def paper_sweep_summary(rows):
+    """Geometric means over the paper's nine layer shapes, per dtype and L."""
+    import math
+    out = {}
+    for dt in ("f32", "f16"):
+        per_l = []
+        for L in range(1, 6):
+            sel = [r for r in rows if r["name"].startswith("paper_") and r["dtype"] == dt and r["L"] == L]
+            if len(sel) != 9:
+                continue
+            g = lambda key: math.exp(sum(math.log(r[key]) for r in sel) / len(sel))  # noqa: E731
+            per_l.append({"L": L, "fwd_ms": round(g("fwd_ms"), 4), "fwdbwd_ms": round(g("fwdbwd_ms"), 4),
+                          "paper_a6000_fwd_ms": PAPER_A6000_MS[dt]["fwd"][L - 1],
+                          "paper_a6000_fwdbwd_ms": PAPER_A6000_MS[dt]["fwdbwd"][L - 1]})
+        out[dt] = per_l
     return out
 
 
@@ -377,6 +411,7 @@ def main():
         "cpu_baseline": cpu,
         "N": N,
         "configs": table,
+        "paper_layer_sweep_geomean": paper_sweep_summary(table) if table else None,
     }
     print(json.dumps(out), flush=True)
 

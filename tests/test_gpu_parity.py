@@ -313,6 +313,13 @@ def test_large_224_fwdbwd_full(L, dtype):
     check_full_size(16, 64, 224, 224, 5, L, dtype, backward=True, n_planes=6, n_channels=2)
 
 
+@pytest.mark.parametrize("C,H,L,dtype", [(32, 512, 5, "f32"), (32, 256, 3, "f16"), (64, 128, 1, "f32"),
+                                         (32, 512, 2, "f16")])
+def test_paper_layer_sweep_full(C, H, L, dtype):
+    """The paper's layer sweep shapes (B=8, C in {32, 64, 128}, H=W in {128, 256, 512})."""
+    check_full_size(8, C, H, H, 5, L, dtype, backward=True, n_planes=4, n_channels=2)
+
+
 def test_large_plane_determinism_bitwise():
     inp, dev = setup(2, 3, 150, 150, 5, 3, "f32", seed=5)
     y1, y2 = dev.forward(), dev.forward()
