@@ -35,12 +35,12 @@ def _load():
     lib.oracle_pyramid_size.argtypes = [i, i, i]
     lib.oracle_pyramid_size.restype = l
     lib.oracle_plane_pyramid.argtypes = [i, i, i, _D, _D]
-    lib.oracle_plane_forward.argtypes = [i, i, i, i, _D, _D, d, _D, _D, _D, _D]
+    lib.oracle_plane_forward.argtypes = [i, i, i, i, _D, _D, d, _D, _D, d, _D, _D]
     lib.oracle_closed_form_synthesis.argtypes = [i, i, i, _D, _D]
     lib.oracle_cascade_synthesis.argtypes = [i, i, i, _D, _D]
-    lib.oracle_plane_backward.argtypes = [i, i, i, i, _D, _D, _D, d, _D, _D, _D, _D, _D, _D, _D]
-    lib.oracle_forward.argtypes = [i] * 6 + [_D] * 6
-    lib.oracle_backward.argtypes = [i] * 6 + [_D] * 11
+    lib.oracle_plane_backward.argtypes = [i, i, i, i, _D, _D, _D, d, _D, _D, d, _D, _D, _D, _D, _D, _D]
+    lib.oracle_forward.argtypes = [i] * 6 + [_D] * 7
+    lib.oracle_backward.argtypes = [i] * 6 + [_D] * 13
     lib.oracle_num_threads.restype = i
     lib.oracle_set_num_threads.argtypes = [i]
     _lib = lib
@@ -127,8 +127,8 @@ def plane_pyramid(x, L: int):
     return _split_pyramid(flat, H, W, L)
 
 
-def plane_forward(x, w0, s0, wl, sl, return_z=False):
-    """Alg. 1 on one plane. wl: [L, 4, k, k], sl: [L, 4]. Returns y (and [Z_1..Z_L])."""
+def plane_forward(x, w0, s0, wl, sl, return_z=False, b0=0.0):
+    """Alg. 1 on one plane. wl: [L, 4, k, k], sl: [L, 4], b0: base bias. Returns y (and [Z_1..Z_L])."""
     x, w0 = _f64(x), _f64(w0)
     H, W = x.shape
     k = w0.shape[0]
@@ -139,8 +139,8 @@ def plane_forward(x, w0, s0, wl, sl, return_z=False):
     y = np.empty((H, W))
     n = int(_load().oracle_pyramid_size(H, W, L))
     z = np.zeros(max(n, 1))
-    _check(_load().oracle_plane_forward(H, W, k, L, _p(x), _p(w0), float(s0), _p(wl_p), _p(sl), _p(y), _p(z)),
-           "plane_forward")
+    _check(_load().oracle_plane_forward(H, W, k, L, _p(x), _p(w0), float(s0), _p(wl_p), _p(sl), float(b0), _p(y),
+                                        _p(z)), "plane_forward")
     if return_z:
         return y, _split_pyramid(z, H, W, L)
     return y
@@ -155,8 +155,8 @@ def closed_form_synthesis(levels, H: int, W: int):
     return R
 
 
-def plane_backward(x, dy, w0, s0, wl, sl):
-    """Reverse mode through plane_forward. Returns dx, dw0, ds0, dwl [L,4,k,k], dsl [L,4]."""
+def plane_backward(x, dy, w0, s0, wl, sl, b0=0.0):
+    """Reverse mode through plane_forward. Returns dx, dw0, ds0, dwl [L,4,k,k], dsl [L,4], db0."""
     x, dy, w0 = _f64(x), _f64(dy), _f64(w0)
     H, W = x.shape
     k = w0.shape[0]
@@ -166,12 +166,13 @@ def plane_backward(x, dy, w0, s0, wl, sl):
     dx = np.empty((H, W))
     dw0 = np.empty((k, k))
     ds0 = np.empty(1)
+    db0 = np.empty(1)
     dwl = np.zeros((max(L, 1), 4, k, k))
     dsl = np.zeros((max(L, 1), 4))
     wl_p = wl if L else np.zeros(1)
-    _check(_load().oracle_plane_backward(H, W, k, L, _p(x), _p(dy), _p(w0), float(s0), _p(wl_p), _p(sl),
-                                         _p(dx), _p(dw0), _p(ds0), _p(dwl), _p(dsl)), "plane_backward")
-    return dx, dw0, float(ds0[0]), dwl[:L], dsl[:L]
+    _check(_load().oracle_plane_backward(H, W, k, L, _p(x), _p(dy), _p(w0), float(s0), _p(wl_p), _p(sl), float(b0),
+                                         _p(dx), _p(dw0), _p(ds0), _p(db0), _p(dwl), _p(dsl)), "plane_backward")
+    return dx, dw0, float(ds0[0]), dwl[:L], dsl[:L], float(db0[0])
 
 
 def _stack_levels(level_w, level_scale, C, k):
@@ -183,36 +184,42 @@ def _stack_levels(level_w, level_scale, C, k):
     return lw, ls
 
 
-def forward(x, base_w, base_scale, level_w, level_scale):
-    """Whole-tensor forward. level_w / level_scale: lists of L arrays [4C,k,k] / [4C]."""
+def forward(x, base_w, base_scale, level_w, level_scale, base_bias=None):
+    """Whole-tensor forward. level_w / level_scale: lists of L arrays [4C,k,k] / [4C];
+    base_bias: [C] or None (zero)."""
     x = _f64(x)
     B, C, H, W = x.shape
     base_w = _f64(base_w)
     k = base_w.shape[-1]
     L = len(level_w)
     lw, ls = _stack_levels(level_w, level_scale, C, k)
+    bias = _f64(base_bias) if base_bias is not None else None
     y = np.empty_like(x)
-    _check(_load().oracle_forward(B, C, H, W, k, L, _p(x), _p(base_w), _p(_f64(base_scale)), _p(lw), _p(ls),
-                                  _p(y)), "forward")
+    _check(_load().oracle_forward(B, C, H, W, k, L, _p(x), _p(base_w), _p(_f64(base_scale)),
+                                  _p(bias) if bias is not None else None, _p(lw), _p(ls), _p(y)), "forward")
     return y
 
 
-def backward(x, dy, base_w, base_scale, level_w, level_scale):
-    """Whole-tensor backward. Returns dict with dx, d_base_w, d_base_scale, d_level_w, d_level_scale."""
+def backward(x, dy, base_w, base_scale, level_w, level_scale, base_bias=None):
+    """Whole-tensor backward. Returns dict with dx, d_base_w, d_base_scale, d_base_bias,
+    d_level_w, d_level_scale."""
     x, dy = _f64(x), _f64(dy)
     B, C, H, W = x.shape
     base_w = _f64(base_w)
     k = base_w.shape[-1]
     L = len(level_w)
     lw, ls = _stack_levels(level_w, level_scale, C, k)
+    bias = _f64(base_bias) if base_bias is not None else None
     dx = np.empty_like(x)
     dbw = np.empty((C, k, k))
     dbs = np.empty(C)
+    dbb = np.empty(C)
     dlw = np.zeros((max(L, 1), 4 * C, k, k))
     dls = np.zeros((max(L, 1), 4 * C))
-    _check(_load().oracle_backward(B, C, H, W, k, L, _p(x), _p(dy), _p(base_w), _p(_f64(base_scale)), _p(lw),
-                                   _p(ls), _p(dx), _p(dbw), _p(dbs), _p(dlw), _p(dls)), "backward")
-    return {"dx": dx, "d_base_w": dbw, "d_base_scale": dbs,
+    _check(_load().oracle_backward(B, C, H, W, k, L, _p(x), _p(dy), _p(base_w), _p(_f64(base_scale)),
+                                   _p(bias) if bias is not None else None, _p(lw), _p(ls), _p(dx), _p(dbw),
+                                   _p(dbs), _p(dbb), _p(dlw), _p(dls)), "backward")
+    return {"dx": dx, "d_base_w": dbw, "d_base_scale": dbs, "d_base_bias": dbb,
             "d_level_w": [dlw[l] for l in range(L)], "d_level_scale": [dls[l] for l in range(L)]}
 
 

@@ -14,7 +14,7 @@
  *     X0 = x
  *     for l = 1..L:  Y_l = A(X_{l-1});  Z_l = s_l * (Y_l (*) W_l);  X_l = LL(Y_l)
  *     R = 0;  for l = L..1:  R = A^T( (LL(Z_l) + R) || H(Z_l) )
- *     y = s0 * (x (*) W0) + R                       (bias b = 0)
+ *     y = s0 * (x (*) W0 + b) + R                   (b: one bias per channel)
  *   A is one level of the orthonormal 2x2 Haar transform, i.e. the matrix of
  *   Proposition 1 applied to every non-overlapping 2x2 block, with the band
  *   formulas of eq. (butterfly) in Section 4.1. A^T is its synthesis.
@@ -245,7 +245,8 @@ int oracle_cascade_synthesis(int H, int W, int L, const double* z, double* R)
 
 /*
  * Forward pass of one plane, Alg. 1 exactly as written.
- *   w0: k*k base kernel, s0: base scale,
+ *   w0: k*k base kernel, s0: base scale, b0: base bias (Alg. 1's return line:
+ *       the bias is added to the base convolution before the scale),
  *   wl: L x 4 x k*k level kernels of this channel (row q of level l is
  *       convolution channel 4c+q), sl: L x 4 level scales,
  *   y: H x W output,
@@ -253,7 +254,7 @@ int oracle_cascade_synthesis(int H, int W, int L, const double* z, double* R)
  *       as in oracle_pyramid_size.
  */
 int oracle_plane_forward(int H, int W, int k, int L, const double* x, const double* w0, double s0,
-                         const double* wl, const double* sl, double* y, double* z_out)
+                         const double* wl, const double* sl, double b0, double* y, double* z_out)
 {
     int hs[64], ws[64];
     if (H < 1 || W < 1 || k < 1 || (k % 2) == 0 || L < 0 || L > 60) return 1;
@@ -291,7 +292,7 @@ int oracle_plane_forward(int H, int W, int k, int L, const double* x, const doub
     /* base path plus reconstruction */
     if (rc == 0) {
         oracle_corr_same(H, W, k, x, w0, y);
-        for (long e = 0; e < (long)H * W; ++e) y[e] = s0 * y[e] + R[e];
+        for (long e = 0; e < (long)H * W; ++e) y[e] = s0 * (y[e] + b0) + R[e];
         if (z_out && npyr > 0) memcpy(z_out, Z, sizeof(double) * (size_t)npyr);
     }
     free(Z); free(Yl); free(carrier); free(R);
@@ -332,11 +333,13 @@ void oracle_closed_form_synthesis(int H, int W, int L, const double* z, double* 
 /*
  * Backward pass of one plane: exact reverse mode through oracle_plane_forward.
  * Outputs dx (H x W) and the plane's parameter gradients:
- *   gw0 [k*k], gs0 [1], gwl [L x 4 x k*k], gsl [L x 4]  (overwritten).
+ *   gw0 [k*k], gs0 [1], gb0 [1], gwl [L x 4 x k*k], gsl [L x 4]  (overwritten).
+ * With y_base = s0 (x (*) W0 + b0): dW0 = s0 corr(dy, x), db0 = s0 sum(dy) and
+ * ds0 = sum(dy (x (*) W0 + b0)), which is eq. (foldgrad)'s <dW~, W> + db~ b.
  */
 int oracle_plane_backward(int H, int W, int k, int L, const double* x, const double* dy,
-                          const double* w0, double s0, const double* wl, const double* sl,
-                          double* dx, double* gw0, double* gs0, double* gwl, double* gsl)
+                          const double* w0, double s0, const double* wl, const double* sl, double b0,
+                          double* dx, double* gw0, double* gs0, double* gb0, double* gwl, double* gsl)
 {
     int hs[64], ws[64];
     if (H < 1 || W < 1 || k < 1 || (k % 2) == 0 || L < 0 || L > 60) return 1;
@@ -376,12 +379,16 @@ int oracle_plane_backward(int H, int W, int k, int L, const double* x, const dou
         off += 4L * n;
     }
 
-    /* base path: y_base = s0 * corr(x, w0) */
+    /* base path: y_base = s0 * (corr(x, w0) + b0) */
     for (int t = 0; t < kk; ++t) gw0[t] = 0.0;
     oracle_corr_same(H, W, k, x, w0, tmp);
-    double g = 0.0;
-    for (size_t e = 0; e < HW; ++e) g += dy[e] * tmp[e];
+    double g = 0.0, sdy = 0.0;
+    for (size_t e = 0; e < HW; ++e) {
+        g += dy[e] * (tmp[e] + b0);
+        sdy += dy[e];
+    }
     *gs0 = g;
+    *gb0 = s0 * sdy;
     for (size_t e = 0; e < HW; ++e) dC[e] = s0 * dy[e];
     corr_same_kernel_grad(H, W, k, dC, x, gw0);
     corr_same_adjoint(H, W, k, dC, w0, dx);
@@ -451,7 +458,8 @@ static int check_desc(int B, int C, int H, int W, int k, int L)
 
 /* Whole-tensor forward. OpenMP over the B*C independent planes. */
 int oracle_forward(int B, int C, int H, int W, int k, int L, const double* x, const double* base_w,
-                   const double* base_scale, const double* level_w, const double* level_scale, double* y)
+                   const double* base_scale, const double* base_bias, const double* level_w,
+                   const double* level_scale, double* y)
 {
     if (check_desc(B, C, H, W, k, L)) return 1;
     const int kk = k * k;
@@ -467,7 +475,7 @@ int oracle_forward(int B, int C, int H, int W, int k, int L, const double* x, co
         } else {
             channel_params(C, k, L, c, level_w, level_scale, wl, sl);
             err |= oracle_plane_forward(H, W, k, L, x + pl * HW, base_w + (long)c * kk, base_scale[c], wl, sl,
-                                        y + pl * HW, NULL);
+                                        base_bias ? base_bias[c] : 0.0, y + pl * HW, NULL);
         }
         free(wl);
         free(sl);
@@ -478,15 +486,15 @@ int oracle_forward(int B, int C, int H, int W, int k, int L, const double* x, co
 /* Whole-tensor backward. Planes run in parallel; the per-plane parameter
  * gradients are then summed over b = 0..B-1 in that order. */
 int oracle_backward(int B, int C, int H, int W, int k, int L, const double* x, const double* dy,
-                    const double* base_w, const double* base_scale, const double* level_w,
-                    const double* level_scale, double* dx, double* d_base_w, double* d_base_scale,
-                    double* d_level_w, double* d_level_scale)
+                    const double* base_w, const double* base_scale, const double* base_bias,
+                    const double* level_w, const double* level_scale, double* dx, double* d_base_w,
+                    double* d_base_scale, double* d_base_bias, double* d_level_w, double* d_level_scale)
 {
     if (check_desc(B, C, H, W, k, L)) return 1;
     const int kk = k * k;
     const long HW = (long)H * W;
     const long P = (long)B * C;
-    const long per = kk + 1 + (long)L * 4 * kk + (long)L * 4; /* per-plane gradient record */
+    const long per = kk + 2 + (long)L * 4 * kk + (long)L * 4; /* per-plane gradient record */
     double* part = (double*)malloc(sizeof(double) * (size_t)(P * per));
     if (!part) return 2;
     int err = 0;
@@ -501,8 +509,9 @@ int oracle_backward(int B, int C, int H, int W, int k, int L, const double* x, c
             channel_params(C, k, L, c, level_w, level_scale, wl, sl);
             double* rec = part + pl * per;
             err |= oracle_plane_backward(H, W, k, L, x + pl * HW, dy + pl * HW, base_w + (long)c * kk,
-                                         base_scale[c], wl, sl, dx + pl * HW, rec, rec + kk, rec + kk + 1,
-                                         rec + kk + 1 + (long)L * 4 * kk);
+                                         base_scale[c], wl, sl, base_bias ? base_bias[c] : 0.0, dx + pl * HW,
+                                         rec, rec + kk, rec + kk + 1, rec + kk + 2,
+                                         rec + kk + 2 + (long)L * 4 * kk);
         }
         free(wl);
         free(sl);
@@ -513,6 +522,7 @@ int oracle_backward(int B, int C, int H, int W, int k, int L, const double* x, c
     }
     memset(d_base_w, 0, sizeof(double) * (size_t)C * kk);
     memset(d_base_scale, 0, sizeof(double) * (size_t)C);
+    memset(d_base_bias, 0, sizeof(double) * (size_t)C);
     if (L > 0) {
         memset(d_level_w, 0, sizeof(double) * (size_t)L * 4 * C * kk);
         memset(d_level_scale, 0, sizeof(double) * (size_t)L * 4 * C);
@@ -523,12 +533,13 @@ int oracle_backward(int B, int C, int H, int W, int k, int L, const double* x, c
             /* dW0 = s0 * dW~0 happens inside the plane adjoint (dC = s0*dy) */
             for (int t = 0; t < kk; ++t) d_base_w[(long)c * kk + t] += rec[t];
             d_base_scale[c] += rec[kk];
+            d_base_bias[c] += rec[kk + 1];
             for (int l = 0; l < L; ++l)
                 for (int q = 0; q < 4; ++q) {
-                    const double* gw = rec + kk + 1 + ((long)l * 4 + q) * kk;
+                    const double* gw = rec + kk + 2 + ((long)l * 4 + q) * kk;
                     double* dst = d_level_w + ((long)l * 4 * C + 4L * c + q) * kk;
                     for (int t = 0; t < kk; ++t) dst[t] += gw[t];
-                    d_level_scale[(long)l * 4 * C + 4L * c + q] += rec[kk + 1 + (long)L * 4 * kk + l * 4 + q];
+                    d_level_scale[(long)l * 4 * C + 4L * c + q] += rec[kk + 2 + (long)L * 4 * kk + l * 4 + q];
                 }
         }
     free(part);

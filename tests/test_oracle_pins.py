@@ -383,3 +383,88 @@ def test_batch_sum_order_and_plane_independence():
             np.testing.assert_array_equal(g["dx"][b, c], dxp)
             acc_w0[c] += dw0p
     np.testing.assert_array_equal(g["d_base_w"], acc_w0)
+
+
+# --------------------------------------------------------------------------
+# P12: the base bias of Algorithm 1 (y = s0 (x * W0 + b) + R) and its
+# gradients, eq. (fold) / eq. (foldgrad): db = s0 * sum(dy),
+# ds0 = <dW~, W0> + db~ * b with db~ = sum(dy)
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("B,C,H,W,k,L", [(2, 3, 9, 7, 5, 2), (1, 2, 8, 8, 3, 0), (2, 2, 5, 6, 7, 1)])
+def test_bias_matches_torch_conv2d_bias(B, C, H, W, k, L):
+    """Zero wavelet weights: y = s0 * conv2d(x, W0, bias=b), torch float64."""
+    x = RNG.standard_normal((B, C, H, W))
+    w0, s0, wl, sl = _rand_params(C, k, L, zero_levels=True)
+    b = RNG.uniform(-1, 1, (C,))
+    got = oracle.forward(x, w0, s0, wl, sl, base_bias=b)
+    want = F.conv2d(torch.from_numpy(x), torch.from_numpy(w0).reshape(C, 1, k, k), bias=torch.from_numpy(b),
+                    padding=k // 2, groups=C).numpy() * s0[None, :, None, None]
+    np.testing.assert_allclose(got, want, rtol=0, atol=1e-14)
+
+
+def test_bias_only_closed_form():
+    """All kernels zero: y = s0 * b everywhere; db = s0 * sum(dy), ds0 = b * sum(dy),
+    and dx = 0."""
+    B, C, H, W, k, L = 3, 4, 7, 9, 5, 3
+    rng = np.random.default_rng(3)
+    x = rng.standard_normal((B, C, H, W))
+    dy = rng.standard_normal((B, C, H, W))
+    s0 = rng.uniform(0.5, 1.5, (C,))
+    b = rng.uniform(-1, 1, (C,))
+    wl = [np.zeros((4 * C, k, k)) for _ in range(L)]
+    sl = [rng.uniform(0.05, 0.2, (4 * C,)) for _ in range(L)]
+    y = oracle.forward(x, np.zeros((C, k, k)), s0, wl, sl, base_bias=b)
+    np.testing.assert_array_equal(y, np.broadcast_to((s0 * b)[None, :, None, None], y.shape))
+    g = oracle.backward(x, dy, np.zeros((C, k, k)), s0, wl, sl, base_bias=b)
+    sdy = dy.sum(axis=(0, 2, 3))
+    np.testing.assert_allclose(g["d_base_bias"], s0 * sdy, rtol=1e-13, atol=0)
+    np.testing.assert_allclose(g["d_base_scale"], b * sdy, rtol=1e-13, atol=0)
+    assert not np.any(g["dx"])
+
+
+@pytest.mark.parametrize("H,W,k,L", [(5, 5, 3, 1), (8, 8, 5, 2), (9, 7, 3, 3)])
+def test_bias_finite_differences(H, W, k, L):
+    B, C = 2, 2
+    x = RNG.standard_normal((B, C, H, W))
+    dy = RNG.standard_normal((B, C, H, W))
+    w0, s0, wl, sl = _rand_params(C, k, L)
+    b = RNG.uniform(-1, 1, (C,))
+    g = oracle.backward(x, dy, w0, s0, wl, sl, base_bias=b)
+    h = 1e-3
+
+    def loss():
+        return float((oracle.forward(x, w0, s0, wl, sl, base_bias=b) * dy).sum())
+
+    def fd(arr, idx):
+        a0 = arr[idx]
+        arr[idx] = a0 + h
+        up = loss()
+        arr[idx] = a0 - h
+        dn = loss()
+        arr[idx] = a0
+        return (up - dn) / (2 * h)
+
+    for c in range(C):
+        assert abs(fd(b, (c,)) - g["d_base_bias"][c]) <= 1e-7 * max(1.0, abs(g["d_base_bias"][c]))
+        assert abs(fd(s0, (c,)) - g["d_base_scale"][c]) <= 1e-7 * max(1.0, abs(g["d_base_scale"][c]))
+    # dx and the kernel gradients do not depend on the bias
+    g0 = oracle.backward(x, dy, w0, s0, wl, sl)
+    np.testing.assert_array_equal(g["dx"], g0["dx"])
+    np.testing.assert_array_equal(g["d_base_w"], g0["d_base_w"])
+
+
+def test_bias_homogeneity():
+    """The base branch s0 (x * W0 + b) is linear in (W0, b) jointly and in s0:
+    sum(dW0 W0) + sum(db b) = sum(ds0 s0) = <dy, base branch>."""
+    B, C, H, W, k, L = 2, 5, 16, 12, 5, 2
+    rng = np.random.default_rng(11)
+    x = rng.standard_normal((B, C, H, W))
+    dy = rng.standard_normal((B, C, H, W))
+    w0, s0, wl, sl = _rand_params(C, k, L, rng)
+    b = rng.uniform(-1, 1, (C,))
+    g = oracle.backward(x, dy, w0, s0, wl, sl, base_bias=b)
+    zero = [np.zeros_like(w) for w in wl]
+    ref = (dy * oracle.forward(x, w0, s0, zero, sl, base_bias=b)).sum()
+    assert abs((g["d_base_w"] * w0).sum() + (g["d_base_bias"] * b).sum() - ref) <= 1e-11 * abs(ref)
+    assert abs((g["d_base_scale"] * s0).sum() - ref) <= 1e-11 * abs(ref)
