@@ -373,6 +373,117 @@ Exec choose(const wtconv_desc& d, bool bwd)
     return ex;
 }
 
+// ----------------------------------------------------------------------------
+// Kernel-gradient pass of the backward (wtconv_grad.hip). When it is used, dx
+// is the forward pass on dy with rotated kernels and grad_kernel forms every
+// kernel gradient. It needs every batch of resident planes to load at most
+// one 4x4 block per thread; otherwise the fused backward runs.
+// ----------------------------------------------------------------------------
+struct GradPlan {
+    PlaneGeom g;  // x side (zero-haloed)
+    int dy_off[kMaxLevels + 1] = {}, dy_pitch[kMaxLevels + 1] = {}, dy_band[kMaxLevels + 1] = {};
+    int stride = 0, PP = 1, nb = 1, nchunks = 1, lds_floats = 0;
+};
+
+int grad_gc_floats(const wtconv_desc& d)
+{
+    return d.L > 2 ? ceil_to((d.L - 2) * 4 * d.k * d.k, 4) : 0;
+}
+
+// Compact dy pyramid next to the x side. A level's array covers the sites its
+// tiles read (tile-aligned extents), the sites the block loads write (levels 1
+// and 2), the sources of the next level's butterflies and, for levels >= 3,
+// whole row chunks of the row-wise correlation. Level 1 is stored over the x
+// plane when it fits and the block loads write every site that is read.
+bool grad_layout(const wtconv_desc& d, int PP, GradPlan& gp)
+{
+    // storing dy level 1 over the x plane costs a re-zeroing of the x plane's
+    // halo ring per batch; it pays for large planes (one resident plane), where
+    // it decides the number of workgroups per CU
+    const bool may_alias = PP == 1;
+    if (!layout(d, PP, true, gp.g)) return false;
+    const PlaneGeom& g = gp.g;
+    const long xplane = (long)g.xrows * g.xpitch;
+    long extra = 0;
+    for (int l = 1; l <= d.L; ++l) {
+        const LevelGeom& lg = g.lv[l];
+        int rows = std::max(lg.eh, l == 1 ? 2 * g.tiles_y : (l == 2 ? g.tiles_y : lg.h));
+        int cols = std::max(lg.ew, l == 1 ? 2 * g.tiles_x : (l == 2 ? g.tiles_x : lg.w));
+        if (l < d.L) {
+            rows = std::max(rows, 2 * g.lv[l + 1].h);
+            cols = std::max(cols, 2 * g.lv[l + 1].w);
+        }
+        if (l >= 3) cols = std::max(cols, ceil_to(lg.w, lg.w <= 8 ? 8 : 16));
+        const int pitch = ceil_to(cols, 4);
+        const long size = 4L * rows * pitch;
+        gp.dy_pitch[l] = pitch;
+        gp.dy_band[l] = rows * pitch;
+        if (l == 1 && may_alias && size <= xplane && lg.eh <= 2 * g.tiles_y && lg.ew <= 2 * g.tiles_x) {
+            gp.dy_off[l] = 0;
+        } else {
+            gp.dy_off[l] = (int)(g.plane_floats + extra);
+            extra += size;
+        }
+        if (g.plane_floats + extra > (1L << 28)) return false;
+    }
+    gp.stride = (int)(g.plane_floats + extra);
+    const long planes = std::max((long)PP * gp.stride, 12L * d.k * d.k);
+    const long total = grad_gc_floats(d) + ceil_to((int)std::min(planes, 1L << 28), 4);
+    if (total > kLdsFloatsMax) return false;
+    gp.lds_floats = (int)total;
+    return true;
+}
+
+// Resident planes per batch: the best of (block-load lane use) x (workgroups
+// per CU, up to three) over the feasible counts; larger counts on ties.
+bool make_grad_plan(const wtconv_desc& d, GradPlan& gp)
+{
+    const long per = (long)(ceil_to(d.H, 4) / 4) * (ceil_to(d.W, 4) / 4);
+    if (per > wtc::kThreads) return false;
+    const int maxpp = (int)std::min<long>(d.B, wtc::kThreads / per);
+    double best = -1.0;
+    for (int pp = 1; pp <= maxpp; ++pp) {
+        GradPlan c;
+        if (!grad_layout(d, pp, c)) continue;
+        const int wgs = std::min(3, kLdsFloatsMax / c.lds_floats);
+        const double score = (double)pp * per / wtc::kThreads * wgs;
+        if (score >= best) {
+            best = score;
+            gp = c;
+            gp.PP = pp;
+        }
+    }
+    if (best < 0) return false;
+    // One round of resident workgroups: the per-workgroup setup and the final
+    // reduction of 3 x 25 sums per thread are paid once per workgroup, so few
+    // long-running workgroups that fill every CU beat many short ones
+    // (measured on MI355X at the ConvNeXt-T shapes).
+    const int wgs_per_cu = std::max(1, std::min(3, kLdsFloatsMax / gp.lds_floats));
+    const int slots = 256 * wgs_per_cu;
+    const int chunks = std::max(1, std::min(d.B, (int)((double)slots / d.C + 0.5)));
+    gp.nb = ceil_to(cdiv(d.B, chunks), gp.PP);
+    gp.nchunks = cdiv(d.B, gp.nb);
+    return true;
+}
+
+struct GradExec {
+    bool use = false;
+    GradPlan gp;
+};
+
+// Measured on MI355X: the gradient pass beats the fused backward when the
+// plane's first level at most 8 x 8 is level 2 or deeper (planes above 16 x 16)
+// and there are at least two levels; it then handles every level itself. For
+// smaller planes (whose coarse levels the fused backward runs as a tiny
+// sub-problem) and for L <= 1 the fused backward is as fast or faster.
+GradExec choose_grad(const wtconv_desc& d)
+{
+    GradExec ge;
+    if (use_tiny(d) || tiny_level(d) < 2 || d.L < 2) return ge;
+    ge.use = make_grad_plan(d, ge.gp);
+    return ge;
+}
+
 // Sites of the level-m grid over the whole tensor.
 long level_floats(const wtconv_desc& d, int m)
 {
@@ -448,8 +559,22 @@ size_t forward_ws(const wtconv_desc& d)
     return 2 * align256(level_floats(d, ex.m) * 4) + sub;
 }
 
+size_t backward_ws(const wtconv_desc& d);
+
+// Gradient-pass workspace: [partials][forward workspace of dx]
+size_t grad_partial_bytes(const wtconv_desc& d, const GradExec& ge)
+{
+    return align256((size_t)ge.gp.nchunks * d.C * wtc::partial_floats_per_channel(d.k, d.L) * 4);
+}
+
 size_t backward_ws(const wtconv_desc& d)
 {
+    const GradExec ge = choose_grad(d);
+    if (ge.use) {
+        const size_t fwd = forward_ws(d);
+        if (fwd == kUnsupported) return kUnsupported;
+        return grad_partial_bytes(d, ge) + fwd;
+    }
     const Exec ex = choose(d, true);
     if (ex.mode == Mode::None) return kUnsupported;
     const size_t part = pass_partial_bytes(d, ex);
@@ -558,9 +683,44 @@ wtconv_status forward_impl(const wtconv_desc& d, const void* x, const wtc::Param
     return hip_status(wtc::launch_forward(d.k, d.dtype, a, fp.grid, stream));
 }
 
+wtconv_status grad_pass(const wtconv_desc& d, const GradExec& ge, const void* x, const void* dy, float* partial,
+                        int skip_base, hipStream_t stream)
+{
+    wtc::GradArgs a;
+    memset(&a, 0, sizeof(a));
+    a.x = x;
+    a.dy = dy;
+    a.partial = partial;
+    a.B = d.B;
+    a.C = d.C;
+    a.nb = ge.gp.nb;
+    a.PP = ge.gp.PP;
+    a.vec_ok = vec_ok(x, dy, x);
+    a.lds_floats = ge.gp.lds_floats;
+    a.skip_base = skip_base;
+    a.stride = ge.gp.stride;
+    a.r_ring = 1.0f / (float)(ge.gp.g.xpitch - 4 * ge.gp.g.tiles_x);
+    for (int l = 0; l <= kMaxLevels; ++l) {
+        a.dy_off[l] = ge.gp.dy_off[l];
+        a.dy_pitch[l] = ge.gp.dy_pitch[l];
+        a.dy_band[l] = ge.gp.dy_band[l];
+    }
+    a.g = ge.gp.g;
+    return hip_status(wtc::launch_grad(d.k, d.dtype, a, ge.gp.nchunks * d.C, stream));
+}
+
 wtconv_status partials_impl(const wtconv_desc& d, const void* x, const void* dy, const wtc::ParamPtrs& p,
                             void* dx, char* ws, int skip_base, hipStream_t stream)
 {
+    const GradExec ge = choose_grad(d);
+    if (ge.use) {
+        const wtconv_status st = grad_pass(d, ge, x, dy, reinterpret_cast<float*>(ws), skip_base, stream);
+        if (st != WTCONV_OK || !dx) return st;
+        // dx: the forward pass on dy with every kernel rotated by 180 degrees
+        wtc::ParamPtrs pr = p;
+        pr.rot = 1;
+        return forward_impl(d, dy, pr, dx, ws + grad_partial_bytes(d, ge), skip_base, stream);
+    }
     const Exec ex = choose(d, true);
     if (ex.mode == Mode::None) return WTCONV_ERR_UNSUPPORTED;
     if (ex.mode == Mode::Tiny)
@@ -613,6 +773,8 @@ wtconv_status reduce(const wtconv_desc& d, int L, int nchunks, const wtc::ParamP
 wtconv_status finalize_impl(const wtconv_desc& d, const wtc::ParamPtrs& p, const Grads& gr, const char* ws,
                             int skip_base, hipStream_t stream)
 {
+    const GradExec ge = choose_grad(d);
+    if (ge.use) return reduce(d, d.L, ge.gp.nchunks, p, gr, ws, skip_base, stream);
     const Exec ex = choose(d, true);
     switch (ex.mode) {
         case Mode::None: return WTCONV_ERR_UNSUPPORTED;

@@ -1,0 +1,371 @@
+// Kernel-gradient pass of the WTConv backward for gfx950 (MI355X).
+//
+// eq. (foldgrad): the gradient of a folded kernel is the correlation of the
+// upstream gradient at its convolution output with that convolution's input.
+// For the base path that is
+//   G0[p][t] = sum over pixels of dy(y, x) * x(y + p - R, x + t - R),
+// and for level l, band q, the same correlation between the level-l band-q
+// coefficients of dy and of x on the ceil(H / 2^l) x ceil(W / 2^l) grid, zero
+// outside it (backward through the synthesis of Algorithm 1 is the analysis,
+// Section 2.2, so the upstream gradient of Z_l is the Haar pyramid of dy).
+// dx is not formed here: it is the forward pass on dy with rotated kernels.
+//
+// One workgroup owns channel c and a run of batch planes. Per batch of PP
+// resident planes:
+//   1. each thread loads one 4x4 pixel block of x and of dy. x goes to LDS
+//      with its Haar levels 1-2 (the zero-haloed layout of the fused kernels);
+//      dy stays in registers with its level-1 (2x2 sites x 4 bands) and
+//      level-2 (one site) butterflies;
+//   2. base correlation of the thread's dy block with the x window around it;
+//      the deeper x levels by the butterfly in LDS;
+//   3. dy levels 1-2 written to a compact pyramid (level 1 over the x plane,
+//      which is not read any more, when it fits there), deeper dy levels by the
+//      butterfly;
+//   4. level correlations, one band per wavefront: levels 1 and 2 over T x T
+//      site tiles into per-lane registers, deeper levels row by row.
+// The sums stay in registers across the workgroup's planes and are reduced
+// once, in a fixed order, into the workgroup's partials (the layout of the
+// fused backward, so the same finalize applies). Both pyramids are
+// unnormalised (2^l x the orthonormal coefficients); the finalize removes the
+// resulting 4^l exactly.
+#include "wtconv_fused.h"
+
+namespace wtc {
+namespace {
+
+// T x T consecutive-row tile of a compact array (row pitch a multiple of 4,
+// i0 a multiple of T), read with 16- or 8-byte loads.
+template <int T>
+DEV void load_tile(const float* __restrict__ p, int pitch, int j0, int i0, float (&v)[T][T])
+{
+#pragma unroll
+    for (int r = 0; r < T; ++r) {
+        const float* row = p + (j0 + r) * pitch + i0;
+        if constexpr (T == 4) {
+            const float4 f = *reinterpret_cast<const float4*>(row);
+            v[r][0] = f.x, v[r][1] = f.y, v[r][2] = f.z, v[r][3] = f.w;
+        } else if constexpr (T == 2) {
+            const float2 f = *reinterpret_cast<const float2*>(row);
+            v[r][0] = f.x, v[r][1] = f.y;
+        } else {
+            v[r][0] = row[0];
+        }
+    }
+}
+
+// Compact dy level of a plane region.
+struct DyLevel {
+    int off, pitch, band;
+};
+
+// Level correlation of band q over T x T site tiles of every resident plane:
+//   acc[p][t] += sum over sites s of dY(s) * X(s + (p - R, t - R)),
+// dY from the compact dy pyramid, X from the zero-haloed x pyramid.
+template <int K, int T>
+DEV void grad_band_tiles(const float* __restrict__ region0, int stride, const LevelGeom& xl, DyLevel dl, int q,
+                         int np, float (&acc)[K * K], int lane)
+{
+    const int tx = xl.ew / T;
+    const int per = tx * (xl.eh / T);
+    for (int it = lane; it < np * per; it += 64) {
+        const TileIdx ti = tile_at(it, per, xl.r_tper, tx, xl.r_tx, T);
+        const float* base = region0 + ti.p * stride;
+        float ctr[T][T];
+        load_tile<T>(base + dl.off + q * dl.band, dl.pitch, ti.j0, ti.i0, ctr);
+        corr_tile<K, T>(base + xl.off + q * xl.band, xl.pitch, ti.j0, ti.i0, ctr, acc);
+    }
+}
+
+template <int K>
+DEV void grad_band(const float* region0, int stride, const LevelGeom& xl, DyLevel dl, int q, int np,
+                   float (&acc)[K * K], int lane)
+{
+    if (xl.T == 4)
+        grad_band_tiles<K, 4>(region0, stride, xl, dl, q, np, acc, lane);
+    else if (xl.T == 2)
+        grad_band_tiles<K, 2>(region0, stride, xl, dl, q, np, acc, lane);
+    else
+        grad_band_tiles<K, 1>(region0, stride, xl, dl, q, np, acc, lane);
+}
+
+// One CW-site chunk of a site row for the row-wise correlation below:
+//   acc[t] += sum_i dY[i] * X[i + t] (X read from its array column i0 - R).
+template <int K, int CW>
+DEV void grad_row_chunk(const float* __restrict__ dr, const float* __restrict__ xr, float (&acc)[K])
+{
+    constexpr int R = K / 2;
+    constexpr int NX = ceil4c(CW + 2 * R);
+    float d[CW], xv[NX];
+#pragma unroll
+    for (int v = 0; v < CW / 4; ++v) {
+        const float4 f = reinterpret_cast<const float4*>(dr)[v];
+        d[4 * v] = f.x, d[4 * v + 1] = f.y, d[4 * v + 2] = f.z, d[4 * v + 3] = f.w;
+    }
+#pragma unroll
+    for (int v = 0; v < NX / 4; ++v) {
+        const float4 f = reinterpret_cast<const float4*>(xr)[v];
+        xv[4 * v] = f.x, xv[4 * v + 1] = f.y, xv[4 * v + 2] = f.z, xv[4 * v + 3] = f.w;
+    }
+#pragma unroll
+    for (int i = 0; i < CW; ++i)
+#pragma unroll
+        for (int t = 0; t < K; ++t) acc[t] = __builtin_fmaf(d[i], xv[i + t], acc[t]);
+}
+
+// Level correlation of band q of a deep level, by rows: lane (tap row p, row
+// group rg) keeps the K sums G[p][0..K-1] over the site rows j = rg, rg + NG,
+// ... of every resident plane, walking each row in CW-site chunks; sites past
+// the grid width are zero on both sides. The row groups are summed with a
+// fixed xor tree and added to one LDS slot per tap (only this wavefront
+// touches the slot), so the result does not depend on timing.
+template <int K>
+DEV void grad_band_rows(const float* __restrict__ region0, int stride, const LevelGeom& xl, DyLevel dl, int q,
+                        int np, float* __restrict__ slot, int lane)
+{
+    constexpr int R = K / 2;
+    constexpr int PS = K <= 1 ? 1 : (K <= 2 ? 2 : (K <= 4 ? 4 : 8));  // lanes per row group
+    constexpr int NG = 64 / PS;                                        // row groups
+    const int p = lane & (PS - 1), rg = lane / PS;
+    const bool active = p < K;
+    const int prow = active ? p : R;  // inactive lanes read a valid row and are dropped below
+    float acc[K];
+#pragma unroll
+    for (int t = 0; t < K; ++t) acc[t] = 0.f;
+    for (int pp = 0; pp < np; ++pp) {
+        const float* db = region0 + pp * stride + dl.off + q * dl.band;
+        const float* xb = region0 + pp * stride + xl.off + q * xl.band;
+        for (int j = rg; j < xl.h; j += NG) {
+            const float* dr = db + j * dl.pitch;           // site row j, column 0
+            const float* xr = xb + (j + prow) * xl.pitch;  // site row j + p - R, array column 0
+            if (xl.w <= 8) {
+                grad_row_chunk<K, 8>(dr, xr, acc);
+            } else {
+                for (int i0 = 0; i0 < xl.w; i0 += 16) grad_row_chunk<K, 16>(dr + i0, xr + i0, acc);
+            }
+        }
+    }
+#pragma unroll
+    for (int t = 0; t < K; ++t)
+#pragma unroll
+        for (int m = PS; m < 64; m <<= 1) acc[t] += __shfl_xor(acc[t], m, 64);
+    if (rg == 0 && active) {
+#pragma unroll
+        for (int t = 0; t < K; ++t) slot[p * K + t] += acc[t];
+    }
+}
+
+// Zero the part of a plane's x region that the block loads do not write (the
+// halo ring and the tile-alignment margin). Needed when the compact dy level 1
+// was stored over the x plane in the previous batch.
+DEV void zero_x_ring(float* __restrict__ reg, const PlaneGeom& g, int R, float r_sw, int tid)
+{
+    const int zy = 4 * g.tiles_y, zx = 4 * g.tiles_x;
+    const int n_top = R * g.xpitch;
+    const int n_bot = (g.xrows - R - zy) * g.xpitch;
+    const int sw = g.xpitch - zx;  // ring columns of a middle row
+    const int n = n_top + n_bot + zy * sw;
+    for (int e = tid; e < n; e += kThreads) {
+        int pos;
+        if (e < n_top) {
+            pos = e;
+        } else if (e < n_top + n_bot) {
+            pos = (R + zy) * g.xpitch + (e - n_top);
+        } else {
+            const int k = e - n_top - n_bot;
+            const int row = fdiv(k, r_sw), col = k - row * sw;
+            pos = (R + row) * g.xpitch + (col < R ? col : zx + col);
+        }
+        reg[pos] = 0.f;
+    }
+}
+
+// At least three waves per SIMD (168 VGPRs) for k <= 5: with three
+// workgroups per CU (the LDS budget of the planner) each SIMD then holds one
+// wavefront of each.
+template <int K>
+constexpr int grad_waves_per_simd() { return K <= 5 ? 3 : 2; }
+
+template <int K, typename ST>
+__global__ void __launch_bounds__(kThreads, grad_waves_per_simd<K>()) grad_kernel(const GradArgs a)
+{
+    constexpr int R = K / 2, KK = K * K;
+    extern __shared__ float4 lds4[];
+    float* lds = reinterpret_cast<float*>(lds4);
+
+    const PlaneGeom& g = a.g;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int C = a.C;
+    const int c = blockIdx.x % C;
+    const int chunk = blockIdx.x / C;
+    const int b_begin = chunk * a.nb;
+    const int b_end = min(a.B, b_begin + a.nb);
+    const int L = g.L;
+    const long HW = (long)g.H * g.W;
+    const bool skip_base = a.skip_base != 0;
+    const bool vec = a.vec_ok != 0 && (g.W % 4) == 0;
+    const bool alias1 = L >= 1 && a.dy_off[1] == 0;  // dy level 1 is stored over the x plane
+    const int q = wave;                              // the subband this wavefront correlates
+
+    // LDS: [deep-level kernel-gradient sums][plane regions]
+    const int gc_floats = L > 2 ? ceil4c((L - 2) * 4 * KK) : 0;
+    float* gco = lds;
+    float* planes = lds + gc_floats;
+    const int stride = a.stride;
+
+    const ST* xs = reinterpret_cast<const ST*>(a.x);
+    const ST* dys = reinterpret_cast<const ST*>(a.dy);
+
+    for (int i = tid; i < a.lds_floats / 4; i += kThreads) lds4[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+    __syncthreads();
+
+    float g0[KK], g1[KK], g2[KK];
+#pragma unroll
+    for (int t = 0; t < KK; ++t) g0[t] = g1[t] = g2[t] = 0.f;
+
+    const int per = g.tiles_x * g.tiles_y;
+    for (int b0 = b_begin; b0 < b_end; b0 += a.PP) {
+        const int np = min(a.PP, b_end - b0);
+        const bool mine = tid < np * per;  // at most one block per thread (planned on the host)
+        const TileIdx ti = tile_at(mine ? tid : 0, per, g.r_tiles, g.tiles_x, g.r_tiles_x, 4);
+        float* reg = planes + ti.p * stride;
+
+        // 1. x block -> LDS with its levels 1-2; dy block and its levels 1-2 in registers
+        if (alias1 && b0 != b_begin)
+            for (int p = 0; p < np; ++p) zero_x_ring(planes + p * stride, g, R, a.r_ring, tid);
+        float dyb[4][4];
+        if (mine) {
+            const long plane = (long)(b0 + ti.p) * C + c;
+            float v[4][4];
+            fetch_block<ST>(xs + plane * HW, g.H, g.W, ti.j0, ti.i0, vec, v);
+            store_block<K>(v, reg, g, ti.j0, ti.i0);
+            fetch_block<ST>(dys + plane * HW, g.H, g.W, ti.j0, ti.i0, vec, dyb);
+        }
+        __syncthreads();
+
+        // 2. base correlation; x level 3
+        if (mine && !skip_base) corr_tile<K, 4>(reg, g.xpitch, ti.j0, ti.i0, dyb, g0);
+        if (L >= 3) {
+            const LevelGeom& lg = g.lv[3];
+            const LevelGeom& lp = g.lv[2];
+            analysis_level(planes + lp.off, lp.pitch, planes + lg.off, lg, R, np, stride, tid);
+        }
+        __syncthreads();
+
+        // 3. dy levels 1-2 -> compact pyramid; x level 4
+        if (mine) {
+            float d1[2][2][4], d2[4];
+#pragma unroll
+            for (int ya = 0; ya < 2; ++ya)
+#pragma unroll
+                for (int xb = 0; xb < 2; ++xb)
+                    butterfly(dyb[2 * ya][2 * xb], dyb[2 * ya][2 * xb + 1], dyb[2 * ya + 1][2 * xb],
+                              dyb[2 * ya + 1][2 * xb + 1], d1[ya][xb]);
+            butterfly(d1[0][0][0], d1[0][1][0], d1[1][0][0], d1[1][1][0], d2);
+            if (L >= 1) {
+#pragma unroll
+                for (int bq = 0; bq < 4; ++bq)
+#pragma unroll
+                    for (int ya = 0; ya < 2; ++ya) {
+                        const float pair[2] = {d1[ya][0][bq], d1[ya][1][bq]};
+                        st_row<true, 2>(reg + a.dy_off[1] + bq * a.dy_band[1] + ((ti.j0 >> 1) + ya) * a.dy_pitch[1] +
+                                            (ti.i0 >> 1),
+                                        pair);
+                    }
+            }
+            if (L >= 2) {
+                float* o = reg + a.dy_off[2] + (ti.j0 >> 2) * a.dy_pitch[2] + (ti.i0 >> 2);
+#pragma unroll
+                for (int bq = 0; bq < 4; ++bq) o[bq * a.dy_band[2]] = d2[bq];
+            }
+        }
+        if (L >= 4) {
+            const LevelGeom& lg = g.lv[4];
+            const LevelGeom& lp = g.lv[3];
+            analysis_level(planes + lp.off, lp.pitch, planes + lg.off, lg, R, np, stride, tid);
+        }
+        __syncthreads();
+
+        // deeper levels: dy level l (compact, from dy level l - 1) and x level l + 2
+        for (int l = 3; l <= L; ++l) {
+            LevelGeom dg = g.lv[l];
+            dg.pitch = a.dy_pitch[l];
+            dg.band = a.dy_band[l];
+            analysis_level(planes + a.dy_off[l - 1], a.dy_pitch[l - 1], planes + a.dy_off[l], dg, 0, np, stride, tid);
+            if (l + 2 <= L) {
+                const LevelGeom& lg = g.lv[l + 2];
+                const LevelGeom& lp = g.lv[l + 1];
+                analysis_level(planes + lp.off, lp.pitch, planes + lg.off, lg, R, np, stride, tid);
+            }
+            __syncthreads();
+        }
+
+        // 4. level correlations, band q per wavefront
+        for (int l = 1; l <= L; ++l) {
+            const LevelGeom& xl = g.lv[l];
+            const DyLevel dl = {a.dy_off[l], a.dy_pitch[l], a.dy_band[l]};
+            if (l == 1)
+                grad_band<K>(planes, stride, xl, dl, q, np, g1, lane);
+            else if (l == 2)
+                grad_band<K>(planes, stride, xl, dl, q, np, g2, lane);
+            else
+                grad_band_rows<K>(planes, stride, xl, dl, q, np, gco + ((l - 3) * 4 + q) * KK, lane);
+        }
+        __syncthreads();
+    }
+
+    // fixed-order reduction of the workgroup's sums into its partials
+    const int NP = KK * (1 + 4 * L);
+    float* red = planes;  // the plane regions are free now
+#pragma unroll
+    for (int t = 0; t < KK; ++t) {
+        const float v0 = wave_sum(g0[t]);
+        const float v1 = wave_sum(g1[t]);
+        const float v2 = wave_sum(g2[t]);
+        if (lane == 0) {
+            red[wave * KK + t] = v0;
+            red[(kWaves + wave) * KK + t] = v1;
+            red[(2 * kWaves + wave) * KK + t] = v2;
+        }
+    }
+    __syncthreads();
+    float* dst = a.partial + ((long)chunk * C + c) * NP;
+    for (int t = tid; t < KK; t += kThreads) dst[t] = ((red[t] + red[KK + t]) + red[2 * KK + t]) + red[3 * KK + t];
+    // levels 1-2: band q's sums came from wavefront q
+    for (int i = tid; i < 4 * KK * min(L, 2); i += kThreads) dst[KK + i] = red[kWaves * KK + i];
+    for (int i = tid; i < 4 * KK * (L - 2); i += kThreads) dst[KK + 8 * KK + i] = gco[i];
+}
+
+template <int K, typename ST>
+hipError_t launch_grad_t(const GradArgs& a, int grid, hipStream_t s)
+{
+    const size_t bytes = (size_t)a.lds_floats * sizeof(float);
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&grad_kernel<K, ST>),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((grad_kernel<K, ST>), dim3(grid), dim3(kThreads), bytes, s, a);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_grad(int k, wtconv_dtype dt, const GradArgs& a, int grid, hipStream_t s)
+{
+#define WTC_GRAD_CASE(KV)                                                         \
+    case KV:                                                                      \
+        switch (dt) {                                                             \
+            case WTCONV_F32: return launch_grad_t<KV, float>(a, grid, s);         \
+            case WTCONV_BF16: return launch_grad_t<KV, uint16_t>(a, grid, s);     \
+            case WTCONV_F16: return launch_grad_t<KV, _Float16>(a, grid, s);      \
+        }                                                                         \
+        break;
+    switch (k) {
+        WTC_GRAD_CASE(1)
+        WTC_GRAD_CASE(3)
+        WTC_GRAD_CASE(5)
+        WTC_GRAD_CASE(7)
+    }
+#undef WTC_GRAD_CASE
+    return hipErrorInvalidValue;
+}
+
+}  // namespace wtc

@@ -54,6 +54,11 @@ struct ParamPtrs {
     const float* s0;  // [C]
     const float* lw[kMaxLevels];  // [4C][k][k] per level
     const float* ls[kMaxLevels];  // [4C] per level
+    // 1: the forward kernels fold every kernel rotated by 180 degrees. The
+    // forward pass on dy with rotated kernels is dx (the adjoint of a "same"
+    // correlation is the correlation with the rotated kernel, and synthesis
+    // and analysis are each other's transposes).
+    int rot;
 };
 
 struct FusedArgs {
@@ -121,6 +126,31 @@ struct ReduceArgs {
     float* dls[kMaxLevels];
 };
 
+// Kernel-gradient pass (wtconv_grad.hip): one workgroup owns channel c and a
+// run of nb batch planes of it, PP resident at once, at most one 4x4 pixel
+// block per thread per batch. The x side is held in LDS with zero halos (the
+// layout `g` of the fused kernels: the correlation windows are read there);
+// the dy side is the correlation centre: its pixels and levels 1-2 stay in the
+// registers of the thread that loaded them, and its level pyramid is stored
+// compact (no halo): level l band q site (j, i) at
+// dy_off[l] + q * dy_band[l] + j * dy_pitch[l] + i within a plane's region.
+// Level 1 of the dy side is written over the x plane (dy_off[1] == 0) once
+// the base correlation no longer needs it, when it fits there.
+struct GradArgs {
+    const void* x;
+    const void* dy;
+    float* partial;  // [nchunks][C][NP] kernel-gradient partials, resident layout
+    int B, C;
+    int nb, PP;
+    int vec_ok;      // 1 if both plane bases allow 16-byte (f32) / 8-byte (16-bit) loads
+    int lds_floats;
+    int skip_base;   // 1: no base-kernel gradient (coarse sub-problem)
+    int stride;      // floats per plane region (x side + dy side)
+    float r_ring;    // 1 / (xpitch - 4 * tiles_x): ring columns of a middle row of the x plane
+    int dy_off[kMaxLevels + 1], dy_pitch[kMaxLevels + 1], dy_band[kMaxLevels + 1];
+    PlaneGeom g;
+};
+
 // Number of kernel-gradient floats per (chunk, channel): base k*k, then
 // levels 1..L x bands 0..3 x k*k.
 inline int partial_floats_per_channel(int k, int L) { return k * k * (1 + 4 * L); }
@@ -128,6 +158,7 @@ inline int partial_floats_per_channel(int k, int L) { return k * k * (1 + 4 * L)
 hipError_t launch_forward(int k, wtconv_dtype dt, const FusedArgs& a, int grid, hipStream_t s);
 hipError_t launch_backward(int k, wtconv_dtype dt, const FusedArgs& a, int grid, hipStream_t s);
 hipError_t launch_reduce(const ReduceArgs& a, hipStream_t s);
+hipError_t launch_grad(int k, wtconv_dtype dt, const GradArgs& a, int grid, hipStream_t s);
 hipError_t launch_carrier(wtconv_dtype dt, const CarrierArgs& a, hipStream_t s);
 hipError_t launch_tiny(int k, wtconv_dtype dt, bool bwd, const TinyArgs& a, hipStream_t s);
 size_t tiny_lds_bytes(int k, int L, bool bwd);

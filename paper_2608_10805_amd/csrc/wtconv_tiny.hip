@@ -270,9 +270,11 @@ __global__ void __launch_bounds__(256) tiny_kernel(const TinyArgs a)
 
     for (int i = tid; i < 4 * kTStage / 4; i += 256) tlds4[i] = make_float4(0.f, 0.f, 0.f, 0.f);
     // eq. (fold): base s0*W0; level l band q: s_l*W_l*4^-l
+    const bool rot = !BWD && a.p.rot != 0;  // forward pass computing dx: taps reversed
     for (int i = tid; i < nch * nrows * KK; i += 256) {
         const int cl = i / (nrows * KK), r = i - cl * (nrows * KK);
-        const int row = r / KK, t = r - row * KK, cc = c0 + cl;
+        const int row = r / KK, tt = r - row * KK, cc = c0 + cl;
+        const int t = rot ? KK - 1 - tt : tt;
         float v;
         if (row == 0) {
             v = a.p.s0[cc] * a.p.w0[cc * KK + t];

@@ -84,6 +84,30 @@ def test_backward_without_dx_matches():
     check_backward(3, 4, 21, 19, 5, 3, "f32", need_dx=False)
 
 
+# Planes above 16 x 16 with L >= 2 take the gradient pass (dx as the forward
+# pass on dy with rotated kernels, kernel gradients from the dedicated pass).
+# One resident plane per batch with several batches per workgroup stores the
+# dy level-1 pyramid over the x plane and re-zeroes its halo ring between
+# batches; the cases also cover odd sizes whose tiles do not divide the grid,
+# k = 3 and 7, 16-bit storage and deep levels down to 1 x 1 grids.
+GRAD = [
+    (3, 512, 48, 48, 5, 3, "f32"),
+    (3, 300, 50, 46, 3, 2, "f32"),
+    (3, 400, 52, 52, 7, 4, "bf16"),
+    (2, 3, 45, 61, 5, 6, "f32"),
+    (6, 5, 30, 18, 5, 2, "f16"),
+]
+
+
+@pytest.mark.parametrize("B,C,H,W,k,L,dtype", GRAD)
+def test_grad_pass_backward(B, C, H, W, k, L, dtype):
+    check_backward(B, C, H, W, k, L, dtype)
+
+
+def test_grad_pass_backward_without_dx():
+    check_backward(3, 512, 48, 48, 5, 3, "f32", need_dx=False)
+
+
 def _sample_planes(B, C, n, rng):
     picks = {(0, 0), (B - 1, C - 1)}
     while len(picks) < n:
