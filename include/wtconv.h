@@ -4,16 +4,17 @@
  * The operator (Aflalo et al., Section 2.1, Algorithm 1) maps an input
  * x[B][C][H][W] to y[B][C][H][W]:
  *
- *   y = s0 * (x (*) W0) + R,     R = sum over levels l = 1..L of the Haar
- *                                    synthesis of Z_l,
+ *   y = s0 * (x (*) W0 + b0) + R,  R = sum over levels l = 1..L of the Haar
+ *                                      synthesis of Z_l,
  *   Z_l = s_l * (Y_l (*) W_l),   Y_l = one orthonormal 2x2 Haar analysis
  *                                    level applied to the raw LL band of
  *                                    level l-1 (Y_1 from x),
  *
  * where (*) is the depthwise k x k "same" cross-correlation with zero padding
  * (PyTorch conv2d semantics), W0 is one k x k kernel per channel, W_l one
- * k x k kernel per subband channel (4C of them), s0 one scale per channel and
- * s_l one scale per subband channel. The bias of Algorithm 1 is zero here.
+ * k x k kernel per subband channel (4C of them), s0 one scale per channel,
+ * b0 one bias per channel (the base bias of Algorithm 1, optional: NULL means
+ * zero) and s_l one scale per subband channel.
  * Odd H or W are zero-padded at the bottom/right before each analysis level
  * and cropped after synthesis, which is the same as zero-extending x: level l
  * lives on a ceil(H/2^l) x ceil(W/2^l) grid.
@@ -26,8 +27,9 @@
  * The kernels compute the operator in one pass per plane with the three
  * reformulations of Section 4: Haar analysis recomputed on chip (Section
  * 4.1), the bit-indexed closed-form synthesis of Proposition 2 (Section 4.2),
- * and the scales folded into the kernels (eq. fold, Section 4.3). The backward
- * pass recovers the unfolded parameter gradients with eq. (foldgrad).
+ * and the scales folded into the kernels and the bias (eq. fold, Section 4.3).
+ * The backward pass recovers the unfolded parameter gradients with
+ * eq. (foldgrad).
  *
  * Conventions common to all entry points:
  *   - Tensors are NCHW-contiguous device pointers. x, y, dy and dx have the
@@ -98,9 +100,10 @@ size_t wtconv_forward_workspace_bytes(const wtconv_desc* desc);
  * Forward pass, Algorithm 1 (Section 2.1).
  *   x            [B][C][H][W] dtype
  *   base_w       [C][k][k] float32           base_scale [C] float32
+ *   base_bias    [C] float32, or NULL for no bias
  *   level_w      host array of L device ptrs, each [4C][k][k] float32
  *   level_scale  host array of L device ptrs, each [4C] float32
- *   y            [B][C][H][W] dtype; must not overlap x
+ *   y            [B][C][H][W] dtype; must not overlap any input
  *   workspace    device memory of at least wtconv_forward_workspace_bytes(desc)
  *                bytes, 16-byte aligned; may be NULL when that size is 0. Its
  *                contents are scratch.
@@ -110,7 +113,7 @@ size_t wtconv_forward_workspace_bytes(const wtconv_desc* desc);
  * workspace, the base path and level 1 run on tiles with a halo).
  */
 wtconv_status wtconv_forward(const wtconv_desc* desc, const void* x, const float* base_w,
-                             const float* base_scale, const float* const* level_w,
+                             const float* base_scale, const float* base_bias, const float* const* level_w,
                              const float* const* level_scale, void* y, void* workspace,
                              size_t workspace_bytes, hipStream_t stream);
 
@@ -120,20 +123,27 @@ size_t wtconv_backward_workspace_bytes(const wtconv_desc* desc);
 /*
  * Backward pass: gradients of sum(y * dy) with respect to x and every
  * parameter (Section 2.2 for the Haar steps, eq. foldgrad of Section 4.3 for
- * the folded scales).
+ * the folded scales and bias).
  *   x, dy              [B][C][H][W] dtype
+ *   base_bias          [C] float32 or NULL (zero): it enters d_base_scale
+ *                      (d s0 = <G0, W0> + b0 * sum(dy))
  *   dx                 [B][C][H][W] dtype, or NULL to skip the input gradient
  *   d_base_w [C][k][k], d_base_scale [C]                           float32
+ *   d_base_bias [C] float32 (s0 * sum(dy) per channel), or NULL to skip it
  *   d_level_w / d_level_scale: host arrays of L device ptrs, [4C][k][k] / [4C]
  *   workspace          device memory of at least
  *                      wtconv_backward_workspace_bytes(desc) bytes (16-byte
  *                      aligned); its contents are scratch
  * Outputs must not overlap the inputs, each other or the workspace.
+ * For planes above 16 x 16 with L >= 2, dx is the forward pass on dy with
+ * every kernel rotated by 180 degrees (the adjoint of the operator) and the
+ * kernel gradients come from a separate correlation pass over x and dy; for
+ * other shapes one fused pass per plane produces both.
  */
 wtconv_status wtconv_backward(const wtconv_desc* desc, const void* x, const void* dy,
-                              const float* base_w, const float* base_scale,
+                              const float* base_w, const float* base_scale, const float* base_bias,
                               const float* const* level_w, const float* const* level_scale,
-                              void* dx, float* d_base_w, float* d_base_scale,
+                              void* dx, float* d_base_w, float* d_base_scale, float* d_base_bias,
                               float* const* d_level_w, float* const* d_level_scale,
                               void* workspace, size_t workspace_bytes, hipStream_t stream);
 
@@ -141,13 +151,16 @@ wtconv_status wtconv_backward(const wtconv_desc* desc, const void* x, const void
  * The two phases of wtconv_backward, for callers that want to schedule them
  * separately (wtconv_backward is exactly partials followed by finalize).
  *
- * wtconv_backward_partials: the fused pass over every plane. Writes dx (if
- *   dx != NULL) and per-workgroup kernel-gradient partial sums into
- *   `workspace`. Same arguments and checks as wtconv_backward.
+ * wtconv_backward_partials: the passes over every plane. Writes dx (if
+ *   dx != NULL) and per-workgroup kernel-gradient partial sums (and the sum
+ *   of dy per channel) into `workspace`. The bias does not enter this phase;
+ *   otherwise the same arguments and checks as wtconv_backward.
  * wtconv_backward_finalize: sums the partials of `workspace` in a fixed order
  *   and unfolds them into the parameter gradients (eq. foldgrad): d_base_w =
- *   s0 * G0, d_base_scale = <G0, W0>, and the same per subband channel of
- *   every level. `workspace` must hold the partials of a preceding
+ *   s0 * G0, d_base_scale = <G0, W0> + b0 * sum(dy), d_base_bias = s0 *
+ *   sum(dy) (if not NULL), and d_level_w = s_l * G_l, d_level_scale =
+ *   <G_l, W_l> per subband channel of every level. `workspace` must hold the
+ *   partials of a preceding
  *   wtconv_backward_partials call with the same descriptor and parameters,
  *   enqueued earlier on the same stream (or otherwise ordered before it).
  */
@@ -158,10 +171,10 @@ wtconv_status wtconv_backward_partials(const wtconv_desc* desc, const void* x, c
                                        hipStream_t stream);
 
 wtconv_status wtconv_backward_finalize(const wtconv_desc* desc, const float* base_w, const float* base_scale,
-                                       const float* const* level_w, const float* const* level_scale,
-                                       float* d_base_w, float* d_base_scale, float* const* d_level_w,
-                                       float* const* d_level_scale, const void* workspace,
-                                       size_t workspace_bytes, hipStream_t stream);
+                                       const float* base_bias, const float* const* level_w,
+                                       const float* const* level_scale, float* d_base_w, float* d_base_scale,
+                                       float* d_base_bias, float* const* d_level_w, float* const* d_level_scale,
+                                       const void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 /* Static, human-readable name of a status code. */
 const char* wtconv_status_string(wtconv_status status);

@@ -49,18 +49,18 @@ def load():
     lib = ctypes.CDLL(LIB_PATH)
     lib.wtconv_forward_workspace_bytes.argtypes = [ctypes.POINTER(Desc)]
     lib.wtconv_forward_workspace_bytes.restype = ctypes.c_size_t
-    lib.wtconv_forward.argtypes = [ctypes.POINTER(Desc), _P, _P, _P, _PP, _PP, _P, _P, ctypes.c_size_t, _P]
+    lib.wtconv_forward.argtypes = [ctypes.POINTER(Desc), _P, _P, _P, _P, _PP, _PP, _P, _P, ctypes.c_size_t, _P]
     lib.wtconv_forward.restype = ctypes.c_int
     lib.wtconv_backward_workspace_bytes.argtypes = [ctypes.POINTER(Desc)]
     lib.wtconv_backward_workspace_bytes.restype = ctypes.c_size_t
-    lib.wtconv_backward.argtypes = [ctypes.POINTER(Desc), _P, _P, _P, _P, _PP, _PP, _P, _P, _P, _PP, _PP, _P,
-                                    ctypes.c_size_t, _P]
+    lib.wtconv_backward.argtypes = [ctypes.POINTER(Desc), _P, _P, _P, _P, _P, _PP, _PP, _P, _P, _P, _P, _PP, _PP,
+                                    _P, ctypes.c_size_t, _P]
     lib.wtconv_backward.restype = ctypes.c_int
     lib.wtconv_backward_partials.argtypes = [ctypes.POINTER(Desc), _P, _P, _P, _P, _PP, _PP, _P, _P,
                                              ctypes.c_size_t, _P]
     lib.wtconv_backward_partials.restype = ctypes.c_int
-    lib.wtconv_backward_finalize.argtypes = [ctypes.POINTER(Desc), _P, _P, _PP, _PP, _P, _P, _PP, _PP, _P,
-                                             ctypes.c_size_t, _P]
+    lib.wtconv_backward_finalize.argtypes = [ctypes.POINTER(Desc), _P, _P, _P, _PP, _PP, _P, _P, _P, _PP, _PP,
+                                             _P, ctypes.c_size_t, _P]
     lib.wtconv_backward_finalize.restype = ctypes.c_int
     lib.wtconv_status_string.argtypes = [ctypes.c_int]
     lib.wtconv_status_string.restype = ctypes.c_char_p
@@ -96,10 +96,11 @@ def wtconv_forward_workspace_bytes(desc: Desc) -> int:
     return int(load().wtconv_forward_workspace_bytes(ctypes.byref(desc)))
 
 
-def wtconv_forward(desc: Desc, x, base_w, base_scale, level_w, level_scale, y, workspace, workspace_bytes,
-                   stream) -> int:
-    """Raw call: pointers are integers (device addresses); level_* are lists of addresses."""
-    return load().wtconv_forward(ctypes.byref(desc), x, base_w, base_scale, _ptr_array(level_w),
+def wtconv_forward(desc: Desc, x, base_w, base_scale, base_bias, level_w, level_scale, y, workspace,
+                   workspace_bytes, stream) -> int:
+    """Raw call: pointers are integers (device addresses, base_bias may be None);
+    level_* are lists of addresses."""
+    return load().wtconv_forward(ctypes.byref(desc), x, base_w, base_scale, base_bias, _ptr_array(level_w),
                                  _ptr_array(level_scale), y, workspace, ctypes.c_size_t(workspace_bytes), stream)
 
 
@@ -107,11 +108,12 @@ def wtconv_backward_workspace_bytes(desc: Desc) -> int:
     return int(load().wtconv_backward_workspace_bytes(ctypes.byref(desc)))
 
 
-def wtconv_backward(desc: Desc, x, dy, base_w, base_scale, level_w, level_scale, dx, d_base_w, d_base_scale,
-                    d_level_w, d_level_scale, workspace, workspace_bytes, stream) -> int:
-    return load().wtconv_backward(ctypes.byref(desc), x, dy, base_w, base_scale, _ptr_array(level_w),
-                                  _ptr_array(level_scale), dx, d_base_w, d_base_scale, _ptr_array(d_level_w),
-                                  _ptr_array(d_level_scale), workspace, ctypes.c_size_t(workspace_bytes), stream)
+def wtconv_backward(desc: Desc, x, dy, base_w, base_scale, base_bias, level_w, level_scale, dx, d_base_w,
+                    d_base_scale, d_base_bias, d_level_w, d_level_scale, workspace, workspace_bytes, stream) -> int:
+    return load().wtconv_backward(ctypes.byref(desc), x, dy, base_w, base_scale, base_bias, _ptr_array(level_w),
+                                  _ptr_array(level_scale), dx, d_base_w, d_base_scale, d_base_bias,
+                                  _ptr_array(d_level_w), _ptr_array(d_level_scale), workspace,
+                                  ctypes.c_size_t(workspace_bytes), stream)
 
 
 def wtconv_backward_partials(desc: Desc, x, dy, base_w, base_scale, level_w, level_scale, dx, workspace,
@@ -121,10 +123,11 @@ def wtconv_backward_partials(desc: Desc, x, dy, base_w, base_scale, level_w, lev
                                            ctypes.c_size_t(workspace_bytes), stream)
 
 
-def wtconv_backward_finalize(desc: Desc, base_w, base_scale, level_w, level_scale, d_base_w, d_base_scale,
-                             d_level_w, d_level_scale, workspace, workspace_bytes, stream) -> int:
-    return load().wtconv_backward_finalize(ctypes.byref(desc), base_w, base_scale, _ptr_array(level_w),
-                                           _ptr_array(level_scale), d_base_w, d_base_scale,
+def wtconv_backward_finalize(desc: Desc, base_w, base_scale, base_bias, level_w, level_scale, d_base_w,
+                             d_base_scale, d_base_bias, d_level_w, d_level_scale, workspace, workspace_bytes,
+                             stream) -> int:
+    return load().wtconv_backward_finalize(ctypes.byref(desc), base_w, base_scale, base_bias, _ptr_array(level_w),
+                                           _ptr_array(level_scale), d_base_w, d_base_scale, d_base_bias,
                                            _ptr_array(d_level_w), _ptr_array(d_level_scale), workspace,
                                            ctypes.c_size_t(workspace_bytes), stream)
 
@@ -157,9 +160,10 @@ def _stream(device):
     return torch.cuda.current_stream(device).cuda_stream
 
 
-def forward(x, base_w, base_scale, level_w, level_scale, out=None, workspace=None):
+def forward(x, base_w, base_scale, level_w, level_scale, out=None, workspace=None, bias=None):
     """y = WTConv(x) on the current stream. x: [B,C,H,W] fp32/bf16/fp16 on the GPU;
-    base_w [C,k,k], base_scale [C], level_w list of [4C,k,k], level_scale list of [4C] (fp32).
+    base_w [C,k,k], base_scale [C], level_w list of [4C,k,k], level_scale list of [4C] (fp32);
+    bias: the base bias [C] (fp32) or None.
     Large planes need a device workspace; one is allocated if `workspace` is None or too small."""
     import torch
     _require(x, "x")
@@ -168,7 +172,8 @@ def forward(x, base_w, base_scale, level_w, level_scale, out=None, workspace=Non
     L = len(level_w)
     for name, t in [("base_w", base_w), ("base_scale", base_scale)] + \
             [(f"level_w[{i}]", t) for i, t in enumerate(level_w)] + \
-            [(f"level_scale[{i}]", t) for i, t in enumerate(level_scale)]:
+            [(f"level_scale[{i}]", t) for i, t in enumerate(level_scale)] + \
+            ([("bias", bias)] if bias is not None else []):
         _require(t, name, torch.float32)
     y = torch.empty_like(x) if out is None else out
     desc = make_desc(B, C, H, W, k, L, _dtype_code(x))
@@ -179,13 +184,16 @@ def forward(x, base_w, base_scale, level_w, level_scale, out=None, workspace=Non
             workspace = torch.empty(nbytes, dtype=torch.uint8, device=x.device)
         ws_ptr = workspace.data_ptr()
     _check(wtconv_forward(desc, x.data_ptr(), base_w.data_ptr(), base_scale.data_ptr(),
+                          bias.data_ptr() if bias is not None else None,
                           [t.data_ptr() for t in level_w], [t.data_ptr() for t in level_scale], y.data_ptr(),
                           ws_ptr, nbytes, _stream(x.device)))
     return y
 
 
-def backward(x, dy, base_w, base_scale, level_w, level_scale, need_dx=True, workspace=None):
-    """Gradients of sum(y * dy). Returns (dx or None, d_base_w, d_base_scale, [d_level_w], [d_level_scale])."""
+def backward(x, dy, base_w, base_scale, level_w, level_scale, need_dx=True, workspace=None, bias=None,
+             need_dbias=False):
+    """Gradients of sum(y * dy). Returns (dx or None, d_base_w, d_base_scale, [d_level_w], [d_level_scale]),
+    followed by d_bias when need_dbias. `bias` (the base bias [C] or None) enters d_base_scale."""
     import torch
     _require(x, "x")
     _require(dy, "dy", x.dtype)
@@ -203,11 +211,18 @@ def backward(x, dy, base_w, base_scale, level_w, level_scale, need_dx=True, work
     dbs = torch.empty_like(base_scale)
     dlw = [torch.empty_like(t) for t in level_w]
     dls = [torch.empty_like(t) for t in level_scale]
+    dbb = torch.empty_like(base_scale) if need_dbias else None
+    if bias is not None:
+        _require(bias, "bias", torch.float32)
     _check(wtconv_backward(desc, x.data_ptr(), dy.data_ptr(), base_w.data_ptr(), base_scale.data_ptr(),
+                           bias.data_ptr() if bias is not None else None,
                            [t.data_ptr() for t in level_w], [t.data_ptr() for t in level_scale],
                            dx.data_ptr() if dx is not None else None, dbw.data_ptr(), dbs.data_ptr(),
+                           dbb.data_ptr() if dbb is not None else None,
                            [t.data_ptr() for t in dlw], [t.data_ptr() for t in dls], workspace.data_ptr(),
                            nbytes, _stream(x.device)))
+    if need_dbias:
+        return dx, dbw, dbs, dlw, dls, dbb
     return dx, dbw, dbs, dlw, dls
 
 
@@ -244,6 +259,6 @@ class Backward:
 
     def finalize(self):
         bw, bs, _, _ = self.params
-        _check(wtconv_backward_finalize(self.desc, bw.data_ptr(), bs.data_ptr(), self._lw, self._ls,
-                                        self.dbw.data_ptr(), self.dbs.data_ptr(), self._dlw, self._dls,
+        _check(wtconv_backward_finalize(self.desc, bw.data_ptr(), bs.data_ptr(), None, self._lw, self._ls,
+                                        self.dbw.data_ptr(), self.dbs.data_ptr(), None, self._dlw, self._dls,
                                         self.workspace.data_ptr(), self.nbytes, _stream(self.device)))

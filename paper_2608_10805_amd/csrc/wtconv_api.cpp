@@ -196,12 +196,13 @@ wtconv_status check_levels(int L, const float* const* lw, const float* const* ls
     return WTCONV_OK;
 }
 
-void fill_params(wtc::ParamPtrs& p, int L, const float* w0, const float* s0, const float* const* lw,
+void fill_params(wtc::ParamPtrs& p, int L, const float* w0, const float* s0, const float* b0, const float* const* lw,
                  const float* const* ls)
 {
     memset(&p, 0, sizeof(p));
     p.w0 = w0;
     p.s0 = s0;
+    p.b0 = b0;
     for (int l = 0; l < L; ++l) {
         p.lw[l] = lw[l];
         p.ls[l] = ls[l];
@@ -212,6 +213,7 @@ void fill_params(wtc::ParamPtrs& p, int L, const float* w0, const float* s0, con
 struct Grads {
     float* dw0;
     float* ds0;
+    float* db0;  // nullable
     float* dlw[kMaxLevels];
     float* dls[kMaxLevels];
 };
@@ -427,7 +429,7 @@ bool grad_layout(const wtconv_desc& d, int PP, GradPlan& gp)
         if (g.plane_floats + extra > (1L << 28)) return false;
     }
     gp.stride = (int)(g.plane_floats + extra);
-    const long planes = std::max((long)PP * gp.stride, 12L * d.k * d.k);
+    const long planes = std::max((long)PP * gp.stride, 12L * d.k * d.k + 4);  // also the final reduction scratch
     const long total = grad_gc_floats(d) + ceil_to((int)std::min(planes, 1L << 28), 4);
     if (total > kLdsFloatsMax) return false;
     gp.lds_floats = (int)total;
@@ -719,6 +721,7 @@ wtconv_status partials_impl(const wtconv_desc& d, const void* x, const void* dy,
         // dx: the forward pass on dy with every kernel rotated by 180 degrees
         wtc::ParamPtrs pr = p;
         pr.rot = 1;
+        pr.b0 = nullptr;  // the bias does not reach dx
         return forward_impl(d, dy, pr, dx, ws + grad_partial_bytes(d, ge), skip_base, stream);
     }
     const Exec ex = choose(d, true);
@@ -763,6 +766,7 @@ wtconv_status reduce(const wtconv_desc& d, int L, int nchunks, const wtc::ParamP
     r.p = p;
     r.dw0 = gr.dw0;
     r.ds0 = gr.ds0;
+    r.db0 = skip_base ? nullptr : gr.db0;
     for (int l = 0; l < L; ++l) {
         r.dlw[l] = gr.dlw[l];
         r.dls[l] = gr.dls[l];
@@ -809,13 +813,14 @@ bool any_overlap(const Range* outs, int no, const Range* ins, int ni)
     return false;
 }
 
-int param_ranges(const wtconv_desc& d, const float* w0, const float* s0, const float* const* lw,
+int param_ranges(const wtconv_desc& d, const float* w0, const float* s0, const float* b0, const float* const* lw,
                  const float* const* ls, Range* r)
 {
     const size_t KK = (size_t)d.k * d.k;
     int n = 0;
     r[n++] = {w0, (size_t)d.C * KK * 4};
     r[n++] = {s0, (size_t)d.C * 4};
+    r[n++] = {b0, (size_t)d.C * 4};  // a null range overlaps nothing
     for (int l = 0; l < d.L; ++l) {
         r[n++] = {lw[l], (size_t)4 * d.C * KK * 4};
         r[n++] = {ls[l], (size_t)4 * d.C * 4};
@@ -833,7 +838,7 @@ wtconv_status check_workspace(size_t need, const void* ws, size_t bytes)
 
 // Shared argument checks of the backward entry points.
 wtconv_status backward_checks(const wtconv_desc* desc, const void* x, const void* dy, const float* base_w,
-                              const float* base_scale, const float* const* level_w,
+                              const float* base_scale, const float* base_bias, const float* const* level_w,
                               const float* const* level_scale, const void* dx, const void* workspace,
                               size_t workspace_bytes, const Range* extra_outs, int n_extra, size_t* need_out)
 {
@@ -846,12 +851,12 @@ wtconv_status backward_checks(const wtconv_desc* desc, const void* x, const void
     if ((st = check_workspace(need, workspace, workspace_bytes)) != WTCONV_OK) return st;
     if (need == 0) return WTCONV_ERR_WORKSPACE;  // the backward always writes partials
     const size_t act = (size_t)d.B * d.C * d.H * d.W * elem_size(d.dtype);
-    Range ins[4 + 2 * kMaxLevels];
+    Range ins[5 + 2 * kMaxLevels];
     int ni = 0;
     ins[ni++] = {x, act};
     ins[ni++] = {dy, act};
-    ni += param_ranges(d, base_w, base_scale, level_w, level_scale, ins + ni);
-    Range outs[2 + 2 + 2 * kMaxLevels];
+    ni += param_ranges(d, base_w, base_scale, base_bias, level_w, level_scale, ins + ni);
+    Range outs[2 + 3 + 2 * kMaxLevels];
     int no = 0;
     outs[no++] = {dx, act};
     outs[no++] = {workspace, need};
@@ -861,12 +866,14 @@ wtconv_status backward_checks(const wtconv_desc* desc, const void* x, const void
     return WTCONV_OK;
 }
 
-Grads grads_of(int L, float* d_base_w, float* d_base_scale, float* const* d_level_w, float* const* d_level_scale)
+Grads grads_of(int L, float* d_base_w, float* d_base_scale, float* d_base_bias, float* const* d_level_w,
+               float* const* d_level_scale)
 {
     Grads gr;
     memset(&gr, 0, sizeof(gr));
     gr.dw0 = d_base_w;
     gr.ds0 = d_base_scale;
+    gr.db0 = d_base_bias;
     for (int l = 0; l < L; ++l) {
         gr.dlw[l] = d_level_w[l];
         gr.dls[l] = d_level_scale[l];
@@ -878,7 +885,7 @@ Grads grads_of(int L, float* d_base_w, float* d_base_scale, float* const* d_leve
 
 extern "C" {
 
-int wtconv_version(void) { return 200; }
+int wtconv_version(void) { return 300; }
 
 const char* wtconv_status_string(wtconv_status s)
 {
@@ -905,7 +912,7 @@ size_t wtconv_forward_workspace_bytes(const wtconv_desc* desc)
 }
 
 wtconv_status wtconv_forward(const wtconv_desc* desc, const void* x, const float* base_w,
-                             const float* base_scale, const float* const* level_w,
+                             const float* base_scale, const float* base_bias, const float* const* level_w,
                              const float* const* level_scale, void* y, void* workspace,
                              size_t workspace_bytes, hipStream_t stream)
 {
@@ -917,11 +924,14 @@ wtconv_status wtconv_forward(const wtconv_desc* desc, const void* x, const float
     const size_t need = forward_ws(d);
     if ((st = check_workspace(need, workspace, workspace_bytes)) != WTCONV_OK) return st;
     const size_t bytes = (size_t)d.B * d.C * d.H * d.W * elem_size(d.dtype);
-    if (overlaps(x, bytes, y, bytes)) return WTCONV_ERR_ALIAS;
-    if (need && (overlaps(workspace, need, x, bytes) || overlaps(workspace, need, y, bytes)))
-        return WTCONV_ERR_ALIAS;
+    Range ins[5 + 2 * kMaxLevels];
+    int ni = 0;
+    ins[ni++] = {x, bytes};
+    ni += param_ranges(d, base_w, base_scale, base_bias, level_w, level_scale, ins + ni);
+    const Range outs[2] = {{y, bytes}, {workspace, need}};
+    if (any_overlap(outs, 2, ins, ni)) return WTCONV_ERR_ALIAS;
     wtc::ParamPtrs p;
-    fill_params(p, d.L, base_w, base_scale, level_w, level_scale);
+    fill_params(p, d.L, base_w, base_scale, base_bias, level_w, level_scale);
     return forward_impl(d, x, p, y, reinterpret_cast<char*>(workspace), 0, stream);
 }
 
@@ -939,19 +949,19 @@ wtconv_status wtconv_backward_partials(const wtconv_desc* desc, const void* x, c
                                        hipStream_t stream)
 {
     size_t need = 0;
-    const wtconv_status st = backward_checks(desc, x, dy, base_w, base_scale, level_w, level_scale, dx, workspace,
-                                             workspace_bytes, nullptr, 0, &need);
+    const wtconv_status st = backward_checks(desc, x, dy, base_w, base_scale, nullptr, level_w, level_scale, dx,
+                                             workspace, workspace_bytes, nullptr, 0, &need);
     if (st != WTCONV_OK) return st;
     wtc::ParamPtrs p;
-    fill_params(p, desc->L, base_w, base_scale, level_w, level_scale);
+    fill_params(p, desc->L, base_w, base_scale, nullptr, level_w, level_scale);
     return partials_impl(*desc, x, dy, p, dx, reinterpret_cast<char*>(workspace), 0, stream);
 }
 
 wtconv_status wtconv_backward_finalize(const wtconv_desc* desc, const float* base_w, const float* base_scale,
-                                       const float* const* level_w, const float* const* level_scale,
-                                       float* d_base_w, float* d_base_scale, float* const* d_level_w,
-                                       float* const* d_level_scale, const void* workspace,
-                                       size_t workspace_bytes, hipStream_t stream)
+                                       const float* base_bias, const float* const* level_w,
+                                       const float* const* level_scale, float* d_base_w, float* d_base_scale,
+                                       float* d_base_bias, float* const* d_level_w, float* const* d_level_scale,
+                                       const void* workspace, size_t workspace_bytes, hipStream_t stream)
 {
     wtconv_status st = check_desc(desc);
     if (st != WTCONV_OK) return st;
@@ -963,23 +973,23 @@ wtconv_status wtconv_backward_finalize(const wtconv_desc* desc, const float* bas
     const size_t need = backward_ws(d);
     if ((st = check_workspace(need, workspace, workspace_bytes)) != WTCONV_OK) return st;
     if (need == 0) return WTCONV_ERR_WORKSPACE;
-    Range ins[3 + 2 * kMaxLevels];
-    int ni = param_ranges(d, base_w, base_scale, level_w, level_scale, ins);
+    Range ins[4 + 2 * kMaxLevels];
+    int ni = param_ranges(d, base_w, base_scale, base_bias, level_w, level_scale, ins);
     ins[ni++] = {workspace, need};
-    Range outs[2 + 2 * kMaxLevels];
-    const int no = param_ranges(d, d_base_w, d_base_scale, (const float* const*)d_level_w,
+    Range outs[3 + 2 * kMaxLevels];
+    const int no = param_ranges(d, d_base_w, d_base_scale, d_base_bias, (const float* const*)d_level_w,
                                 (const float* const*)d_level_scale, outs);
     if (any_overlap(outs, no, ins, ni)) return WTCONV_ERR_ALIAS;
     wtc::ParamPtrs p;
-    fill_params(p, d.L, base_w, base_scale, level_w, level_scale);
-    return finalize_impl(d, p, grads_of(d.L, d_base_w, d_base_scale, d_level_w, d_level_scale),
+    fill_params(p, d.L, base_w, base_scale, base_bias, level_w, level_scale);
+    return finalize_impl(d, p, grads_of(d.L, d_base_w, d_base_scale, d_base_bias, d_level_w, d_level_scale),
                          reinterpret_cast<const char*>(workspace), 0, stream);
 }
 
 wtconv_status wtconv_backward(const wtconv_desc* desc, const void* x, const void* dy,
-                              const float* base_w, const float* base_scale,
+                              const float* base_w, const float* base_scale, const float* base_bias,
                               const float* const* level_w, const float* const* level_scale,
-                              void* dx, float* d_base_w, float* d_base_scale,
+                              void* dx, float* d_base_w, float* d_base_scale, float* d_base_bias,
                               float* const* d_level_w, float* const* d_level_scale,
                               void* workspace, size_t workspace_bytes, hipStream_t stream)
 {
@@ -992,19 +1002,20 @@ wtconv_status wtconv_backward(const wtconv_desc* desc, const void* x, const void
     if (!base_w || !base_scale) return WTCONV_ERR_NULL;
     if ((st = check_levels(d.L, level_w, level_scale)) != WTCONV_OK) return st;
     // the gradient outputs join the overlap check of the fused phase
-    Range grads[2 + 2 * kMaxLevels];
-    const int ng = param_ranges(d, d_base_w, d_base_scale, (const float* const*)d_level_w,
+    Range grads[3 + 2 * kMaxLevels];
+    const int ng = param_ranges(d, d_base_w, d_base_scale, d_base_bias, (const float* const*)d_level_w,
                                 (const float* const*)d_level_scale, grads);
     size_t need = 0;
-    st = backward_checks(desc, x, dy, base_w, base_scale, level_w, level_scale, dx, workspace, workspace_bytes,
-                         grads, ng, &need);
+    st = backward_checks(desc, x, dy, base_w, base_scale, base_bias, level_w, level_scale, dx, workspace,
+                         workspace_bytes, grads, ng, &need);
     if (st != WTCONV_OK) return st;
     wtc::ParamPtrs p;
-    fill_params(p, d.L, base_w, base_scale, level_w, level_scale);
+    fill_params(p, d.L, base_w, base_scale, base_bias, level_w, level_scale);
     char* ws = reinterpret_cast<char*>(workspace);
     st = partials_impl(d, x, dy, p, dx, ws, 0, stream);
     if (st != WTCONV_OK) return st;
-    return finalize_impl(d, p, grads_of(d.L, d_base_w, d_base_scale, d_level_w, d_level_scale), ws, 0, stream);
+    return finalize_impl(d, p, grads_of(d.L, d_base_w, d_base_scale, d_base_bias, d_level_w, d_level_scale), ws,
+                         0, stream);
 }
 
 }  // extern "C"

@@ -552,7 +552,7 @@ DEV void grad_and_filter(float* side_in, const float* side_aux, int stride, cons
 // Base correlation of the 4x4 tile at (y0, x0); also returns the tile's own
 // input values (the window centre), which the backward pass correlates with x.
 template <int K>
-DEV void base_tile(const float* __restrict__ xa, int xpitch, int y0, int x0, const float (&w)[K * K],
+DEV void base_tile(const float* __restrict__ xa, int xpitch, int y0, int x0, const float (&w)[K * K], float init,
                    float (&acc)[4][4], float (&ctr)[4][4])
 {
     constexpr int R = K / 2, N = Win<K, 4>::N;
@@ -575,9 +575,8 @@ DEV void base_tile(const float* __restrict__ xa, int xpitch, int y0, int x0, con
 #pragma unroll
             for (int ox = 0; ox < 4; ++ox)
 #pragma unroll
-                for (int t = 0; t < K; ++t)  // the first term is a product (no zeroed accumulator)
-                    acc[oy][ox] = (p == 0 && t == 0) ? w[0] * row[ox]
-                                                     : __builtin_fmaf(w[p * K + t], row[ox + t], acc[oy][ox]);
+                for (int t = 0; t < K; ++t)  // the first term starts from `init` (the folded bias)
+                    acc[oy][ox] = __builtin_fmaf(w[p * K + t], row[ox + t], (p == 0 && t == 0) ? init : acc[oy][ox]);
         }
     }
 }
@@ -731,6 +730,8 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(const FusedArgs a)
     const int PH = RGN ? a.real_H : g.H, PW = RGN ? a.real_W : g.W;  // the real plane
     const long HW = (long)PH * PW;
     const bool skip_base = a.skip_base != 0;
+    // eq. (fold): the folded base bias s0 * b0 starts every output pixel's sum
+    const float bias = (!BWD && !skip_base && a.p.b0) ? a.p.s0[c] * a.p.b0[c] : 0.f;
 
     // LDS: [folded weights][coarse kernel-gradient sums (backward)][planes]
     const int wt_floats = ceil4c((1 + 4 * L) * KK);
@@ -773,6 +774,7 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(const FusedArgs a)
     float g0[KK], g1[KK], g2[KK];
 #pragma unroll
     for (int t = 0; t < KK; ++t) g0[t] = g1[t] = g2[t] = 0.f;
+    float gdy = 0.f;  // backward: sum of dy over the workgroup's pixels (bias gradient)
 
     for (int b0 = b_begin; b0 < b_end; b0 += a.PP) {
         const int np = min(a.PP, b_end - b0);
@@ -854,7 +856,7 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(const FusedArgs a)
 #pragma unroll
                             for (int ox2 = 0; ox2 < 4; ++ox2) acc[oy2][ox2] = 0.f;
                     } else {
-                        base_tile<K>(reg, g.xpitch, ti.j0, ti.i0, w, acc, ctr);
+                        base_tile<K>(reg, g.xpitch, ti.j0, ti.i0, w, bias, acc, ctr);
                     }
                     Carry cr = {nullptr, 0, 0, 0, 0, 0};
                     if (a.carry) {
@@ -871,7 +873,12 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(const FusedArgs a)
                     load_center<K, 4>(reg, g.xpitch, ti.j0, ti.i0, ctr);
                 }
                 if constexpr (BWD) {
-                    if (!skip_base) corr_tile<K, 4>(side_aux + ti.p * stride, g.xpitch, ti.j0, ti.i0, ctr, g0);
+                    if (!skip_base) {
+                        corr_tile<K, 4>(side_aux + ti.p * stride, g.xpitch, ti.j0, ti.i0, ctr, g0);
+#pragma unroll
+                        for (int oy2 = 0; oy2 < 4; ++oy2)
+                            gdy += (ctr[oy2][0] + ctr[oy2][1]) + (ctr[oy2][2] + ctr[oy2][3]);
+                    }
                 }
             }
         }
@@ -880,7 +887,7 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(const FusedArgs a)
 
     if constexpr (BWD) {
         // fixed-order reduction of the kernel-gradient sums of this workgroup
-        const int NP = KK * (1 + 4 * L);
+        const int NP = partial_floats_per_channel(K, L);
         float* red = planes;  // the plane regions are free now
 #pragma unroll
         for (int t = 0; t < KK; ++t) {
@@ -893,10 +900,16 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(const FusedArgs a)
                 red[(2 * kWaves + wave) * KK + t] = v2;
             }
         }
+        const float vdy = wave_sum(gdy);
+        if (lane == 0) red[3 * kWaves * KK + wave] = vdy;
         __syncthreads();
         float* dst = a.partial + ((long)(chunk * ntiles + tile) * C + c) * NP;
         for (int t = tid; t < KK; t += kThreads)
             dst[t] = ((red[t] + red[KK + t]) + red[2 * KK + t]) + red[3 * KK + t];
+        if (tid == 0) {
+            const float* r = red + 3 * kWaves * KK;
+            dst[NP - 1] = ((r[0] + r[1]) + r[2]) + r[3];
+        }
         // register-held levels: band q's sums came from wavefront q
         for (int i = tid; i < 4 * KK * min(L, reg_levels<ONE>()); i += kThreads) dst[KK + i] = red[kWaves * KK + i];
         for (int i = 4 * KK * reg_levels<ONE>() + tid; i < 4 * L * KK; i += kThreads) dst[KK + i] = gco[i];

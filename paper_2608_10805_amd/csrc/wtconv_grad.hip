@@ -221,6 +221,7 @@ __global__ void __launch_bounds__(kThreads, grad_waves_per_simd<K>()) grad_kerne
     float g0[KK], g1[KK], g2[KK];
 #pragma unroll
     for (int t = 0; t < KK; ++t) g0[t] = g1[t] = g2[t] = 0.f;
+    float gdy = 0.f;  // sum of dy over the workgroup's pixels (bias gradient)
 
     const int per = g.tiles_x * g.tiles_y;
     for (int b0 = b_begin; b0 < b_end; b0 += a.PP) {
@@ -243,7 +244,11 @@ __global__ void __launch_bounds__(kThreads, grad_waves_per_simd<K>()) grad_kerne
         __syncthreads();
 
         // 2. base correlation; x level 3
-        if (mine && !skip_base) corr_tile<K, 4>(reg, g.xpitch, ti.j0, ti.i0, dyb, g0);
+        if (mine && !skip_base) {
+            corr_tile<K, 4>(reg, g.xpitch, ti.j0, ti.i0, dyb, g0);
+#pragma unroll
+            for (int r = 0; r < 4; ++r) gdy += (dyb[r][0] + dyb[r][1]) + (dyb[r][2] + dyb[r][3]);
+        }
         if (L >= 3) {
             const LevelGeom& lg = g.lv[3];
             const LevelGeom& lp = g.lv[2];
@@ -314,7 +319,7 @@ __global__ void __launch_bounds__(kThreads, grad_waves_per_simd<K>()) grad_kerne
     }
 
     // fixed-order reduction of the workgroup's sums into its partials
-    const int NP = KK * (1 + 4 * L);
+    const int NP = partial_floats_per_channel(K, L);
     float* red = planes;  // the plane regions are free now
 #pragma unroll
     for (int t = 0; t < KK; ++t) {
@@ -327,9 +332,15 @@ __global__ void __launch_bounds__(kThreads, grad_waves_per_simd<K>()) grad_kerne
             red[(2 * kWaves + wave) * KK + t] = v2;
         }
     }
+    const float vdy = wave_sum(gdy);
+    if (lane == 0) red[3 * kWaves * KK + wave] = vdy;
     __syncthreads();
     float* dst = a.partial + ((long)chunk * C + c) * NP;
     for (int t = tid; t < KK; t += kThreads) dst[t] = ((red[t] + red[KK + t]) + red[2 * KK + t]) + red[3 * KK + t];
+    if (tid == 0) {
+        const float* r = red + 3 * kWaves * KK;
+        dst[NP - 1] = ((r[0] + r[1]) + r[2]) + r[3];
+    }
     // levels 1-2: band q's sums came from wavefront q
     for (int i = tid; i < 4 * KK * min(L, 2); i += kThreads) dst[KK + i] = red[kWaves * KK + i];
     for (int i = tid; i < 4 * KK * (L - 2); i += kThreads) dst[KK + 8 * KK + i] = gco[i];

@@ -52,6 +52,7 @@ struct PlaneGeom {
 struct ParamPtrs {
     const float* w0;  // [C][k][k]
     const float* s0;  // [C]
+    const float* b0;  // [C] base bias, or null (zero)
     const float* lw[kMaxLevels];  // [4C][k][k] per level
     const float* ls[kMaxLevels];  // [4C] per level
     // 1: the forward kernels fold every kernel rotated by 180 degrees. The
@@ -122,6 +123,7 @@ struct ReduceArgs {
     ParamPtrs p;
     float* dw0;
     float* ds0;
+    float* db0;  // nullable
     float* dlw[kMaxLevels];
     float* dls[kMaxLevels];
 };
@@ -152,8 +154,9 @@ struct GradArgs {
 };
 
 // Number of kernel-gradient floats per (chunk, channel): base k*k, then
-// levels 1..L x bands 0..3 x k*k.
-inline int partial_floats_per_channel(int k, int L) { return k * k * (1 + 4 * L); }
+// levels 1..L x bands 0..3 x k*k, then the sum of dy over the channel's pixels
+// (the gradient of the folded base bias).
+__host__ __device__ inline int partial_floats_per_channel(int k, int L) { return k * k * (1 + 4 * L) + 1; }
 
 hipError_t launch_forward(int k, wtconv_dtype dt, const FusedArgs& a, int grid, hipStream_t s);
 hipError_t launch_backward(int k, wtconv_dtype dt, const FusedArgs& a, int grid, hipStream_t s);

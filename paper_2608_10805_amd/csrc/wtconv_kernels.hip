@@ -9,12 +9,14 @@ namespace {
 // Sum the per-workgroup partials over chunks in increasing order, then unfold
 // eq. (foldgrad): dW = s * G and ds = <G, W>, where G is the gradient of the
 // folded kernel s*W (the level partials carry an extra 4^l from the
-// unnormalised pyramids, removed here exactly). One wavefront per (channel,
-// band row); lane t owns tap t; <G, W> is a fixed-order wavefront reduction.
+// unnormalised pyramids, removed here exactly); for the base row also the bias
+// terms d b0 = s0 * sum(dy) and b0 * sum(dy) in d s0. One wavefront per
+// (channel, band row); lane t owns tap t (lane k*k the sum of dy); the
+// d(scale) dot product is a fixed-order wavefront reduction.
 __global__ void __launch_bounds__(64) reduce_kernel(const ReduceArgs a)
 {
     const int KK = a.k * a.k;
-    const int NP = KK * (1 + 4 * a.L);
+    const int NP = partial_floats_per_channel(a.k, a.L);
     const int c = blockIdx.x;
     const int band = blockIdx.y;  // 0 = base, else 1 + (l-1)*4 + q
     const int t = threadIdx.x;
@@ -57,6 +59,15 @@ __global__ void __launch_bounds__(64) reduce_kernel(const ReduceArgs a)
         G *= norm;
         dw[t] = scale * G;
         prod = G * w[t];
+    } else if (band == 0 && t == KK) {
+        // folded base bias b~ = s0 * b0: its gradient is the sum of dy, so
+        // d b0 = s0 * sum(dy) and d s0 gains b0 * sum(dy) (eq. foldgrad)
+        const float* src = a.partial + (long)c * NP + (NP - 1);
+        const long step = (long)a.C * NP;
+        float Gb = 0.f;
+        for (int ch = 0; ch < a.nchunks; ++ch) Gb += src[(long)ch * step];
+        if (a.db0) a.db0[c] = scale * Gb;
+        if (a.p.b0) prod = a.p.b0[c] * Gb;
     }
     prod = wave_sum(prod);
     if (t == 0) *ds = prod;

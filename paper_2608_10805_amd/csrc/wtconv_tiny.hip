@@ -68,8 +68,7 @@ DEV void grid_conv(const float (&u)[N * N], const float (&w)[K * K], float (&z)[
         }
 #pragma unroll
         for (int i = 0; i < N; ++i) {
-            float acc = 0.f;
-            bool first = true;
+            float acc = 0.f;  // fma(w, u, 0) rounds like the product w * u
 #pragma unroll
             for (int p = 0; p < K; ++p) {
                 const int y = j + p - R;
@@ -78,8 +77,7 @@ DEV void grid_conv(const float (&u)[N * N], const float (&w)[K * K], float (&z)[
                 for (int t = 0; t < K; ++t) {
                     const int x = i + t - R;
                     if (x < 0 || x >= N) continue;
-                    acc = first ? w[p * K + t] * u[y * N + x] : __builtin_fmaf(w[p * K + t], u[y * N + x], acc);
-                    first = false;
+                    acc = __builtin_fmaf(w[p * K + t], u[y * N + x], acc);
                 }
             }
             z[j * N + i] = acc;
@@ -91,7 +89,7 @@ DEV void grid_conv(const float (&u)[N * N], const float (&w)[K * K], float (&z)[
 // lane's column of the position-major rows `park` (rows >= `rows`: zero), so
 // the 64 outputs never occupy registers together.
 template <int K>
-DEV void grid_conv8_park(const float (&u)[64], const float (&w)[K * K], float* park, int lane, int rows)
+DEV void grid_conv8_park(const float (&u)[64], const float (&w)[K * K], float init, float* park, int lane, int rows)
 {
     constexpr int R = K / 2, N = 8;
 #pragma unroll
@@ -103,8 +101,7 @@ DEV void grid_conv8_park(const float (&u)[64], const float (&w)[K * K], float* p
         }
 #pragma unroll
         for (int i = 0; i < N; ++i) {
-            float acc = 0.f;
-            bool first = true;
+            float acc = init;  // the folded bias (zero in the backward pass)
 #pragma unroll
             for (int p = 0; p < K; ++p) {
                 const int y = j + p - R;
@@ -113,8 +110,7 @@ DEV void grid_conv8_park(const float (&u)[64], const float (&w)[K * K], float* p
                 for (int t = 0; t < K; ++t) {
                     const int x = i + t - R;
                     if (x < 0 || x >= N) continue;
-                    acc = first ? w[p * K + t] * u[y * N + x] : __builtin_fmaf(w[p * K + t], u[y * N + x], acc);
-                    first = false;
+                    acc = __builtin_fmaf(w[p * K + t], u[y * N + x], acc);
                 }
             }
             park[(j * N + i) * kTPitch + lane] = acc;
@@ -245,6 +241,15 @@ DEV void gq_put(GradQueue& q, const float (&g)[K * K], int off, float* __restric
     }
 }
 
+// Queue one value (partial-row offset `off`).
+DEV void gq_put1(GradQueue& q, float v, int off, float* __restrict__ dst, int lane, bool store)
+{
+    if (q.n + 1 > 64) gq_flush(q, dst, lane, store);
+    q.scr[lane * kTPitch + q.n] = v;
+    if (lane == 0) q.offs[q.n] = off;
+    ++q.n;
+}
+
 template <int K, typename ST, bool BWD>
 __global__ void __launch_bounds__(256) tiny_kernel(const TinyArgs a)
 {
@@ -350,7 +355,9 @@ __global__ void __launch_bounds__(256) tiny_kernel(const TinyArgs a)
             for (int i = 0; i < kTPos; ++i) mystage[i * kTPitch + lane] = 0.f;
         } else {
             load_taps<K>(mytab, trow(0, 0), false, w);
-            grid_conv8_park<K>(X, w, mystage, lane, H);
+            // eq. (fold): the folded base bias s0 * b0 starts every output pixel's sum
+            const float bias = (cvalid && a.p.b0) ? a.p.s0[c] * a.p.b0[c] : 0.f;
+            grid_conv8_park<K>(X, w, bias, mystage, lane, H);
         }
         if (L >= 1) {
             float U1[4][16], U2[4][4], U3[4];
@@ -414,7 +421,7 @@ __global__ void __launch_bounds__(256) tiny_kernel(const TinyArgs a)
         float X[kTPos], D[kTPos];
         stage_in(reinterpret_cast<const ST*>(a.aux), X);
         stage_in(reinterpret_cast<const ST*>(a.in), D);
-        const int NP = KK * nrows;
+        const int NP = partial_floats_per_channel(K, L);  // KK * nrows taps, then the sum of dy
         float* prow = a.partial + ((long)bg * a.C + (cvalid ? c : 0)) * NP;
         const bool store_g = cvalid;
         GradQueue gq = {mystage, offs + wave * 64, 0};
@@ -429,8 +436,13 @@ __global__ void __launch_bounds__(256) tiny_kernel(const TinyArgs a)
             for (int t = 0; t < KK; ++t) g[t] = 0.f;
             grid_corr<K, 8>(D, X, g, H);
             gq_put<K, 8>(gq, g, 0, prow, lane, store_g);
+            // the bias gradient: sum of this entry's dy plane (zero beyond it)
+            float sdy = 0.f;
+#pragma unroll
+            for (int i = 0; i < kTPos; ++i) sdy += D[i];
+            gq_put1(gq, sdy, NP - 1, prow, lane, store_g);
             load_taps<K>(mytab, trow(0, 0), true, w);
-            grid_conv8_park<K>(D, w, mypark, lane, H);
+            grid_conv8_park<K>(D, w, 0.f, mypark, lane, H);
         }
         if (L >= 1) {
             float U1[4][16], V1[4][16];

@@ -104,6 +104,12 @@ def make_inputs(B: int, C: int, H: int, W: int, k: int, L: int, dtype: str = "f3
     )
 
 
+def make_bias(C: int, seed: int = 0) -> np.ndarray:
+    """Seeded base bias for runs that use one (the benchmark workloads have none):
+    numpy.random.default_rng([seed, 1]), b0 ~ U(-0.5, 0.5) [C], rounded to float32."""
+    return np.random.default_rng([seed, 1]).uniform(-0.5, 0.5, (C,)).astype(np.float32)
+
+
 # Named workloads. ConvNeXt-T stage shapes follow from 224x224 inputs
 # (56, 28, 14, 7 pixels at C = 96, 192, 384, 768).
 WORKLOADS: Dict[str, Workload] = {

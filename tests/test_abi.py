@@ -41,12 +41,13 @@ def test_status_strings():
     assert binding.status_string(99) == "unknown status"
 
 
-def fwd(desc, x=FAKE, bw=FAKE + 4096, bs=FAKE + 8192, lw=None, ls=None, y=FAKE + (1 << 36), ws=None, ws_bytes=0):
+def fwd(desc, x=FAKE, bw=FAKE + 4096, bs=FAKE + 8192, lw=None, ls=None, y=FAKE + (1 << 36), ws=None, ws_bytes=0,
+        bias=None):
     L = desc.L if desc is not None else 0
     lw = [FAKE + 16384 + 64 * i for i in range(L)] if lw is None else lw
     ls = [FAKE + 32768 + 64 * i for i in range(L)] if ls is None else ls
     lib = binding.load()
-    return lib.wtconv_forward(ctypes.byref(desc) if desc is not None else None, x, bw, bs,
+    return lib.wtconv_forward(ctypes.byref(desc) if desc is not None else None, x, bw, bs, bias,
                               binding._ptr_array(lw), binding._ptr_array(ls), y, ws, ctypes.c_size_t(ws_bytes), None)
 
 
@@ -71,7 +72,8 @@ def test_forward_rejects_nulls():
     assert fwd(d, bw=None) == 1
     assert fwd(d, bs=None) == 1
     lib = binding.load()
-    assert lib.wtconv_forward(ctypes.byref(d), FAKE, FAKE, FAKE, None, None, FAKE + (1 << 36), None, 0, None) == 1
+    assert lib.wtconv_forward(ctypes.byref(d), FAKE, FAKE, FAKE, None, None, None, FAKE + (1 << 36), None, 0,
+                              None) == 1
     assert fwd(d, lw=[FAKE, 0]) == 1
 
 
@@ -79,6 +81,9 @@ def test_forward_rejects_alias():
     d = make_desc(2, 3, 8, 8, 5, 1)
     assert fwd(d, x=FAKE, y=FAKE + 64) == 6
     assert fwd(d, x=FAKE + 64, y=FAKE) == 6
+    # the optional bias is an input: y must not overlap it, and a bias is accepted
+    assert fwd(d, bias=FAKE + (1 << 36) + 32) == 6
+    assert fwd(d, bias=FAKE + (1 << 36) + (1 << 20), y=FAKE + (1 << 36), x=None) == 1
 
 
 def test_forward_workspace_query():
@@ -109,16 +114,17 @@ def test_forward_large_plane_workspace_checks():
 def bwd(desc, ws=FAKE + (1 << 38), ws_bytes=1 << 30, dx=FAKE + (1 << 37), **kw):
     L = desc.L
     lib = binding.load()
-    p = dict(x=FAKE, dy=FAKE + (1 << 35), bw=FAKE + (1 << 34), bs=FAKE + (1 << 34) + 65536,
-             dbw=FAKE + (1 << 39), dbs=FAKE + (1 << 39) + 65536)
+    p = dict(x=FAKE, dy=FAKE + (1 << 35), bw=FAKE + (1 << 34), bs=FAKE + (1 << 34) + 65536, bias=None,
+             dbw=FAKE + (1 << 39), dbs=FAKE + (1 << 39) + 65536, dbb=None)
     p.update(kw)
     lw = [FAKE + (1 << 33) + 4096 * i for i in range(L)]
     ls = [FAKE + (1 << 33) + 65536 + 4096 * i for i in range(L)]
     dlw = kw.get("dlw", [FAKE + (1 << 41) + (1 << 20) * i for i in range(L)])
     dls = kw.get("dls", [FAKE + (1 << 41) + (1 << 30) + (1 << 20) * i for i in range(L)])
-    return lib.wtconv_backward(ctypes.byref(desc), p["x"], p["dy"], p["bw"], p["bs"], binding._ptr_array(lw),
-                               binding._ptr_array(ls), dx, p["dbw"], p["dbs"], binding._ptr_array(dlw),
-                               binding._ptr_array(dls), ws, ctypes.c_size_t(ws_bytes), None)
+    return lib.wtconv_backward(ctypes.byref(desc), p["x"], p["dy"], p["bw"], p["bs"], p["bias"],
+                               binding._ptr_array(lw), binding._ptr_array(ls), dx, p["dbw"], p["dbs"], p["dbb"],
+                               binding._ptr_array(dlw), binding._ptr_array(dls), ws, ctypes.c_size_t(ws_bytes),
+                               None)
 
 
 def test_backward_workspace_query():
@@ -147,6 +153,9 @@ def test_backward_rejects_bad_arguments():
     assert bwd(d, ws=FAKE + (1 << 35)) == 6      # workspace overlaps dy
     assert bwd(d, dbs=FAKE + (1 << 39) + 16) == 6  # two gradient outputs overlap
     assert bwd(d, dlw=[FAKE + (1 << 41), 0]) == 1
+    assert bwd(d, dbb=FAKE + (1 << 39) + 16) == 6  # the bias gradient overlaps d_base_w
+    assert bwd(d, dbb=FAKE + 256) == 6             # ... or an input
+    assert bwd(d, bias=FAKE + (1 << 37) + 64) == 6  # dx overlaps the bias
 
 
 def test_descriptor_layout_matches_header():

@@ -80,6 +80,69 @@ def test_backward_small(B, C, H, W, k, L, dtype):
     check_backward(B, C, H, W, k, L, dtype)
 
 
+# The base bias of Algorithm 1 (folded as s0 * b0, eq. fold) through every
+# execution mode: fused backward, gradient pass, tiny planes, split levels and
+# large-plane regions; d_base_scale gains b0 * sum(dy) and d_base_bias is
+# s0 * sum(dy) (eq. foldgrad).
+BIAS = [
+    (2, 3, 13, 11, 5, 3, "f32"),      # fused backward
+    (2, 4, 28, 28, 5, 3, "f32"),      # gradient pass
+    (70, 3, 7, 6, 5, 4, "f32"),       # tiny planes
+    (2, 2, 56, 56, 5, 5, "f32"),      # split levels
+    (1, 2, 130, 126, 5, 3, "f32"),    # region tiles
+    (2, 4, 28, 28, 3, 2, "bf16"),
+]
+
+
+@pytest.mark.parametrize("B,C,H,W,k,L,dtype", BIAS)
+def test_bias_forward_backward(B, C, H, W, k, L, dtype):
+    from paper_2608_10805_amd import binding
+    from paper_2608_10805_amd.inputs import make_bias
+
+    inp, dev = setup(B, C, H, W, k, L, dtype)
+    b = make_bias(C)
+    bt = torch.from_numpy(b).to("cuda:0")
+    tol = TOL[dtype]
+    y = binding.forward(dev.x, dev.bw, dev.bs, dev.lw, dev.ls, bias=bt)
+    torch.cuda.synchronize()
+    ref_y = oracle.forward(inp.x, inp.base_w, inp.base_scale, inp.level_w, inp.level_scale, base_bias=b)
+    assert rel_err(to_np(y), ref_y) < tol
+    dx, dbw, dbs, dlw, dls, dbb = binding.backward(dev.x, dev.dy, dev.bw, dev.bs, dev.lw, dev.ls, bias=bt,
+                                                   need_dbias=True)
+    torch.cuda.synchronize()
+    ref = oracle.backward(inp.x, inp.dy, inp.base_w, inp.base_scale, inp.level_w, inp.level_scale, base_bias=b)
+    errs = {"dx": rel_err(to_np(dx), ref["dx"]), "d_base_w": rel_err(to_np(dbw), ref["d_base_w"]),
+            "d_base_scale": rel_err(to_np(dbs), ref["d_base_scale"]),
+            "d_base_bias": rel_err(to_np(dbb), ref["d_base_bias"])}
+    for l in range(L):
+        errs[f"d_level_w{l + 1}"] = rel_err(to_np(dlw[l]), ref["d_level_w"][l])
+        errs[f"d_level_scale{l + 1}"] = rel_err(to_np(dls[l]), ref["d_level_scale"][l])
+    bad = {k_: v for k_, v in errs.items() if not v < tol}
+    assert not bad, f"rel errs over {tol}: {bad}"
+
+
+def test_bias_autograd_module():
+    from paper_2608_10805_amd.autograd import WTConv2d
+
+    torch.manual_seed(1)
+    m = WTConv2d(5, kernel_size=5, levels=2, bias=True, device="cuda:0")
+    with torch.no_grad():
+        m.base_bias.uniform_(-0.5, 0.5)
+    x = torch.randn(2, 5, 24, 20, device="cuda:0", requires_grad=True)
+    y = m(x)
+    g = torch.randn_like(y)
+    y.backward(g)
+    c64 = lambda t: t.detach().cpu().double().numpy()  # noqa: E731
+    lw = [c64(p) for p in m.level_w]
+    ls = [c64(p) for p in m.level_scale]
+    args = (c64(x), c64(m.base_w), c64(m.base_scale), lw, ls)
+    assert rel_err(to_np(y), oracle.forward(*args, base_bias=c64(m.base_bias))) < 1e-5
+    ref = oracle.backward(args[0], c64(g), *args[1:], base_bias=c64(m.base_bias))
+    assert rel_err(to_np(x.grad), ref["dx"]) < 1e-5
+    assert rel_err(to_np(m.base_scale.grad), ref["d_base_scale"]) < 1e-5
+    assert rel_err(to_np(m.base_bias.grad), ref["d_base_bias"]) < 1e-5
+
+
 def test_backward_without_dx_matches():
     check_backward(3, 4, 21, 19, 5, 3, "f32", need_dx=False)
 
