@@ -3,16 +3,20 @@
 
 Workload: ConvNeXt-T stage-1 layer shape, B=64, C=96, H=W=56, k=5, L=3,
 float32, seeded synthetic inputs (see paper_2608_10805_amd/inputs.py). One
-step is the whole operator: wtconv_forward, then the two phases of
-wtconv_backward (the fused pass writing dx and kernel-gradient partials, then
-the finalize that reduces and unfolds them). Inputs are resident in HBM before
-timing starts; steps rotate over several distinct buffer sets so that the
-256 MB Infinity Cache cannot hold one step's tensors for the next.
+step is the whole operator, forward and backward, as the library's entry
+points run it for this shape: wtconv_forward (y), wtconv_backward_partials
+without dx (the kernel-gradient pass), wtconv_backward_data (dx: the forward
+pass on dy with rotated kernels) and wtconv_backward_finalize (fixed-order
+reduction and unfold) -- exactly the kernels wtconv_backward launches here,
+each bracketed by its own HIP events. Inputs are resident in HBM before timing
+starts; steps rotate over several distinct buffer sets so that the 256 MB
+Infinity Cache cannot hold one step's tensors for the next.
 
 Prints one JSON line. `value` is achieved GB/s: the single-pass algorithmic
 bytes (x, y, dy, dx, each read or written once; parameters and gradients)
-divided by the measured step time. `roofline` describes the dominant kernel,
-timed with HIP events on the stream it runs on. `cpu_baseline` times the
+divided by the measured step time. `roofline` describes the dominant kernel (the one
+with the largest share of the step), timed with HIP events on the stream it
+runs on; `kernels` lists every kernel of the step the same way. `cpu_baseline` times the
 float64 CPU oracle on the host cores.
 """
 import argparse
@@ -49,6 +53,14 @@ def parse():
     ap.add_argument("--no-config-table", action="store_true",
                     help="skip the per-configuration fwd / fwd+bwd timing table")
     ap.add_argument("--table-steps", type=int, default=10)
+    ap.add_argument("--summarize-trace", metavar="DB",
+                    help="write the kernel statistics of a rocprofv3 --kernel-trace database to --out and exit")
+    ap.add_argument("--summarize-traffic", nargs=4, metavar=("FETCH_DB", "WRITE_DB", "COPY_FETCH_DB", "COPY_WRITE_DB"),
+                    help="write per-launch HBM bytes from rocprofv3 FETCH_SIZE / WRITE_SIZE databases of this "
+                         "benchmark and of --copy-calibration-mib runs to --out and exit")
+    ap.add_argument("--copy-mib", type=int, default=256, help="size of the calibration copy behind --summarize-traffic")
+    ap.add_argument("--command", default="", help="the profiling command, recorded in the summary")
+    ap.add_argument("--out", help="summary file for --summarize-trace / --summarize-traffic")
     return ap.parse_args()
 
 
@@ -287,8 +299,93 @@ def load_traffic(path, kernel):
     return float(rec[key]) if key in rec else None
 
 
+# Kernels of the benchmark step, by the symbol prefix rocprofv3 reports.
+STEP_KERNELS = {"forward": "fused_kernel<5, float, false, true, false>", "grad": "grad_kernel<5, float>",
+                "finalize": "reduce_kernel"}
+
+
+def _rocpd_rows(db, sql):
+    import sqlite3
+    con = sqlite3.connect(db)
+    try:
+        return con.execute(sql).fetchall()
+    finally:
+        con.close()
+
+
+def summarize_trace(db, out, command):
+    """Kernel statistics (calls, total and average duration) of a rocprofv3
+    --kernel-trace database, one line per kernel."""
+    rows = _rocpd_rows(db, "select name, count(*), sum(duration), avg(duration) from kernels group by name "
+                           "order by sum(duration) desc")
+    total = sum(r[2] for r in rows)
+    lines = ["# rocprofv3 kernel trace statistics, fused WTConv fwd+bwd benchmark step",
+             f"# workload: {WORKLOAD['workload']} B={WORKLOAD['B']} C={WORKLOAD['C']} H=W={WORKLOAD['H']} "
+             f"k={WORKLOAD['k']} L={WORKLOAD['L']} fp32, MI355X",
+             f"# command: {command}",
+             f"kernel_source_sha256: {kernel_source_hash()}",
+             "# kernel | calls | total_us | average_us | percent"]
+    for name, n, tot, avg in rows:
+        short = name.replace("void ", "").replace("wtc::(anonymous namespace)::", "").split("(wtc::")[0]
+        lines.append(f"{short[:110]} | {n} | {tot / 1e3:.1f} | {avg / 1e3:.3f} | {100.0 * tot / total:.1f}")
+    with open(out, "w") as f:
+        f.write("\n".join(lines) + "\n")
+
+
+def _counter_per_kernel(db, counter):
+    """Mean value of `counter` per dispatch, by kernel name (rocprofv3 --pmc database)."""
+    rows = _rocpd_rows(db, f"select kernel_name, dispatch_id, sum(value) from counters_collection where "
+                           f"counter_name = '{counter}' group by kernel_name, dispatch_id")
+    acc = {}
+    for name, _, v in rows:
+        acc.setdefault(name, []).append(v)
+    return {k: sum(v) / len(v) for k, v in acc.items()}
+
+
+def summarize_traffic(fetch_db, write_db, cfetch_db, cwrite_db, copy_mib, out, command):
+    """Measured HBM bytes per launch of the step's kernels: FETCH_SIZE and
+    WRITE_SIZE (KiB) scaled by what the same counters report for a plain device
+    copy of known size."""
+    copy_kib = copy_mib * 1024.0
+    cf = max((v for k, v in _counter_per_kernel(cfetch_db, "FETCH_SIZE").items() if "copyBuffer" in k), default=0)
+    cw = max((v for k, v in _counter_per_kernel(cwrite_db, "WRITE_SIZE").items() if "copyBuffer" in k), default=0)
+    fscale, wscale = copy_kib / cf, copy_kib / cw
+    fetch = _counter_per_kernel(fetch_db, "FETCH_SIZE")
+    write = _counter_per_kernel(write_db, "WRITE_SIZE")
+    B, C, H, W, k, L = (WORKLOAD[n] for n in ("B", "C", "H", "W", "k", "L"))
+    from paper_2608_10805_amd import iomodel
+    algo = 2.0 * B * C * H * W * 4 + 4.0 * iomodel.param_count(C, k, L)
+    lines = ["# HBM traffic per kernel launch from rocprofv3 counters, fused WTConv fwd+bwd benchmark step",
+             f"# workload: B={B} C={C} H=W={H} k={k} L={L} fp32 (ConvNeXt-T stage 1), MI355X",
+             f"# commands (one counter per run): {command}",
+             f"# calibration: a {copy_mib} MiB device copy reads and writes {copy_kib:.0f} KiB; FETCH_SIZE reports "
+             f"{cf:.0f} KiB (scale x{fscale:.3f}), WRITE_SIZE reports {cw:.0f} KiB (scale x{wscale:.3f})",
+             f"workload: {WORKLOAD['workload']}",
+             f"kernel_source_sha256: {kernel_source_hash()}",
+             f"fetch_scale: {fscale:.4f}",
+             f"write_scale: {wscale:.4f}"]
+    for key, prefix in STEP_KERNELS.items():
+        fk = [v for n, v in fetch.items() if prefix in n]
+        wk = [v for n, v in write.items() if prefix in n]
+        if not fk or not wk:
+            continue
+        f_kib, w_kib = sum(fk) / len(fk), sum(wk) / len(wk)
+        hbm = f_kib * 1024 * fscale + w_kib * 1024 * wscale
+        note = f"; algorithmic {algo / 1e6:.2f} MB; ratio {hbm / algo:.3f}" if key != "finalize" else ""
+        lines.append(f"# {key} = {prefix}: FETCH {f_kib:.1f} KiB, WRITE {w_kib:.1f} KiB -> {hbm / 1e6:.2f} MB{note}")
+        lines.append(f"{key}_hbm_bytes_per_launch: {hbm:.0f}")
+    with open(out, "w") as f:
+        f.write("\n".join(lines) + "\n")
+
+
 def main():
     args = parse()
+    if args.summarize_trace:
+        summarize_trace(args.summarize_trace, args.out, args.command)
+        return
+    if args.summarize_traffic:
+        summarize_traffic(*args.summarize_traffic, args.copy_mib, args.out, args.command)
+        return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}, WORLD_SIZE {world}); this operator's "
@@ -326,7 +423,7 @@ def main():
         x = x0 if s == 0 else x0.clone()
         dy = dy0 if s == 0 else dy0.clone()
         sets.append((x, dy, torch.empty_like(x), torch.empty_like(x)))
-    bk = binding.Backward(x0, bw, bs, lw, ls, need_dx=True)
+    bk = binding.Backward(x0, bw, bs, lw, ls, need_dx=False)
 
     def step(i, ev=None):
         x, dy, y, dx = sets[i % len(sets)]
@@ -335,19 +432,22 @@ def main():
         binding.forward(x, bw, bs, lw, ls, out=y)
         if ev is not None:
             ev[1].record()
-        bk.partials(x, dy, dx)
+        bk.partials(x, dy, None)
         if ev is not None:
             ev[2].record()
-        bk.finalize()
+        bk.data(dy, dx)
         if ev is not None:
             ev[3].record()
+        bk.finalize()
+        if ev is not None:
+            ev[4].record()
 
     for i in range(args.warmup):
         step(i)
     torch.cuda.synchronize()
     log("bench: warmup done")
 
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     start.record()
@@ -356,19 +456,35 @@ def main():
     end.record()
     torch.cuda.synchronize()
     ms_step = start.elapsed_time(end) / args.steps
-    per_step = [e[0].elapsed_time(e[3]) for e in evs]
+    per_step = [e[0].elapsed_time(e[4]) for e in evs]
     fwd_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
-    bwd_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
-    fin_ms = float(np.mean([e[2].elapsed_time(e[3]) for e in evs]))
-    log(f"bench: {ms_step * 1e3:.1f} us/step (forward {fwd_ms * 1e3:.1f}, backward fused {bwd_ms * 1e3:.1f}, "
-        f"finalize {fin_ms * 1e3:.1f})")
+    grad_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
+    data_ms = float(np.mean([e[2].elapsed_time(e[3]) for e in evs]))
+    fin_ms = float(np.mean([e[3].elapsed_time(e[4]) for e in evs]))
+    log(f"bench: {ms_step * 1e3:.1f} us/step (forward {fwd_ms * 1e3:.1f}, kernel-gradient pass {grad_ms * 1e3:.1f}, "
+        f"dx pass {data_ms * 1e3:.1f}, finalize {fin_ms * 1e3:.1f})")
 
     work = iomodel.single_pass_work(B, C, H, W, k, L, "f32")
     value = work.bytes_fwdbwd / (ms_step * 1e-3) / 1e9
-    if bwd_ms >= fwd_ms:
-        dom, dom_ms, dom_fma, dom_bytes = "backward_fused", bwd_ms, work.fma_bwd, work.bytes_bwd
-    else:
-        dom, dom_ms, dom_fma, dom_bytes = "forward", fwd_ms, work.fma_fwd, work.bytes_fwd
+    # Kernels of the step for this workload (each entry point is one launch
+    # here): the fused forward kernel runs twice (y, and dx on dy with rotated
+    # kernels), the kernel-gradient pass once. Algorithmic work per launch:
+    # the forward k^2 (N + coefficient sites) FMAs, moving x (or dy) in and y
+    # (or dx) out; the gradient pass the same FMA count, reading x and dy.
+    N = B * C * H * W
+    fwd_bytes = 2.0 * N * 4 + 4.0 * iomodel.param_count(C, k, L)
+    kernels = {
+        "forward": {"launches_per_step": 2, "ms": (fwd_ms + data_ms) / 2, "fma": work.fma_fwd, "bytes": fwd_bytes},
+        "grad": {"launches_per_step": 1, "ms": grad_ms, "fma": work.fma_fwd, "bytes": fwd_bytes},
+    }
+    for kv in kernels.values():
+        kv["TFLOPs"] = round(2.0 * kv["fma"] / (kv["ms"] * 1e-3) / 1e12, 3)
+        kv["fma_frac"] = round(iomodel.fma_floor_s(kv["fma"]) / (kv["ms"] * 1e-3), 4)
+        kv["GBps"] = round(kv["bytes"] / (kv["ms"] * 1e-3) / 1e9, 1)
+        kv["ms"] = round(kv["ms"], 5)
+    kernels["finalize"] = {"launches_per_step": 1, "ms": round(fin_ms, 5)}
+    dom = max(("forward", "grad"), key=lambda n: kernels[n]["ms"] * kernels[n]["launches_per_step"])
+    dom_ms, dom_fma, dom_bytes = kernels[dom]["ms"], kernels[dom]["fma"], kernels[dom]["bytes"]
     achieved = 2.0 * dom_fma / (dom_ms * 1e-3) / 1e12
     peak = iomodel.FP32_FLOPS / 1e12
     traffic = load_traffic(args.traffic, dom)
@@ -387,7 +503,6 @@ def main():
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(inp, work.bytes_fwdbwd, args.cpu_seconds)
-    N = B * C * H * W
     out = {
         "metric": METRIC, "value": round(value, 2), "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(ms_step, 5), "higher_is_better": True, "scaling": "weak",
@@ -399,7 +514,7 @@ def main():
         "copy_ceiling_GBps": round(copy_gbps, 1), "hbm_frac_of_copy": round(value / copy_gbps, 4),
         "valu_probe": probe,
         "fma_frac": round(iomodel.fma_floor_s(work.fma_fwdbwd) / (ms_step * 1e-3), 4),
-        "fwd_ms": round(fwd_ms, 5), "bwd_fused_ms": round(bwd_ms, 5), "bwd_finalize_ms": round(fin_ms, 5),
+        "fwd_ms": round(fwd_ms, 5), "bwd_ms": round(grad_ms + data_ms + fin_ms, 5), "kernels": kernels,
         "algorithmic_bytes_per_step": work.bytes_fwdbwd,
         "floors_us": {"hbm": round(iomodel.hbm_floor_s(work.bytes_fwdbwd) * 1e6, 2),
                       "fp32_fma": round(iomodel.fma_floor_s(work.fma_fwdbwd) * 1e6, 2)},

@@ -176,6 +176,30 @@ wtconv_status wtconv_backward_finalize(const wtconv_desc* desc, const float* bas
                                        float* d_base_bias, float* const* d_level_w, float* const* d_level_scale,
                                        const void* workspace, size_t workspace_bytes, hipStream_t stream);
 
+/* Bytes of device workspace wtconv_backward_data needs for `desc` (the same as
+ * the forward pass; 0 when the planes are processed on chip, or on a bad desc). */
+size_t wtconv_backward_data_workspace_bytes(const wtconv_desc* desc);
+
+/*
+ * Input gradient only: dx = d sum(y * dy) / dx. The operator is linear in x
+ * and its adjoint is the same operator with every kernel rotated by 180
+ * degrees (the adjoint of a "same" correlation is the correlation with the
+ * rotated kernel; Haar synthesis and analysis are each other's transposes,
+ * Proposition 1), so this is the forward pass on dy with rotated kernels and
+ * no bias. For callers that do not need parameter gradients, or that schedule
+ * the input gradient separately from wtconv_backward_partials(dx = NULL) and
+ * wtconv_backward_finalize.
+ *   dy           [B][C][H][W] dtype
+ *   base_w, base_scale, level_w, level_scale: as for wtconv_forward
+ *   dx           [B][C][H][W] dtype; must not overlap any input
+ *   workspace    at least wtconv_backward_data_workspace_bytes(desc) bytes,
+ *                16-byte aligned (may be NULL when that size is 0)
+ */
+wtconv_status wtconv_backward_data(const wtconv_desc* desc, const void* dy, const float* base_w,
+                                   const float* base_scale, const float* const* level_w,
+                                   const float* const* level_scale, void* dx, void* workspace,
+                                   size_t workspace_bytes, hipStream_t stream);
+
 /* Static, human-readable name of a status code. */
 const char* wtconv_status_string(wtconv_status status);
 

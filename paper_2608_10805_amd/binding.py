@@ -18,7 +18,8 @@ STATUS = {
     8: "WTCONV_ERR_UNSUPPORTED", 9: "WTCONV_ERR_HIP",
 }
 EXPORTS = ["wtconv_forward_workspace_bytes", "wtconv_forward", "wtconv_backward", "wtconv_backward_workspace_bytes",
-           "wtconv_backward_partials", "wtconv_backward_finalize", "wtconv_status_string", "wtconv_version"]
+           "wtconv_backward_partials", "wtconv_backward_finalize", "wtconv_backward_data_workspace_bytes",
+           "wtconv_backward_data", "wtconv_status_string", "wtconv_version"]
 MAX_LEVELS = 8
 
 
@@ -62,6 +63,10 @@ def load():
     lib.wtconv_backward_finalize.argtypes = [ctypes.POINTER(Desc), _P, _P, _P, _PP, _PP, _P, _P, _P, _PP, _PP,
                                              _P, ctypes.c_size_t, _P]
     lib.wtconv_backward_finalize.restype = ctypes.c_int
+    lib.wtconv_backward_data_workspace_bytes.argtypes = [ctypes.POINTER(Desc)]
+    lib.wtconv_backward_data_workspace_bytes.restype = ctypes.c_size_t
+    lib.wtconv_backward_data.argtypes = [ctypes.POINTER(Desc), _P, _P, _P, _PP, _PP, _P, _P, ctypes.c_size_t, _P]
+    lib.wtconv_backward_data.restype = ctypes.c_int
     lib.wtconv_status_string.argtypes = [ctypes.c_int]
     lib.wtconv_status_string.restype = ctypes.c_char_p
     lib.wtconv_version.restype = ctypes.c_int
@@ -130,6 +135,17 @@ def wtconv_backward_finalize(desc: Desc, base_w, base_scale, base_bias, level_w,
                                            _ptr_array(level_scale), d_base_w, d_base_scale, d_base_bias,
                                            _ptr_array(d_level_w), _ptr_array(d_level_scale), workspace,
                                            ctypes.c_size_t(workspace_bytes), stream)
+
+
+def wtconv_backward_data_workspace_bytes(desc: Desc) -> int:
+    return int(load().wtconv_backward_data_workspace_bytes(ctypes.byref(desc)))
+
+
+def wtconv_backward_data(desc: Desc, dy, base_w, base_scale, level_w, level_scale, dx, workspace, workspace_bytes,
+                         stream) -> int:
+    return load().wtconv_backward_data(ctypes.byref(desc), dy, base_w, base_scale, _ptr_array(level_w),
+                                       _ptr_array(level_scale), dx, workspace, ctypes.c_size_t(workspace_bytes),
+                                       stream)
 
 
 def wtconv_version() -> int:
@@ -226,6 +242,25 @@ def backward(x, dy, base_w, base_scale, level_w, level_scale, need_dx=True, work
     return dx, dbw, dbs, dlw, dls
 
 
+def backward_data(dy, base_w, base_scale, level_w, level_scale, out=None, workspace=None):
+    """dx alone (wtconv_backward_data): the forward pass on dy with rotated kernels."""
+    import torch
+    _require(dy, "dy")
+    B, C, H, W = dy.shape
+    desc = make_desc(B, C, H, W, base_w.shape[-1], len(level_w), _dtype_code(dy))
+    dx = torch.empty_like(dy) if out is None else out
+    nbytes = wtconv_backward_data_workspace_bytes(desc)
+    ws_ptr = None
+    if nbytes:
+        if workspace is None or workspace.numel() * workspace.element_size() < nbytes:
+            workspace = torch.empty(nbytes, dtype=torch.uint8, device=dy.device)
+        ws_ptr = workspace.data_ptr()
+    _check(wtconv_backward_data(desc, dy.data_ptr(), base_w.data_ptr(), base_scale.data_ptr(),
+                                [t.data_ptr() for t in level_w], [t.data_ptr() for t in level_scale], dx.data_ptr(),
+                                ws_ptr, nbytes, _stream(dy.device)))
+    return dx
+
+
 class Backward:
     """Preallocated backward of one problem, callable in its two phases
     (used by the benchmark to time the fused pass and the finalize separately)."""
@@ -249,6 +284,8 @@ class Backward:
         self._dlw = [t.data_ptr() for t in self.dlw]
         self._dls = [t.data_ptr() for t in self.dls]
         self.device = x.device
+        self.data_nbytes = wtconv_backward_data_workspace_bytes(self.desc)
+        self.data_workspace = None
 
     def partials(self, x, dy, dx=None):
         bw, bs, _, _ = self.params
@@ -256,6 +293,17 @@ class Backward:
         _check(wtconv_backward_partials(self.desc, x.data_ptr(), dy.data_ptr(), bw.data_ptr(), bs.data_ptr(),
                                         self._lw, self._ls, out.data_ptr() if out is not None else None,
                                         self.workspace.data_ptr(), self.nbytes, _stream(self.device)))
+
+    def data(self, dy, dx):
+        """dx alone (wtconv_backward_data) into `dx`."""
+        bw, bs, _, _ = self.params
+        if self.data_nbytes and self.data_workspace is None:
+            import torch
+            self.data_workspace = torch.empty(self.data_nbytes, dtype=torch.uint8, device=self.device)
+        _check(wtconv_backward_data(self.desc, dy.data_ptr(), bw.data_ptr(), bs.data_ptr(), self._lw, self._ls,
+                                    dx.data_ptr(),
+                                    self.data_workspace.data_ptr() if self.data_workspace is not None else None,
+                                    self.data_nbytes, _stream(self.device)))
 
     def finalize(self):
         bw, bs, _, _ = self.params

@@ -986,6 +986,38 @@ wtconv_status wtconv_backward_finalize(const wtconv_desc* desc, const float* bas
                          reinterpret_cast<const char*>(workspace), 0, stream);
 }
 
+size_t wtconv_backward_data_workspace_bytes(const wtconv_desc* desc)
+{
+    if (check_desc(desc) != WTCONV_OK) return 0;
+    const size_t n = forward_ws(*desc);
+    return n == kUnsupported ? 0 : n;
+}
+
+wtconv_status wtconv_backward_data(const wtconv_desc* desc, const void* dy, const float* base_w,
+                                   const float* base_scale, const float* const* level_w,
+                                   const float* const* level_scale, void* dx, void* workspace,
+                                   size_t workspace_bytes, hipStream_t stream)
+{
+    wtconv_status st = check_desc(desc);
+    if (st != WTCONV_OK) return st;
+    const wtconv_desc& d = *desc;
+    if (!dy || !dx || !base_w || !base_scale) return WTCONV_ERR_NULL;
+    if ((st = check_levels(d.L, level_w, level_scale)) != WTCONV_OK) return st;
+    const size_t need = forward_ws(d);
+    if ((st = check_workspace(need, workspace, workspace_bytes)) != WTCONV_OK) return st;
+    const size_t bytes = (size_t)d.B * d.C * d.H * d.W * elem_size(d.dtype);
+    Range ins[5 + 2 * kMaxLevels];
+    int ni = 0;
+    ins[ni++] = {dy, bytes};
+    ni += param_ranges(d, base_w, base_scale, nullptr, level_w, level_scale, ins + ni);
+    const Range outs[2] = {{dx, bytes}, {workspace, need}};
+    if (any_overlap(outs, 2, ins, ni)) return WTCONV_ERR_ALIAS;
+    wtc::ParamPtrs p;
+    fill_params(p, d.L, base_w, base_scale, nullptr, level_w, level_scale);
+    p.rot = 1;  // the forward pass on dy with every kernel rotated by 180 degrees
+    return forward_impl(d, dy, p, dx, reinterpret_cast<char*>(workspace), 0, stream);
+}
+
 wtconv_status wtconv_backward(const wtconv_desc* desc, const void* x, const void* dy,
                               const float* base_w, const float* base_scale, const float* base_bias,
                               const float* const* level_w, const float* const* level_scale,

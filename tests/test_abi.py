@@ -158,5 +158,27 @@ def test_backward_rejects_bad_arguments():
     assert bwd(d, bias=FAKE + (1 << 37) + 64) == 6  # dx overlaps the bias
 
 
+def test_backward_data_checks():
+    lib = binding.load()
+    d = make_desc(2, 3, 8, 8, 5, 2)
+
+    def call(desc=d, dy=FAKE, bw=FAKE + 4096, bs=FAKE + 8192, dx=FAKE + (1 << 36), ws=None, nbytes=0):
+        lw = binding._ptr_array([FAKE + (1 << 30) + 4096 * i for i in range(desc.L)])
+        ls = binding._ptr_array([FAKE + (1 << 31) + 4096 * i for i in range(desc.L)])
+        return lib.wtconv_backward_data(ctypes.byref(desc), dy, bw, bs, lw, ls, dx, ws, ctypes.c_size_t(nbytes), None)
+
+    assert call(desc=make_desc(2, 3, 8, 8, 4, 2)) == 3
+    assert call(dy=None) == 1
+    assert call(dx=None) == 1
+    assert call(bw=None) == 1
+    assert call(dx=FAKE + 128) == 6           # dx overlaps dy
+    assert call(dx=FAKE + 4096 + 16) == 6     # dx overlaps the base kernel
+    big = make_desc(1, 1, 512, 512, 5, 3)
+    need = binding.wtconv_backward_data_workspace_bytes(big)
+    assert need == binding.wtconv_forward_workspace_bytes(big) > 0
+    assert call(desc=big) == 7                # no workspace
+    assert binding.wtconv_backward_data_workspace_bytes(make_desc(64, 96, 56, 56, 5, 3)) == 0
+
+
 def test_descriptor_layout_matches_header():
     assert ctypes.sizeof(Desc) == 7 * 4

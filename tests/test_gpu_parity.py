@@ -143,6 +143,30 @@ def test_bias_autograd_module():
     assert rel_err(to_np(m.base_bias.grad), ref["d_base_bias"]) < 1e-5
 
 
+# dx alone (the forward pass on dy with rotated kernels) in every execution
+# mode of the forward: resident, tiny, split, region, 16-bit storage.
+DATA = [
+    (2, 4, 28, 28, 5, 3, "f32"),
+    (70, 3, 7, 6, 5, 4, "f32"),
+    (2, 2, 56, 56, 5, 5, "f32"),
+    (1, 2, 130, 126, 5, 3, "f32"),
+    (2, 3, 17, 23, 7, 2, "bf16"),
+    (3, 2, 9, 1, 3, 1, "f16"),
+]
+
+
+@pytest.mark.parametrize("B,C,H,W,k,L,dtype", DATA)
+def test_backward_data(B, C, H, W, k, L, dtype):
+    from paper_2608_10805_amd import binding
+
+    inp, dev = setup(B, C, H, W, k, L, dtype)
+    dx = binding.backward_data(dev.dy, dev.bw, dev.bs, dev.lw, dev.ls)
+    torch.cuda.synchronize()
+    ref = oracle.backward(inp.x, inp.dy, inp.base_w, inp.base_scale, inp.level_w, inp.level_scale)
+    e = rel_err(to_np(dx), ref["dx"])
+    assert e < TOL[dtype], f"dx rel err {e:.3e}"
+
+
 def test_backward_without_dx_matches():
     check_backward(3, 4, 21, 19, 5, 3, "f32", need_dx=False)
 
