@@ -25,6 +25,7 @@ int cdiv(long a, long b) { return (int)((a + b - 1) / b); }
 struct Plan {
     PlaneGeom g;
     int one_round = 0;  // every level filtered in one register-tile round per lane
+    int merge_deep = 0;  // forward: levels 1 and >= 3 filtered in one round (4x4 tiles)
     int PP = 1;        // planes resident at once
     int nb = 1;        // planes per workgroup
     int nchunks = 1;   // workgroups per channel
@@ -71,7 +72,7 @@ int pick_tile(int h, int w, int PP, int k, bool bwd)
 
 // Lay out one plane's input array and pyramid for a given number of resident
 // planes. Returns false if a level cannot be tiled within the register caps.
-bool layout(const wtconv_desc& d, int PP, bool bwd, PlaneGeom& g)
+bool layout(const wtconv_desc& d, int PP, bool bwd, PlaneGeom& g, bool t4_deep = false)
 {
     const int R = d.k / 2;
     memset(&g, 0, sizeof(g));
@@ -90,7 +91,7 @@ bool layout(const wtconv_desc& d, int PP, bool bwd, PlaneGeom& g)
         LevelGeom& lg = g.lv[l];
         lg.h = h;
         lg.w = w;
-        lg.T = pick_tile(h, w, PP, d.k, bwd);
+        lg.T = (t4_deep && l >= 3) ? 4 : pick_tile(h, w, PP, d.k, bwd);
         if (lg.T == 0) return false;
         lg.eh = ceil_to(h, lg.T);
         lg.ew = ceil_to(w, lg.T);
@@ -154,6 +155,26 @@ bool make_plan(const wtconv_desc& d, bool bwd, Plan& pl)
     for (int l = 1; l <= d.L; ++l) {
         const LevelGeom& lg = pl.g.lv[l];
         if ((long)PP * (lg.eh / lg.T) * (lg.ew / lg.T) > 64) pl.one_round = 0;
+    }
+    // Forward, single round, level 1 in 4x4 tiles and at least three levels:
+    // the levels from 3 on (small grids, each otherwise a round of its own
+    // with a handful of busy lanes) take 4x4 tiles too and share level 1's
+    // round on the lanes level 1 leaves idle, if they fit (measured on MI355X:
+    // the 7x7 level 3 of a 56x56 plane cost 5 us of a 73 us forward on its own).
+    if (!bwd && pl.one_round && d.L >= 3 && pl.g.lv[1].T == 4) {
+        PlaneGeom gm;
+        if (layout(d, PP, bwd, gm, true)) {
+            long lanes = (long)PP * (gm.lv[1].eh / 4) * (gm.lv[1].ew / 4);
+            for (int l = 3; l <= d.L; ++l) lanes += (long)PP * (gm.lv[l].eh / 4) * (gm.lv[l].ew / 4);
+            const int lds = lds_floats_for(d, bwd, PP, gm);
+            const bool fits = lds <= kLdsFloatsShared || (PP == 1 && lds <= kLdsFloatsMax);
+            // and keep the workgroups per CU of the unmerged layout
+            if (lanes <= 64 && fits && kLdsFloatsMax / lds >= kLdsFloatsMax / pl.lds_floats) {
+                pl.g = gm;
+                pl.lds_floats = lds;
+                pl.merge_deep = 1;
+            }
+        }
     }
     const int target = bwd ? kBackwardTargetWorkgroups : kForwardTargetWorkgroups;
     const int chunks_target = std::max(1, cdiv(target, d.C));
@@ -602,6 +623,7 @@ FusedArgs base_args(const wtconv_desc& d, const Plan& pl, const void* in, const 
     a.vec_ok = vec_ok(in, aux ? aux : in, out ? out : in);
     a.lds_floats = pl.lds_floats;
     a.one_round = pl.one_round;
+    a.merge_deep = pl.merge_deep;
     a.skip_base = skip_base;
     a.g = pl.g;
     return a;

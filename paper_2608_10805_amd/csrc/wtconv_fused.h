@@ -411,6 +411,62 @@ DEV void filter_band_inplace(float* __restrict__ region0, const float* __restric
     }
 }
 
+// Forward, single round: levels 1 and 3..L of band q in one pass over the
+// wavefront, all in 4x4 site tiles. Lanes [s_l, s_l + n_l) take the n_l tiles
+// of level l (level 1 first, then 3, 4, ...); every lane reads its own level's
+// folded kernel from LDS and filters its tile in place once the whole
+// wavefront has read its windows (levels are separate arrays, and a
+// wavefront's LDS operations complete in program order).
+template <int K>
+DEV void filter_merged(float* __restrict__ region0, int stride, const PlaneGeom& g, const float* __restrict__ wtab,
+                       int q, int np, int lane)
+{
+    constexpr int R = K / 2, KK = K * K;
+    // this lane's level, tile index and level geometry (uniform loop, per-lane selects)
+    int lvl = 0, it = 0, start = 0, off = 0, pitch = 0, band = 0, h = 0, w = 0, tx = 0, per = 0;
+    float r_tper = 0.f, r_tx = 0.f;
+    for (int l = 1; l <= g.L; ++l) {
+        if (l == 2) continue;
+        const LevelGeom& lg = g.lv[l];
+        const int ltx = lg.ew / 4;
+        const int n = np * ltx * (lg.eh / 4);
+        if (lvl == 0 && lane < start + n) {
+            lvl = l;
+            it = lane - start;
+            off = lg.off;
+            pitch = lg.pitch;
+            band = lg.band;
+            h = lg.h;
+            w = lg.w;
+            tx = ltx;
+            per = ltx * (lg.eh / 4);
+            r_tper = lg.r_tper;
+            r_tx = lg.r_tx;
+        }
+        start += n;
+    }
+    if (lvl == 0) return;
+    float wv[KK];
+    const float* wrow_p = wtab + (1 + (lvl - 1) * 4 + q) * KK;
+#pragma unroll
+    for (int i = 0; i < KK; ++i) wv[i] = wrow_p[i];
+    const TileIdx ti = tile_at(it, per, r_tper, tx, r_tx, 4);
+    float* base = region0 + ti.p * stride + off + q * band;
+    float res[4][4];
+    conv_tile<K, 4>(base, pitch, ti.j0, ti.i0, wv, res);
+    float* dst = base + (ti.j0 + R) * pitch + ti.i0 + R;
+    if (ti.j0 + 4 <= h && ti.i0 + 4 <= w) {
+#pragma unroll
+        for (int oy = 0; oy < 4; ++oy) st_row<(R % 2) == 0, 4>(dst + oy * pitch, res[oy]);
+    } else {
+#pragma unroll
+        for (int oy = 0; oy < 4; ++oy)
+#pragma unroll
+            for (int ox = 0; ox < 4; ++ox)
+                if (ti.j0 + oy < h && ti.i0 + ox < w) dst[oy * pitch + ox] = res[oy][ox];
+    }
+}
+
 template <int K, bool ONE, bool GRAD>
 DEV void filter_band(float* region0, const float* aux0, int stride, const LevelGeom& lg, int q, int np,
                      const float (&w)[K * K], float (&gacc)[K * K], int lane)
@@ -812,6 +868,13 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(const FusedArgs a)
         //    row by row into LDS.
         for (int l = 1; l <= L; ++l) {
             const LevelGeom& lg = g.lv[l];
+            if constexpr (!BWD && ONE) {
+                // levels 1 and >= 3 in one round (see filter_merged), level 2 below
+                if (a.merge_deep && l != 2) {
+                    if (l == 1) filter_merged<K>(side_in, stride, g, wtab, q, np, lane);
+                    continue;
+                }
+            }
             float w[KK];
             fetch_weights<K>(wtab, wrow(l, q), BWD, lane, w);
             if constexpr (BWD) {

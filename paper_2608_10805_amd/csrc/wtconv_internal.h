@@ -74,6 +74,7 @@ struct FusedArgs {
     int vec_ok;          // 1 if plane bases allow 16-byte (f32) / 8-byte (16-bit) vector access
     int lds_floats;      // dynamic LDS of the workgroup, in floats
     int one_round;       // 1 if every level is filtered in a single register-tile round
+    int merge_deep;      // forward: levels 1 and >= 3 share one round of 4x4 site tiles
     int skip_base;       // 1: no base path and no base-kernel gradient (coarse sub-problem)
     // Region mode (planes too large for LDS): each workgroup processes an
     // rg_T x rg_T output tile of a real_H x real_W plane through a region with
