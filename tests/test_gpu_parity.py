@@ -62,6 +62,8 @@ SMALL = [
     (2, 2, 20, 20, 5, 0, "f32"),
     (1, 2, 40, 36, 5, 8, "f32"),
     (5, 3, 14, 14, 5, 2, "f32"),    # several planes resident per workgroup
+    (3, 2, 40, 40, 5, 3, "f32"),    # levels >= 3 share level 1's round, 2 planes + a ragged batch
+    (3, 2, 40, 40, 3, 5, "f32"),
     (9, 2, 7, 7, 3, 3, "f32"),
     (2, 4, 28, 28, 5, 3, "bf16"),
     (2, 3, 13, 11, 5, 2, "bf16"),
