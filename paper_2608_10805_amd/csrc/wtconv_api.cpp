@@ -492,7 +492,17 @@ bool make_grad_plan(const wtconv_desc& d, GradPlan& gp)
 struct GradExec {
     bool use = false;
     GradPlan gp;
+    int Lf = 0;           // levels whose kernel gradients grad_kernel forms
+    bool coarse = false;  // levels Lf+1..L: backward of the coarse sub-problem on X_m, dY_m
 };
+
+// The gradient pass sheds the levels above m (the first level whose grid is
+// at most 8 x 8) to a coarse sub-problem on the level-m carriers of x and dy
+// when that removes at least this many levels and more than one plane is
+// resident per batch (each deep level is then a row pass over every resident
+// plane). Measured on MI355X, backward us, split / not: 28x28 B64 L4 174 / 198,
+// L5 187 / 238, B128 L5 278 / 439; 56x56 (one resident plane) B128 L5 429 / 382.
+constexpr int kGradSplitMinShed = 2;
 
 // Measured on MI355X: the gradient pass beats the fused backward when the
 // plane's first level at most 8 x 8 is level 2 or deeper (planes above 16 x 16)
@@ -503,7 +513,15 @@ GradExec choose_grad(const wtconv_desc& d)
 {
     GradExec ge;
     if (use_tiny(d) || tiny_level(d) < 2 || d.L < 2) return ge;
-    ge.use = make_grad_plan(d, ge.gp);
+    const int m = tiny_level(d);
+    wtconv_desc f = d;
+    if (d.L - m >= kGradSplitMinShed) {
+        GradPlan full;
+        if (make_grad_plan(d, full) && full.PP > 1) f.L = m;
+    }
+    ge.use = make_grad_plan(f, ge.gp);
+    ge.Lf = f.L;
+    ge.coarse = d.L > f.L;
     return ge;
 }
 
@@ -584,19 +602,29 @@ size_t forward_ws(const wtconv_desc& d)
 
 size_t backward_ws(const wtconv_desc& d);
 
-// Gradient-pass workspace: [partials][forward workspace of dx]
+// Gradient-pass workspace: [partials][X_m][dY_m][coarse backward][forward workspace of dx]
 size_t grad_partial_bytes(const wtconv_desc& d, const GradExec& ge)
 {
-    return align256((size_t)ge.gp.nchunks * d.C * wtc::partial_floats_per_channel(d.k, d.L) * 4);
+    return align256((size_t)ge.gp.nchunks * d.C * wtc::partial_floats_per_channel(d.k, ge.Lf) * 4);
+}
+
+
+size_t grad_coarse_bytes(const wtconv_desc& d, const GradExec& ge)
+{
+    if (!ge.coarse) return 0;
+    const size_t sub = backward_ws(coarse_desc(d, ge.Lf));
+    if (sub == kUnsupported) return kUnsupported;
+    return 2 * align256(level_floats(d, ge.Lf) * 4) + sub;
 }
 
 size_t backward_ws(const wtconv_desc& d)
 {
     const GradExec ge = choose_grad(d);
     if (ge.use) {
+        const size_t coarse = grad_coarse_bytes(d, ge);
         const size_t fwd = forward_ws(d);
-        if (fwd == kUnsupported) return kUnsupported;
-        return grad_partial_bytes(d, ge) + fwd;
+        if (coarse == kUnsupported || fwd == kUnsupported) return kUnsupported;
+        return grad_partial_bytes(d, ge) + coarse + fwd;
     }
     const Exec ex = choose(d, true);
     if (ex.mode == Mode::None) return kUnsupported;
@@ -738,13 +766,28 @@ wtconv_status partials_impl(const wtconv_desc& d, const void* x, const void* dy,
 {
     const GradExec ge = choose_grad(d);
     if (ge.use) {
-        const wtconv_status st = grad_pass(d, ge, x, dy, reinterpret_cast<float*>(ws), skip_base, stream);
+        const size_t part = grad_partial_bytes(d, ge);
+        wtconv_status st = WTCONV_OK;
+        if (ge.coarse) {
+            // kernel gradients of levels Lf+1..L: the coarse sub-problem's on
+            // the level-Lf carriers of x and dy (no dx, no base path)
+            const size_t n1 = align256(level_floats(d, ge.Lf) * 4);
+            float* x1 = reinterpret_cast<float*>(ws + part);
+            float* dy1 = reinterpret_cast<float*>(ws + part + n1);
+            st = carrier(d, ge.Lf, x, x1, stream);
+            if (st == WTCONV_OK) st = carrier(d, ge.Lf, dy, dy1, stream);
+            if (st == WTCONV_OK)
+                st = partials_impl(coarse_desc(d, ge.Lf), x1, dy1, shift_params(p, ge.Lf), nullptr, ws + part + 2 * n1,
+                                   1, stream);
+            if (st != WTCONV_OK) return st;
+        }
+        st = grad_pass(d, ge, x, dy, reinterpret_cast<float*>(ws), skip_base, stream);
         if (st != WTCONV_OK || !dx) return st;
         // dx: the forward pass on dy with every kernel rotated by 180 degrees
         wtc::ParamPtrs pr = p;
         pr.rot = 1;
         pr.b0 = nullptr;  // the bias does not reach dx
-        return forward_impl(d, dy, pr, dx, ws + grad_partial_bytes(d, ge), skip_base, stream);
+        return forward_impl(d, dy, pr, dx, ws + part + grad_coarse_bytes(d, ge), skip_base, stream);
     }
     const Exec ex = choose(d, true);
     if (ex.mode == Mode::None) return WTCONV_ERR_UNSUPPORTED;
@@ -800,7 +843,16 @@ wtconv_status finalize_impl(const wtconv_desc& d, const wtc::ParamPtrs& p, const
                             int skip_base, hipStream_t stream)
 {
     const GradExec ge = choose_grad(d);
-    if (ge.use) return reduce(d, d.L, ge.gp.nchunks, p, gr, ws, skip_base, stream);
+    if (ge.use) {
+        if (ge.coarse) {
+            const size_t part = grad_partial_bytes(d, ge);
+            const size_t n1 = align256(level_floats(d, ge.Lf) * 4);
+            const wtconv_status st = finalize_impl(coarse_desc(d, ge.Lf), shift_params(p, ge.Lf),
+                                                   shift_grads(gr, ge.Lf), ws + part + 2 * n1, 1, stream);
+            if (st != WTCONV_OK) return st;
+        }
+        return reduce(d, ge.Lf, ge.gp.nchunks, p, gr, ws, skip_base, stream);
+    }
     const Exec ex = choose(d, true);
     switch (ex.mode) {
         case Mode::None: return WTCONV_ERR_UNSUPPORTED;
