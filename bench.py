@@ -56,6 +56,8 @@ def parse():
     ap.add_argument("--table-steps", type=int, default=10)
     ap.add_argument("--summarize-trace", metavar="DB",
                     help="write the kernel statistics of a rocprofv3 --kernel-trace database to --out and exit")
+    ap.add_argument("--summarize-counters", metavar="DB",
+                    help="write the SQ instruction counters of a rocprofv3 --pmc database to --out and exit")
     ap.add_argument("--summarize-traffic", nargs=4, metavar=("FETCH_DB", "WRITE_DB", "COPY_FETCH_DB", "COPY_WRITE_DB"),
                     help="write per-launch HBM bytes from rocprofv3 FETCH_SIZE / WRITE_SIZE databases of this "
                          "benchmark and of --copy-calibration-mib runs to --out and exit")
@@ -379,8 +381,52 @@ def summarize_traffic(fetch_db, write_db, cfetch_db, cwrite_db, copy_mib, out, c
         f.write("\n".join(lines) + "\n")
 
 
+SQ_COUNTERS = ("SQ_WAVES", "SQ_INSTS_VALU", "SQ_INSTS_LDS", "SQ_INSTS_SALU", "SQ_WAVE_CYCLES", "SQ_BUSY_CYCLES",
+               "SQ_ACTIVE_INST_VALU", "SQ_WAIT_INST_LDS")
+
+
+def summarize_counters(db, out, command):
+    """Instruction counters per launch of the step's forward and gradient
+    kernels (one rocprofv3 --pmc run with the eight SQ counters above), set
+    against the algorithmic FMA count: each full-lane wavefront FMA does 64 of
+    them, and a SIMD issues one wavefront VALU instruction per 4 cycles."""
+    from paper_2608_10805_amd import iomodel
+    B, C, H, W, k, L = (WORKLOAD[n] for n in ("B", "C", "H", "W", "k", "L"))
+    work = iomodel.single_pass_work(B, C, H, W, k, L, "f32")
+    per = {name: _counter_per_kernel(db, name) for name in SQ_COUNTERS}
+    lines = ["# SQ instruction counters per kernel launch, fused WTConv fwd+bwd benchmark step",
+             f"# workload: B={B} C={C} H=W={H} k={k} L={L} fp32 (ConvNeXt-T stage 1), MI355X",
+             f"# command: {command}",
+             f"workload: {WORKLOAD['workload']}",
+             f"kernel_source_sha256: {kernel_source_hash()}"]
+    simds = 256 * 4
+    for key in ("forward", "grad"):
+        prefix = STEP_KERNELS[key]
+        vals = {}
+        for name in SQ_COUNTERS:
+            v = [x for n, x in per[name].items() if prefix in n]
+            if v:
+                vals[name] = sum(v) / len(v)
+        if "SQ_INSTS_VALU" not in vals:
+            continue
+        fma_wave = work.fma_fwd / 64.0
+        issue_cycles = 4.0 * vals["SQ_INSTS_VALU"] / simds
+        lines.append(f"# {key} = {prefix}")
+        for name in SQ_COUNTERS:
+            if name in vals:
+                lines.append(f"{key}_{name}: {vals[name]:.0f}")
+        lines.append(f"# {key}: algorithmic FMAs {work.fma_fwd:.4g} = {fma_wave:.4g} full-lane wavefront FMAs, "
+                     f"{fma_wave / vals['SQ_INSTS_VALU']:.3f} of the VALU instructions issued; VALU issue per SIMD "
+                     f"{issue_cycles:.4g} cycles = {issue_cycles / 2.2e3:.1f} us at 2.2 GHz")
+    with open(out, "w") as f:
+        f.write("\n".join(lines) + "\n")
+
+
 def main():
     args = parse()
+    if args.summarize_counters:
+        summarize_counters(args.summarize_counters, args.out, args.command)
+        return
     if args.summarize_trace:
         summarize_trace(args.summarize_trace, args.out, args.command)
         return
