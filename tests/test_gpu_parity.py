@@ -185,6 +185,7 @@ GRAD = [
     (3, 400, 52, 52, 7, 4, "bf16"),
     (2, 3, 45, 61, 5, 6, "f32"),
     (6, 5, 30, 18, 5, 2, "f16"),
+    (7, 3, 19, 19, 7, 2, "f32"),  # level-1 tiles over three rounds, 6 resident planes and a ragged batch
 ]
 
 
