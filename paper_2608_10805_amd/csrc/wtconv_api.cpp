@@ -130,6 +130,25 @@ int lds_floats_for(const wtconv_desc& d, bool bwd, int PP, const PlaneGeom& g)
     return total > (1L << 30) ? (1 << 30) : (int)total;
 }
 
+// Single-round variant: one 4x4 block / output tile per thread and one
+// register tile per lane for every level.
+bool single_round(const wtconv_desc& d, int PP, const PlaneGeom& g)
+{
+    if ((long)PP * g.tiles_x * g.tiles_y > wtc::kThreads) return false;
+    for (int l = 1; l <= d.L; ++l) {
+        const LevelGeom& lg = g.lv[l];
+        if ((long)PP * (lg.eh / lg.T) * (lg.ew / lg.T) > 64) return false;
+    }
+    return true;
+}
+
+// Lane use of one workgroup's output-tile rounds with PP resident planes.
+double tile_use(const PlaneGeom& g, int PP)
+{
+    const long nt = (long)PP * g.tiles_x * g.tiles_y;
+    return (double)nt / ((double)wtc::kThreads * cdiv(nt, wtc::kThreads));
+}
+
 bool make_plan(const wtconv_desc& d, bool bwd, Plan& pl)
 {
     const long px = (long)ceil_to(d.H, 4) * ceil_to(d.W, 4);
@@ -148,14 +167,29 @@ bool make_plan(const wtconv_desc& d, bool bwd, Plan& pl)
         }
     }
     if (PP == 0) return false;
-    pl.PP = PP;
-    // single-round variant: one 4x4 block / output tile per thread and one
-    // register tile per lane for every level
-    pl.one_round = (long)PP * pl.g.tiles_x * pl.g.tiles_y <= wtc::kThreads ? 1 : 0;
-    for (int l = 1; l <= d.L; ++l) {
-        const LevelGeom& lg = pl.g.lv[l];
-        if ((long)PP * (lg.eh / lg.T) * (lg.ew / lg.T) > 64) pl.one_round = 0;
+    // Forward: a plane count whose layout runs in the single-round variant
+    // (fewer registers, no round loops), with at least two workgroups per CU
+    // and at least 3/4 of the output-tile lane use, beats a general one.
+    // Measured on MI355X, k = 5 unless noted: 28 x 28 L = 1 54.5 -> 40.6 us,
+    // L = 2 55.5 -> 46.1 us; 56 x 56 L = 1 (B = 128) 153.6 -> 121.1 us; 40 x 40
+    // k = 7 L = 4 155.9 -> 81.4 us; at 14 x 14 L = 3 the general variant's
+    // higher lane use wins (4 single-round planes 118 us, 9 general 98 us).
+    if (!bwd && !single_round(d, PP, pl.g)) {
+        const double use = tile_use(pl.g, PP);
+        for (int pp = want; pp >= 1; --pp) {
+            PlaneGeom g;
+            if (!layout(d, pp, bwd, g) || !single_round(d, pp, g)) continue;
+            const int lds = lds_floats_for(d, bwd, pp, g);
+            if (lds <= kLdsFloatsMax / 2 && tile_use(g, pp) >= 0.75 * use) {
+                PP = pp;
+                pl.g = g;
+                pl.lds_floats = lds;
+                break;
+            }
+        }
     }
+    pl.PP = PP;
+    pl.one_round = single_round(d, PP, pl.g) ? 1 : 0;
     // Forward, single round, level 1 in 4x4 tiles and at least three levels:
     // the levels from 3 on (small grids, each otherwise a round of its own
     // with a handful of busy lanes) take 4x4 tiles too and share level 1's
@@ -167,9 +201,8 @@ bool make_plan(const wtconv_desc& d, bool bwd, Plan& pl)
             long lanes = (long)PP * (gm.lv[1].eh / 4) * (gm.lv[1].ew / 4);
             for (int l = 3; l <= d.L; ++l) lanes += (long)PP * (gm.lv[l].eh / 4) * (gm.lv[l].ew / 4);
             const int lds = lds_floats_for(d, bwd, PP, gm);
-            const bool fits = lds <= kLdsFloatsShared || (PP == 1 && lds <= kLdsFloatsMax);
-            // and keep the workgroups per CU of the unmerged layout
-            if (lanes <= 64 && fits && kLdsFloatsMax / lds >= kLdsFloatsMax / pl.lds_floats) {
+            // if it keeps the workgroups per CU of the unmerged layout
+            if (lanes <= 64 && lds <= kLdsFloatsMax && kLdsFloatsMax / lds >= kLdsFloatsMax / pl.lds_floats) {
                 pl.g = gm;
                 pl.lds_floats = lds;
                 pl.merge_deep = 1;
