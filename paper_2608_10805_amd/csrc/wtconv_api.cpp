@@ -513,10 +513,13 @@ bool make_grad_plan(const wtconv_desc& d, GradPlan& gp)
     // One round of resident workgroups: the per-workgroup setup and the final
     // reduction of 3 x 25 sums per thread are paid once per workgroup, so few
     // long-running workgroups that fill every CU beat many short ones
-    // (measured on MI355X at the ConvNeXt-T shapes).
+    // (measured on MI355X at the ConvNeXt-T shapes). The chunk count rounds
+    // down so that the grid fits the slots: rounding 512 / 192 up to 3 chunks
+    // left a second round of 64 workgroups (28 x 28, L = 3: 150 -> 143 us per
+    // backward at B = 64, 289 -> 250 us at B = 128 with 2 chunks).
     const int wgs_per_cu = std::max(1, std::min(3, kLdsFloatsMax / gp.lds_floats));
     const int slots = 256 * wgs_per_cu;
-    const int chunks = std::max(1, std::min(d.B, (int)((double)slots / d.C + 0.5)));
+    const int chunks = std::max(1, std::min(d.B, slots / d.C));
     gp.nb = ceil_to(cdiv(d.B, chunks), gp.PP);
     gp.nchunks = cdiv(d.B, gp.nb);
     return true;
