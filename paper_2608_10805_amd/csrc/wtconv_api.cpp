@@ -542,13 +542,14 @@ constexpr int kGradSplitMinShed = 2;
 
 // Measured on MI355X: the gradient pass beats the fused backward when the
 // plane's first level at most 8 x 8 is level 2 or deeper (planes above 16 x 16)
-// and there are at least two levels; it then handles every level itself. For
-// smaller planes (whose coarse levels the fused backward runs as a tiny
-// sub-problem) and for L <= 1 the fused backward is as fast or faster.
+// and there is at least one level (L = 1, k = 5: 28 x 28 115 -> 94 us, 40 x 40
+// 130 -> 80 us, 56 x 56 B = 128 252 -> 231 us); it then handles every level
+// itself. For smaller planes (whose coarse levels the fused backward runs as a
+// tiny sub-problem) and for L = 0 the fused backward runs.
 GradExec choose_grad(const wtconv_desc& d)
 {
     GradExec ge;
-    if (use_tiny(d) || tiny_level(d) < 2 || d.L < 2) return ge;
+    if (use_tiny(d) || tiny_level(d) < 2 || d.L < 1) return ge;
     const int m = tiny_level(d);
     wtconv_desc f = d;
     if (d.L - m >= kGradSplitMinShed) {

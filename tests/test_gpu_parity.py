@@ -186,6 +186,7 @@ GRAD = [
     (2, 3, 45, 61, 5, 6, "f32"),
     (6, 5, 30, 18, 5, 2, "f16"),
     (7, 3, 19, 19, 7, 2, "f32"),  # level-1 tiles over three rounds, 6 resident planes and a ragged batch
+    (4, 6, 33, 29, 5, 1, "bf16"),  # one level
 ]
 
 
