@@ -439,6 +439,7 @@ struct GradPlan {
     PlaneGeom g;  // x side (zero-haloed)
     int dy_off[kMaxLevels + 1] = {}, dy_pitch[kMaxLevels + 1] = {}, dy_band[kMaxLevels + 1] = {};
     int stride = 0, PP = 1, nb = 1, nchunks = 1, lds_floats = 0;
+    int rounds = 1;  // 4x4 block rounds per plane (more than one only with PP = 1)
 };
 
 int grad_gc_floats(const wtconv_desc& d)
@@ -490,26 +491,36 @@ bool grad_layout(const wtconv_desc& d, int PP, GradPlan& gp)
     return true;
 }
 
+// Planes with more 4x4 blocks than a workgroup has threads take up to this
+// many block rounds per plane (one resident plane): 63 x 95 and similar.
+constexpr int kGradMaxRounds = 4;
+
 // Resident planes per batch: the best of (block-load lane use) x (workgroups
 // per CU, up to three) over the feasible counts; larger counts on ties.
 bool make_grad_plan(const wtconv_desc& d, GradPlan& gp)
 {
     const long per = (long)(ceil_to(d.H, 4) / 4) * (ceil_to(d.W, 4) / 4);
-    if (per > wtc::kThreads) return false;
-    const int maxpp = (int)std::min<long>(d.B, wtc::kThreads / per);
-    double best = -1.0;
-    for (int pp = 1; pp <= maxpp; ++pp) {
-        GradPlan c;
-        if (!grad_layout(d, pp, c)) continue;
-        const int wgs = std::min(3, kLdsFloatsMax / c.lds_floats);
-        const double score = (double)pp * per / wtc::kThreads * wgs;
-        if (score >= best) {
-            best = score;
-            gp = c;
-            gp.PP = pp;
+    if (per > wtc::kThreads) {
+        // one resident plane, its 4x4 blocks in several rounds per thread
+        if (per > (long)kGradMaxRounds * wtc::kThreads || !grad_layout(d, 1, gp)) return false;
+        gp.PP = 1;
+        gp.rounds = (int)cdiv(per, (long)wtc::kThreads);
+    } else {
+        const int maxpp = (int)std::min<long>(d.B, wtc::kThreads / per);
+        double best = -1.0;
+        for (int pp = 1; pp <= maxpp; ++pp) {
+            GradPlan c;
+            if (!grad_layout(d, pp, c)) continue;
+            const int wgs = std::min(3, kLdsFloatsMax / c.lds_floats);
+            const double score = (double)pp * per / wtc::kThreads * wgs;
+            if (score >= best) {
+                best = score;
+                gp = c;
+                gp.PP = pp;
+            }
         }
+        if (best < 0) return false;
     }
-    if (best < 0) return false;
     // One round of resident workgroups: the per-workgroup setup and the final
     // reduction of 3 x 25 sums per thread are paid once per workgroup, so few
     // long-running workgroups that fill every CU beat many short ones
@@ -784,6 +795,7 @@ wtconv_status grad_pass(const wtconv_desc& d, const GradExec& ge, const void* x,
     a.C = d.C;
     a.nb = ge.gp.nb;
     a.PP = ge.gp.PP;
+    a.rounds = ge.gp.rounds;
     a.vec_ok = vec_ok(x, dy, x);
     a.lds_floats = ge.gp.lds_floats;
     a.skip_base = skip_base;

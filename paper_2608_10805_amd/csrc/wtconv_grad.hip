@@ -185,7 +185,9 @@ DEV void zero_x_ring(float* __restrict__ reg, const PlaneGeom& g, int R, float r
 template <int K>
 constexpr int grad_waves_per_simd() { return K <= 5 ? 3 : 2; }
 
-template <int K, typename ST>
+// MR: planes with more 4x4 blocks than threads, one resident plane, block
+// rounds (a separate instantiation keeps the one-round kernel's registers).
+template <int K, typename ST, bool MR>
 __global__ void __launch_bounds__(kThreads, grad_waves_per_simd<K>()) grad_kernel(const GradArgs a)
 {
     constexpr int R = K / 2, KK = K * K;
@@ -226,38 +228,9 @@ __global__ void __launch_bounds__(kThreads, grad_waves_per_simd<K>()) grad_kerne
     const int per = g.tiles_x * g.tiles_y;
     for (int b0 = b_begin; b0 < b_end; b0 += a.PP) {
         const int np = min(a.PP, b_end - b0);
-        const bool mine = tid < np * per;  // at most one block per thread (planned on the host)
-        const TileIdx ti = tile_at(mine ? tid : 0, per, g.r_tiles, g.tiles_x, g.r_tiles_x, 4);
-        float* reg = planes + ti.p * stride;
-
-        // 1. x block -> LDS with its levels 1-2; dy block and its levels 1-2 in registers
-        if (alias1 && b0 != b_begin)
-            for (int p = 0; p < np; ++p) zero_x_ring(planes + p * stride, g, R, a.r_ring, tid);
-        float dyb[4][4];
-        if (mine) {
-            const long plane = (long)(b0 + ti.p) * C + c;
-            float v[4][4];
-            fetch_block<ST>(xs + plane * HW, g.H, g.W, ti.j0, ti.i0, vec, v);
-            store_block<K>(v, reg, g, ti.j0, ti.i0);
-            fetch_block<ST>(dys + plane * HW, g.H, g.W, ti.j0, ti.i0, vec, dyb);
-        }
-        __syncthreads();
-
-        // 2. base correlation; x level 3
-        if (mine && !skip_base) {
-            corr_tile<K, 4>(reg, g.xpitch, ti.j0, ti.i0, dyb, g0);
-#pragma unroll
-            for (int r = 0; r < 4; ++r) gdy += (dyb[r][0] + dyb[r][1]) + (dyb[r][2] + dyb[r][3]);
-        }
-        if (L >= 3) {
-            const LevelGeom& lg = g.lv[3];
-            const LevelGeom& lp = g.lv[2];
-            analysis_level(planes + lp.off, lp.pitch, planes + lg.off, lg, R, np, stride, tid);
-        }
-        __syncthreads();
-
-        // 3. dy levels 1-2 -> compact pyramid; x level 4
-        if (mine) {
+        // dy levels 1-2 of one block -> the compact pyramid
+        auto dy_levels = [&](const TileIdx& ti, const float (&dyb)[4][4]) {
+            float* reg = planes + ti.p * stride;
             float d1[2][2][4], d2[4];
 #pragma unroll
             for (int ya = 0; ya < 2; ++ya)
@@ -281,6 +254,77 @@ __global__ void __launch_bounds__(kThreads, grad_waves_per_simd<K>()) grad_kerne
                 float* o = reg + a.dy_off[2] + (ti.j0 >> 2) * a.dy_pitch[2] + (ti.i0 >> 2);
 #pragma unroll
                 for (int bq = 0; bq < 4; ++bq) o[bq * a.dy_band[2]] = d2[bq];
+            }
+        };
+        // base correlation of one block (dy centre, x window) and its dy sum
+        auto base_corr = [&](const TileIdx& ti, const float (&dyb)[4][4]) {
+            corr_tile<K, 4>(planes + ti.p * stride, g.xpitch, ti.j0, ti.i0, dyb, g0);
+#pragma unroll
+            for (int r = 0; r < 4; ++r) gdy += (dyb[r][0] + dyb[r][1]) + (dyb[r][2] + dyb[r][3]);
+        };
+
+        if constexpr (!MR) {
+            const bool mine = tid < np * per;  // at most one block per thread (planned on the host)
+            const TileIdx ti = tile_at(mine ? tid : 0, per, g.r_tiles, g.tiles_x, g.r_tiles_x, 4);
+
+            // 1. x block -> LDS with its levels 1-2; dy block in registers
+            if (alias1 && b0 != b_begin)
+                for (int p = 0; p < np; ++p) zero_x_ring(planes + p * stride, g, R, a.r_ring, tid);
+            float dyb[4][4];
+            if (mine) {
+                const long plane = (long)(b0 + ti.p) * C + c;
+                float v[4][4];
+                fetch_block<ST>(xs + plane * HW, g.H, g.W, ti.j0, ti.i0, vec, v);
+                store_block<K>(v, planes + ti.p * stride, g, ti.j0, ti.i0);
+                fetch_block<ST>(dys + plane * HW, g.H, g.W, ti.j0, ti.i0, vec, dyb);
+            }
+            __syncthreads();
+
+            // 2. base correlation; x level 3
+            if (mine && !skip_base) base_corr(ti, dyb);
+            if (L >= 3) {
+                const LevelGeom& lg = g.lv[3];
+                const LevelGeom& lp = g.lv[2];
+                analysis_level(planes + lp.off, lp.pitch, planes + lg.off, lg, R, np, stride, tid);
+            }
+            __syncthreads();
+
+            // 3. dy levels 1-2 -> compact pyramid
+            if (mine) dy_levels(ti, dyb);
+        } else {
+            // One resident plane with more 4x4 blocks than threads: each phase
+            // walks the block rounds and fetches its dy blocks itself (they
+            // cannot stay in registers across rounds). Every base correlation
+            // reads the x plane before the barrier after which dy level 1 may
+            // be stored over it.
+            if (alias1 && b0 != b_begin) zero_x_ring(planes, g, R, a.r_ring, tid);
+            const long plane = (long)b0 * C + c;
+            for (int it = tid; it < per; it += kThreads) {
+                const TileIdx ti = tile_at(it, per, g.r_tiles, g.tiles_x, g.r_tiles_x, 4);
+                float v[4][4];
+                fetch_block<ST>(xs + plane * HW, g.H, g.W, ti.j0, ti.i0, vec, v);
+                store_block<K>(v, planes, g, ti.j0, ti.i0);
+            }
+            __syncthreads();
+            if (!skip_base) {
+                for (int it = tid; it < per; it += kThreads) {
+                    const TileIdx ti = tile_at(it, per, g.r_tiles, g.tiles_x, g.r_tiles_x, 4);
+                    float dyb[4][4];
+                    fetch_block<ST>(dys + plane * HW, g.H, g.W, ti.j0, ti.i0, vec, dyb);
+                    base_corr(ti, dyb);
+                }
+            }
+            if (L >= 3) {
+                const LevelGeom& lg = g.lv[3];
+                const LevelGeom& lp = g.lv[2];
+                analysis_level(planes + lp.off, lp.pitch, planes + lg.off, lg, R, np, stride, tid);
+            }
+            __syncthreads();
+            for (int it = tid; it < per; it += kThreads) {
+                const TileIdx ti = tile_at(it, per, g.r_tiles, g.tiles_x, g.r_tiles_x, 4);
+                float dyb[4][4];
+                fetch_block<ST>(dys + plane * HW, g.H, g.W, ti.j0, ti.i0, vec, dyb);
+                dy_levels(ti, dyb);
             }
         }
         if (L >= 4) {
@@ -346,15 +390,25 @@ __global__ void __launch_bounds__(kThreads, grad_waves_per_simd<K>()) grad_kerne
     for (int i = tid; i < 4 * KK * (L - 2); i += kThreads) dst[KK + 8 * KK + i] = gco[i];
 }
 
+template <int K, typename ST, bool MR>
+hipError_t launch_grad_v(const GradArgs& a, int grid, hipStream_t s)
+{
+    const size_t bytes = (size_t)a.lds_floats * sizeof(float);
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&grad_kernel<K, ST, MR>),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((grad_kernel<K, ST, MR>), dim3(grid), dim3(kThreads), bytes, s, a);
+    return hipGetLastError();
+}
+
 template <int K, typename ST>
 hipError_t launch_grad_t(const GradArgs& a, int grid, hipStream_t s)
 {
-    const size_t bytes = (size_t)a.lds_floats * sizeof(float);
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&grad_kernel<K, ST>),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((grad_kernel<K, ST>), dim3(grid), dim3(kThreads), bytes, s, a);
-    return hipGetLastError();
+    if (a.rounds > 1) {
+        if (a.PP != 1) return hipErrorInvalidValue;  // block rounds need one resident plane
+        return launch_grad_v<K, ST, true>(a, grid, s);
+    }
+    return launch_grad_v<K, ST, false>(a, grid, s);
 }
 
 }  // namespace

@@ -145,6 +145,7 @@ struct GradArgs {
     float* partial;  // [nchunks][C][NP] kernel-gradient partials, resident layout
     int B, C;
     int nb, PP;
+    int rounds;      // 4x4 block rounds per plane: 1, or more with one resident plane
     int vec_ok;      // 1 if both plane bases allow 16-byte (f32) / 8-byte (16-bit) loads
     int lds_floats;
     int skip_base;   // 1: no base-kernel gradient (coarse sub-problem)

@@ -187,6 +187,10 @@ GRAD = [
     (6, 5, 30, 18, 5, 2, "f16"),
     (7, 3, 19, 19, 7, 2, "f32"),  # level-1 tiles over three rounds, 6 resident planes and a ragged batch
     (4, 6, 33, 29, 5, 1, "bf16"),  # one level
+    (2, 3, 63, 95, 5, 3, "f32"),  # more 4x4 blocks than threads: two block rounds per plane
+    (3, 260, 65, 61, 5, 2, "f32"),  # two block rounds, three planes per workgroup in turn
+    (2, 3, 65, 61, 3, 2, "bf16"),
+    (1, 2, 70, 66, 7, 1, "f16"),
 ]
 
 
