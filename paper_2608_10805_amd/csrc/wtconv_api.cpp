@@ -740,7 +740,8 @@ wtconv_status carrier(const wtconv_desc& d, int m, const void* in, float* out, h
     c.H1 = cd.H;
     c.W1 = cd.W;
     c.m = m;
-    c.vec_ok = (d.W % 4 == 0 && ((uintptr_t)in & (d.dtype == WTCONV_F32 ? 15 : 7)) == 0) ? 1 : 0;
+    // m = 1 reads row pairs (W even suffices), deeper levels rows of 4-multiples
+    c.vec_ok = (d.W % (m == 1 ? 2 : 4) == 0 && ((uintptr_t)in & (d.dtype == WTCONV_F32 ? 15 : 7)) == 0) ? 1 : 0;
     return hip_status(wtc::launch_carrier(d.dtype, c, stream));
 }
 

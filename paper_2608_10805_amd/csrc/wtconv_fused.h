@@ -157,13 +157,33 @@ DEV void st_row(float* __restrict__ p, const float* v)
 //    the level grids are written as the zeros they are.
 // ----------------------------------------------------------------------------
 // A 4x4 pixel block whose top-left pixel is (y0, x0) of an H x W plane; pixels
-// outside the plane (including negative coordinates) read as zero.
+// outside the plane (including negative coordinates) read as zero. vw is the
+// vector width the plane allows: 4 (W % 4 == 0), 2 (W even: a pair starting at
+// an even column lies wholly inside or wholly outside the plane) or 1; x0 is a
+// multiple of 4.
 template <typename T>
-DEV void fetch_block(const T* __restrict__ src, int H, int W, int y0, int x0, bool vec, float (&v)[4][4])
+DEV void fetch_block(const T* __restrict__ src, int H, int W, int y0, int x0, int vw, float (&v)[4][4])
 {
-    if (vec && y0 >= 0 && x0 >= 0 && y0 + 4 <= H && x0 + 4 <= W) {  // vec: W % 4 == 0 and x0 % 4 == 0
+    if (vw == 4 && y0 >= 0 && x0 >= 0 && y0 + 4 <= H && x0 + 4 <= W) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) load4(src + (long)(y0 + r) * W + x0, v[r]);
+    } else if (vw == 2) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int y = y0 + r;
+#pragma unroll
+            for (int c = 0; c < 4; c += 2) {
+                const int x = x0 + c;
+                if (y >= 0 && y < H && x >= 0 && x < W) {
+                    float pr[2];
+                    load2(src + (long)y * W + x, pr);
+                    v[r][c] = pr[0];
+                    v[r][c + 1] = pr[1];
+                } else {
+                    v[r][c] = v[r][c + 1] = 0.f;
+                }
+            }
+        }
     } else {
 #pragma unroll
         for (int r = 0; r < 4; ++r)
@@ -212,10 +232,10 @@ DEV void store_block(const float (&v)[4][4], float* __restrict__ reg, const Plan
 // written as the zeros they are.
 template <int K, typename T>
 DEV void load_block(const T* __restrict__ src, float* __restrict__ reg, const PlaneGeom& g, int y0, int x0,
-                    bool vec)
+                    int vw)
 {
     float v[4][4];
-    fetch_block<T>(src, g.H, g.W, y0, x0, vec, v);
+    fetch_block<T>(src, g.H, g.W, y0, x0, vw, v);
     store_block<K>(v, reg, g, y0, x0);
 }
 
@@ -711,15 +731,30 @@ DEV void synth_tile(const float* __restrict__ reg, const PlaneGeom& g, int y0, i
         }
 }
 
+// Store a 4x4 output tile at (y0, x0) (non-negative, x0 a multiple of 4) of an
+// H x W plane, cropped to the plane; vw as for fetch_block.
 template <typename T>
-DEV void store_tile(T* __restrict__ plane, int H, int W, int y0, int x0, const float (&v)[4][4], bool vec)
+DEV void store_tile(T* __restrict__ plane, int H, int W, int y0, int x0, const float (&v)[4][4], int vw)
 {
 #pragma unroll
     for (int oy = 0; oy < 4; ++oy) {
         const int y = y0 + oy;
         if (y >= H || x0 >= W) break;
         T* row = plane + (long)y * W + x0;
-        if (vec && x0 + 4 <= W) {
+        if (vw == 2) {
+#pragma unroll
+            for (int c = 0; c < 4; c += 2) {
+                if (x0 + c >= W) break;
+                if constexpr (sizeof(T) == 4) {
+                    *reinterpret_cast<float2*>(row + c) = make_float2(v[oy][c], v[oy][c + 1]);
+                } else {
+                    T h[2] = {from_f32<T>(v[oy][c]), from_f32<T>(v[oy][c + 1])};
+                    uint32_t packed;
+                    __builtin_memcpy(&packed, h, 4);
+                    *reinterpret_cast<uint32_t*>(row + c) = packed;
+                }
+            }
+        } else if (vw == 4 && x0 + 4 <= W) {
             if constexpr (sizeof(T) == 4) {
                 *reinterpret_cast<float4*>(row) = make_float4(v[oy][0], v[oy][1], v[oy][2], v[oy][3]);
             } else {
@@ -803,9 +838,8 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(const FusedArgs a)
     const ST* aux = reinterpret_cast<const ST*>(a.aux);
     ST* out = reinterpret_cast<ST*>(a.out);
     const bool have_out = out != nullptr;
-    const bool vec_ok = a.vec_ok != 0;
-    const bool vec_store = vec_ok && (PW % 4) == 0;
-    const bool vec_load = vec_store;
+    // vector width of the plane's rows (plane bases are 16-byte aligned when vec_ok)
+    const int vw = a.vec_ok == 0 ? 1 : ((PW % 4) == 0 ? 4 : ((PW % 2) == 0 ? 2 : 1));
     const int q = wave;  // the subband this wavefront filters
 
     for (int i = tid; i < a.lds_floats / 4; i += kThreads) lds4[i] = make_float4(0.f, 0.f, 0.f, 0.f);
@@ -842,10 +876,10 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(const FusedArgs a)
                 const TileIdx ti = tile_at(it, per, g.r_tiles, tx, g.r_tiles_x, 4);
                 const long plane = (long)(b0 + ti.p) * C + c;
                 float v[4][4];
-                fetch_block<ST>(in + plane * HW, PH, PW, oy + ti.j0, ox + ti.i0, vec_load, v);
+                fetch_block<ST>(in + plane * HW, PH, PW, oy + ti.j0, ox + ti.i0, vw, v);
                 store_block<K>(v, side_in + ti.p * stride, g, ti.j0, ti.i0);
                 if constexpr (BWD) {
-                    fetch_block<ST>(aux + plane * HW, PH, PW, oy + ti.j0, ox + ti.i0, vec_load, v);
+                    fetch_block<ST>(aux + plane * HW, PH, PW, oy + ti.j0, ox + ti.i0, vw, v);
                     store_block<K>(v, side_aux + ti.p * stride, g, ti.j0, ti.i0);
                 }
             }
@@ -931,7 +965,7 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(const FusedArgs a)
                         cr.cx = (ox + ti.i0) >> cr.m;
                     }
                     synth_tile<K>(reg, g, ti.j0, ti.i0, acc, cr);
-                    store_tile<ST>(out + plane * HW, PH, PW, oy + ti.j0, ox + ti.i0, acc, vec_store);
+                    store_tile<ST>(out + plane * HW, PH, PW, oy + ti.j0, ox + ti.i0, acc, vw);
                 } else if (!skip_base) {
                     load_center<K, 4>(reg, g.xpitch, ti.j0, ti.i0, ctr);
                 }

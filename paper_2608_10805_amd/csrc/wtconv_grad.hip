@@ -204,7 +204,7 @@ __global__ void __launch_bounds__(kThreads, grad_waves_per_simd<K>()) grad_kerne
     const int L = g.L;
     const long HW = (long)g.H * g.W;
     const bool skip_base = a.skip_base != 0;
-    const bool vec = a.vec_ok != 0 && (g.W % 4) == 0;
+    const int vw = a.vec_ok == 0 ? 1 : ((g.W % 4) == 0 ? 4 : ((g.W % 2) == 0 ? 2 : 1));  // row vector width
     const bool alias1 = L >= 1 && a.dy_off[1] == 0;  // dy level 1 is stored over the x plane
     const int q = wave;                              // the subband this wavefront correlates
 
@@ -274,9 +274,9 @@ __global__ void __launch_bounds__(kThreads, grad_waves_per_simd<K>()) grad_kerne
             if (mine) {
                 const long plane = (long)(b0 + ti.p) * C + c;
                 float v[4][4];
-                fetch_block<ST>(xs + plane * HW, g.H, g.W, ti.j0, ti.i0, vec, v);
+                fetch_block<ST>(xs + plane * HW, g.H, g.W, ti.j0, ti.i0, vw, v);
                 store_block<K>(v, planes + ti.p * stride, g, ti.j0, ti.i0);
-                fetch_block<ST>(dys + plane * HW, g.H, g.W, ti.j0, ti.i0, vec, dyb);
+                fetch_block<ST>(dys + plane * HW, g.H, g.W, ti.j0, ti.i0, vw, dyb);
             }
             __syncthreads();
 
@@ -302,7 +302,7 @@ __global__ void __launch_bounds__(kThreads, grad_waves_per_simd<K>()) grad_kerne
             for (int it = tid; it < per; it += kThreads) {
                 const TileIdx ti = tile_at(it, per, g.r_tiles, g.tiles_x, g.r_tiles_x, 4);
                 float v[4][4];
-                fetch_block<ST>(xs + plane * HW, g.H, g.W, ti.j0, ti.i0, vec, v);
+                fetch_block<ST>(xs + plane * HW, g.H, g.W, ti.j0, ti.i0, vw, v);
                 store_block<K>(v, planes, g, ti.j0, ti.i0);
             }
             __syncthreads();
@@ -310,7 +310,7 @@ __global__ void __launch_bounds__(kThreads, grad_waves_per_simd<K>()) grad_kerne
                 for (int it = tid; it < per; it += kThreads) {
                     const TileIdx ti = tile_at(it, per, g.r_tiles, g.tiles_x, g.r_tiles_x, 4);
                     float dyb[4][4];
-                    fetch_block<ST>(dys + plane * HW, g.H, g.W, ti.j0, ti.i0, vec, dyb);
+                    fetch_block<ST>(dys + plane * HW, g.H, g.W, ti.j0, ti.i0, vw, dyb);
                     base_corr(ti, dyb);
                 }
             }
@@ -323,7 +323,7 @@ __global__ void __launch_bounds__(kThreads, grad_waves_per_simd<K>()) grad_kerne
             for (int it = tid; it < per; it += kThreads) {
                 const TileIdx ti = tile_at(it, per, g.r_tiles, g.tiles_x, g.r_tiles_x, 4);
                 float dyb[4][4];
-                fetch_block<ST>(dys + plane * HW, g.H, g.W, ti.j0, ti.i0, vec, dyb);
+                fetch_block<ST>(dys + plane * HW, g.H, g.W, ti.j0, ti.i0, vw, dyb);
                 dy_levels(ti, dyb);
             }
         }

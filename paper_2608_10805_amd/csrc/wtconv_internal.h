@@ -100,8 +100,8 @@ struct CarrierArgs {
     long planes;
     int H, W, H1, W1;
     int m;
-    int vec_ok;  // 1 if W % 4 == 0 and the input base allows 4-element vector loads
-                 // (2-element loads for m = 1, 4-element ones beyond)
+    int vec_ok;  // 1 if the rows allow vector loads: 2-element loads for m = 1 (W even),
+                 // 4-element ones beyond (W % 4 == 0); the input base is 16-byte aligned
 };
 
 // Planes of at most 8 x 8 pixels (wtconv_tiny.hip): one workgroup per four
