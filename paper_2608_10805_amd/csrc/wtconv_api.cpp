@@ -50,15 +50,20 @@ int round_cap(int T)
 // share at 128 bytes per cycle (the backward pass reads two windows). The
 // tile with the smallest estimated time max(FMA, LDS) wins, larger tiles on
 // ties; rounds are capped by the registers that hold in-place results.
-int pick_tile(int h, int w, int PP, int k, bool bwd)
+// With one_pref, tile edges that take a single round are preferred whenever
+// one exists (so that the plan can use the single-round kernel variant).
+int pick_tile(int h, int w, int PP, int k, bool bwd, bool one_pref = false)
 {
     const int R = k / 2;
     long best_cost = -1;
     int best = 0;
+    bool one_avail = false;
+    for (int T : {4, 2, 1})
+        if (one_pref && (long)PP * (ceil_to(h, T) / T) * (ceil_to(w, T) / T) <= 64) one_avail = true;
     for (int T : {4, 2, 1}) {
         const long tiles = (long)PP * (ceil_to(h, T) / T) * (ceil_to(w, T) / T);
         const long rounds = cdiv(tiles, 64);
-        if (rounds > round_cap(T)) continue;
+        if (rounds > round_cap(T) || (one_avail && rounds > 1)) continue;
         const long fma_cycles = rounds * T * T * k * k * 4;
         const long lds_bytes = rounds * wtc::kWaves * (bwd ? 2 : 1) * (T + 2 * R) * window_floats(T, R) * 4 * 64;
         const long cost = std::max(fma_cycles, lds_bytes / 128);
@@ -72,7 +77,7 @@ int pick_tile(int h, int w, int PP, int k, bool bwd)
 
 // Lay out one plane's input array and pyramid for a given number of resident
 // planes. Returns false if a level cannot be tiled within the register caps.
-bool layout(const wtconv_desc& d, int PP, bool bwd, PlaneGeom& g, bool t4_deep = false)
+bool layout(const wtconv_desc& d, int PP, bool bwd, PlaneGeom& g, bool t4_deep = false, bool one_pref = false)
 {
     const int R = d.k / 2;
     memset(&g, 0, sizeof(g));
@@ -91,7 +96,7 @@ bool layout(const wtconv_desc& d, int PP, bool bwd, PlaneGeom& g, bool t4_deep =
         LevelGeom& lg = g.lv[l];
         lg.h = h;
         lg.w = w;
-        lg.T = (t4_deep && l >= 3) ? 4 : pick_tile(h, w, PP, d.k, bwd);
+        lg.T = (t4_deep && l >= 3) ? 4 : pick_tile(h, w, PP, d.k, bwd, one_pref);
         if (lg.T == 0) return false;
         lg.eh = ceil_to(h, lg.T);
         lg.ew = ceil_to(w, lg.T);
@@ -142,6 +147,16 @@ bool single_round(const wtconv_desc& d, int PP, const PlaneGeom& g)
     return true;
 }
 
+// Workgroups (4 wavefronts) per CU that the forward kernel's registers allow:
+// 512 registers per SIMD lane over its VGPR count as compiled for gfx950
+// (single round: 55 / 63-68 / 100-103 / 147-148 for k = 1 / 3 / 5 / 7;
+// general: 123 / 137 / 148-149 / 173). A planning estimate only.
+int forward_wgs_by_regs(int k, bool one)
+{
+    if (one) return k <= 1 ? 8 : (k <= 3 ? 7 : (k <= 5 ? 4 : 3));
+    return k <= 1 ? 4 : (k <= 5 ? 3 : 2);
+}
+
 // Lane use of one workgroup's output-tile rounds with PP resident planes.
 double tile_use(const PlaneGeom& g, int PP)
 {
@@ -167,26 +182,37 @@ bool make_plan(const wtconv_desc& d, bool bwd, Plan& pl)
         }
     }
     if (PP == 0) return false;
-    // Forward: a plane count whose layout runs in the single-round variant
-    // (fewer registers, no round loops), with at least two workgroups per CU
-    // and at least 3/4 of the output-tile lane use, beats a general one.
-    // Measured on MI355X, k = 5 unless noted: 28 x 28 L = 1 54.5 -> 40.6 us,
-    // L = 2 55.5 -> 46.1 us; 56 x 56 L = 1 (B = 128) 153.6 -> 121.1 us; 40 x 40
-    // k = 7 L = 4 155.9 -> 81.4 us; at 14 x 14 L = 3 the general variant's
-    // higher lane use wins (4 single-round planes 118 us, 9 general 98 us).
-    if (!bwd && !single_round(d, PP, pl.g)) {
-        const double use = tile_use(pl.g, PP);
-        for (int pp = want; pp >= 1; --pp) {
-            PlaneGeom g;
-            if (!layout(d, pp, bwd, g) || !single_round(d, pp, g)) continue;
-            const int lds = lds_floats_for(d, bwd, pp, g);
-            if (lds <= kLdsFloatsMax / 2 && tile_use(g, pp) >= 0.75 * use) {
-                PP = pp;
-                pl.g = g;
-                pl.lds_floats = lds;
-                break;
+    // Forward: every plane count up to one round of output tiles (or the
+    // count above), in the default tile layout and in one preferring
+    // single-round tiles, scored by output-tile lane use x workgroups per CU
+    // (registers and LDS), the general kernel variant at 3/4 (its round loops);
+    // more planes on ties. Measured on MI355X (us per forward, k = 5, B64 C192
+    // 28 x 28 unless noted): L = 1 6 planes 54.5 -> 4 single-round 40.6; L = 3
+    // 4 planes 64.7 -> 3 single-round 61.3; L = 4 70.0 -> 62.0; B128 56 x 56
+    // L = 1 2 planes 153.6 -> 1 single-round 121.1; 40 x 40 k = 7 L = 4 155.9 ->
+    // 81.4.
+    bool pref_used = false;
+    if (!bwd) {
+        const long tiles = px / 16;
+        const int ppmax = std::max(PP, (int)std::min<long>(d.B, wtc::kThreads / tiles));
+        double best = -1.0;
+        for (int pp = 1; pp <= ppmax; ++pp)
+            for (int pref = 0; pref < 2; ++pref) {
+                PlaneGeom g;
+                if (!layout(d, pp, bwd, g, false, pref == 1)) continue;
+                const int lds = lds_floats_for(d, bwd, pp, g);
+                if (lds > kLdsFloatsMax) continue;
+                const bool one = single_round(d, pp, g);
+                const int wgs = std::min(forward_wgs_by_regs(d.k, one), kLdsFloatsMax / lds);
+                const double score = tile_use(g, pp) * wgs * (one ? 1.0 : 0.75);
+                if (score >= best) {
+                    best = score;
+                    PP = pp;
+                    pl.g = g;
+                    pl.lds_floats = lds;
+                    pref_used = pref == 1;
+                }
             }
-        }
     }
     pl.PP = PP;
     pl.one_round = single_round(d, PP, pl.g) ? 1 : 0;
@@ -197,7 +223,7 @@ bool make_plan(const wtconv_desc& d, bool bwd, Plan& pl)
     // the 7x7 level 3 of a 56x56 plane cost 5 us of a 73 us forward on its own).
     if (!bwd && pl.one_round && d.L >= 3 && pl.g.lv[1].T == 4) {
         PlaneGeom gm;
-        if (layout(d, PP, bwd, gm, true)) {
+        if (layout(d, PP, bwd, gm, true, pref_used)) {
             long lanes = (long)PP * (gm.lv[1].eh / 4) * (gm.lv[1].ew / 4);
             for (int l = 3; l <= d.L; ++l) lanes += (long)PP * (gm.lv[l].eh / 4) * (gm.lv[l].ew / 4);
             const int lds = lds_floats_for(d, bwd, PP, gm);
