@@ -303,7 +303,7 @@ def load_traffic(path, kernel):
 
 
 # Kernels of the benchmark step, by the symbol prefix rocprofv3 reports.
-STEP_KERNELS = {"forward": "fused_kernel<5, float, false, true, false>", "grad": "grad_kernel<5, float>",
+STEP_KERNELS = {"forward": "fused_kernel<5, float, false, true, false>", "grad": "grad_kernel<5, float, false>",
                 "finalize": "reduce_kernel"}
 
 
