@@ -49,7 +49,8 @@
  *     Results are bitwise reproducible for identical inputs and shapes.
  *   - Supported: B, C, H, W >= 1; k in {1, 3, 5, 7}; 0 <= L <= 8. Planes whose
  *     fused working set fits one compute unit's 160 KB of LDS (float32, k = 5:
- *     forward up to about 120 x 120 pixels, backward up to about 84 x 84) run
+ *     forward up to about 120 x 120 pixels, backward up to about 112 x 112, or
+ *     about 90 x 90 at L = 1) run
  *     in one pass; larger planes use a split with a workspace.
  */
 #ifndef WTCONV_H
@@ -135,7 +136,7 @@ size_t wtconv_backward_workspace_bytes(const wtconv_desc* desc);
  *                      wtconv_backward_workspace_bytes(desc) bytes (16-byte
  *                      aligned); its contents are scratch
  * Outputs must not overlap the inputs, each other or the workspace.
- * For planes above 16 x 16 with L >= 2, dx is the forward pass on dy with
+ * For planes above 16 x 16 with L >= 1, dx is the forward pass on dy with
  * every kernel rotated by 180 degrees (the adjoint of the operator) and the
  * kernel gradients come from a separate correlation pass over x and dy; for
  * other shapes one fused pass per plane produces both.

@@ -527,10 +527,15 @@ bool make_grad_plan(const wtconv_desc& d, GradPlan& gp)
 {
     const long per = (long)(ceil_to(d.H, 4) / 4) * (ceil_to(d.W, 4) / 4);
     if (per > wtc::kThreads) {
-        // one resident plane, its 4x4 blocks in several rounds per thread
-        if (per > (long)kGradMaxRounds * wtc::kThreads || !grad_layout(d, 1, gp)) return false;
+        // One resident plane, its 4x4 blocks in several rounds per thread. At
+        // L = 1 beyond two rounds the region-tiled fused backward is as fast or
+        // faster (measured on MI355X, k = 5, B16 C64: 96 x 96 121 vs 122 us,
+        // 112 x 112 121 vs 155 us; at L = 3 the gradient pass wins: 84 x 84
+        // 183 -> 127, 96 x 96 192 -> 153, 112 x 112 200 -> 189 us).
+        const long rounds = cdiv(per, (long)wtc::kThreads);
+        if (rounds > kGradMaxRounds || (d.L < 2 && rounds > 2) || !grad_layout(d, 1, gp)) return false;
         gp.PP = 1;
-        gp.rounds = (int)cdiv(per, (long)wtc::kThreads);
+        gp.rounds = (int)rounds;
     } else {
         const int maxpp = (int)std::min<long>(d.B, wtc::kThreads / per);
         double best = -1.0;

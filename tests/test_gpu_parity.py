@@ -191,6 +191,8 @@ GRAD = [
     (3, 260, 65, 61, 5, 2, "f32"),  # two block rounds, three planes per workgroup in turn
     (2, 3, 65, 61, 3, 2, "bf16"),
     (1, 2, 70, 66, 7, 1, "f16"),
+    (1, 2, 97, 90, 3, 2, "bf16"),  # three block rounds
+    (1, 3, 112, 112, 5, 3, "f32"),  # four block rounds
 ]
 
 
