@@ -282,8 +282,20 @@ def test_sweep_fwdbwd(shape, L, dtype):
     check_full_size(B, C, H, W, 5, L, dtype, backward=True, n_planes=6, n_channels=2)
 
 
-def test_determinism_bitwise():
-    inp, dev = setup(8, 12, 56, 56, 5, 3, "f32", seed=3)
+# One shape per execution path: the gradient pass (one block per thread), its
+# block rounds, its coarse split, at L = 1, and the fused backward.
+DETERMINISM = [
+    (8, 12, 56, 56, 5, 3),
+    (3, 16, 63, 95, 5, 3),
+    (6, 20, 28, 28, 5, 5),
+    (4, 6, 34, 30, 3, 1),
+    (16, 20, 14, 14, 5, 2),
+]
+
+
+@pytest.mark.parametrize("B,C,H,W,k,L", DETERMINISM)
+def test_determinism_bitwise(B, C, H, W, k, L):
+    inp, dev = setup(B, C, H, W, k, L, "f32", seed=3)
     y1, y2 = dev.forward(), dev.forward()
     assert torch.equal(y1, y2)
     g1, g2 = dev.backward(), dev.backward()
