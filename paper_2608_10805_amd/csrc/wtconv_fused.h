@@ -184,6 +184,13 @@ DEV void fetch_block(const T* __restrict__ src, int H, int W, int y0, int x0, in
                 }
             }
         }
+    } else if (y0 >= 0 && x0 >= 0 && y0 + 4 <= H && x0 + 4 <= W) {
+        // a block inside the plane: element loads, no bounds checks
+        const T* p = src + (long)y0 * W + x0;
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+#pragma unroll
+            for (int c = 0; c < 4; ++c) v[r][c] = to_f32(p[(long)r * W + c]);
     } else {
 #pragma unroll
         for (int r = 0; r < 4; ++r)
@@ -764,6 +771,9 @@ DEV void store_tile(T* __restrict__ plane, int H, int W, int y0, int x0, const f
                 __builtin_memcpy(&packed, h, 8);
                 *reinterpret_cast<uint2*>(row) = packed;
             }
+        } else if (x0 + 4 <= W) {
+#pragma unroll
+            for (int ox = 0; ox < 4; ++ox) row[ox] = from_f32<T>(v[oy][ox]);
         } else {
 #pragma unroll
             for (int ox = 0; ox < 4; ++ox)
