@@ -1,0 +1,127 @@
+"""Host-side logic of bench.py (no GPU): the one-GPU guard, the rocprofv3
+summaries and the traffic lookup that gates `roofline.traffic`."""
+import os
+import sqlite3
+import subprocess
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+sys.path.insert(0, ROOT)
+
+import bench  # noqa: E402
+
+FWD = "void wtc::(anonymous namespace)::fused_kernel<5, float, false, true, false>(wtc::FusedArgs)"
+GRAD = "void wtc::(anonymous namespace)::grad_kernel<5, float, false>(wtc::GradArgs)"
+RED = "wtc::(anonymous namespace)::reduce_kernel(wtc::ReduceArgs)"
+COPY = "__amd_rocclr_copyBuffer"
+
+
+def _trace_db(path, rows):
+    con = sqlite3.connect(path)
+    con.execute("create table kernels (name text, duration integer)")
+    con.executemany("insert into kernels values (?, ?)", rows)
+    con.commit()
+    con.close()
+    return str(path)
+
+
+def _counter_db(path, counter, per_kernel):
+    """per_kernel: {kernel name: [value per dispatch]}; each dispatch's value is
+    split over two rows (as per-XCD rows are) to exercise the summation."""
+    con = sqlite3.connect(path)
+    con.execute("create table counters_collection (kernel_name text, dispatch_id integer, counter_name text, "
+                "value real)")
+    disp = 0
+    for name, values in per_kernel.items():
+        for v in values:
+            disp += 1
+            con.execute("insert into counters_collection values (?, ?, ?, ?)", (name, disp, counter, v / 2))
+            con.execute("insert into counters_collection values (?, ?, ?, ?)", (name, disp, counter, v / 2))
+    con.commit()
+    con.close()
+    return str(path)
+
+
+def _kv(path):
+    rec = {}
+    with open(path) as f:
+        for line in f:
+            if ":" in line and not line.startswith("#"):
+                k, v = line.split(":", 1)
+                rec[k.strip()] = v.strip()
+    return rec
+
+
+def test_more_than_one_gpu_is_refused():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"], capture_output=True,
+                       text=True, timeout=120)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr
+
+
+def test_summarize_trace(tmp_path):
+    db = _trace_db(tmp_path / "t.db", [(FWD, 70000), (FWD, 72000), (GRAD, 90000), (RED, 4000)])
+    out = tmp_path / "trace.txt"
+    bench.summarize_trace(db, str(out), "the command")
+    text = out.read_text()
+    assert "# command: the command" in text
+    assert _kv(out)["kernel_source_sha256"] == bench.kernel_source_hash()
+    fwd_line = [ln for ln in text.splitlines() if ln.startswith("fused_kernel<5, float, false, true, false>")][0]
+    name, calls, total, avg, pct = [f.strip() for f in fwd_line.split("|")]
+    assert (calls, total, avg) == ("2", "142.0", "71.000")
+    assert abs(float(pct) - 100.0 * 142 / 236) < 0.06
+
+
+def test_summarize_traffic_scales_by_the_copy(tmp_path):
+    # the copy reads 256 MiB but FETCH_SIZE shows half of it; WRITE_SIZE all of it
+    kib = 256 * 1024.0
+    fetch = _counter_db(tmp_path / "f.db", "FETCH_SIZE", {FWD: [1000.0, 1000.0], GRAD: [3000.0]})
+    write = _counter_db(tmp_path / "w.db", "WRITE_SIZE", {FWD: [500.0, 500.0], GRAD: [10.0]})
+    cfetch = _counter_db(tmp_path / "cf.db", "FETCH_SIZE", {COPY: [kib / 2]})
+    cwrite = _counter_db(tmp_path / "cw.db", "WRITE_SIZE", {COPY: [kib]})
+    out = tmp_path / "traffic.txt"
+    bench.summarize_traffic(fetch, write, cfetch, cwrite, 256, str(out), "cmd")
+    rec = _kv(out)
+    assert float(rec["fetch_scale"]) == pytest.approx(2.0)
+    assert float(rec["write_scale"]) == pytest.approx(1.0)
+    assert float(rec["forward_hbm_bytes_per_launch"]) == pytest.approx((2 * 1000 + 500) * 1024, rel=1e-9)
+    assert float(rec["grad_hbm_bytes_per_launch"]) == pytest.approx((2 * 3000 + 10) * 1024, rel=1e-9)
+
+
+def test_traffic_lookup_needs_current_sources(tmp_path):
+    kib = 1024.0
+    fetch = _counter_db(tmp_path / "f.db", "FETCH_SIZE", {FWD: [100.0]})
+    write = _counter_db(tmp_path / "w.db", "WRITE_SIZE", {FWD: [100.0]})
+    cfetch = _counter_db(tmp_path / "cf.db", "FETCH_SIZE", {COPY: [kib]})
+    cwrite = _counter_db(tmp_path / "cw.db", "WRITE_SIZE", {COPY: [kib]})
+    out = tmp_path / "traffic.txt"
+    bench.summarize_traffic(fetch, write, cfetch, cwrite, 1, str(out), "cmd")
+    assert bench.load_traffic(str(out), "forward") == pytest.approx(200 * 1024)
+    assert bench.load_traffic(str(out), "grad") is None  # no counters for it
+    stale = out.read_text().replace(bench.kernel_source_hash(), "0" * 64)
+    out.write_text(stale)
+    assert bench.load_traffic(str(out), "forward") is None
+    assert bench.load_traffic(str(tmp_path / "missing.txt"), "forward") is None
+
+
+def test_summarize_counters(tmp_path):
+    per = {n: {FWD: [v], GRAD: [2 * v]} for n, v in zip(bench.SQ_COUNTERS, range(1, 9))}
+    con = sqlite3.connect(tmp_path / "sq.db")
+    con.execute("create table counters_collection (kernel_name text, dispatch_id integer, counter_name text, "
+                "value real)")
+    disp = 0
+    for name, kv in per.items():
+        for kern, vals in kv.items():
+            for v in vals:
+                disp += 1
+                con.execute("insert into counters_collection values (?, ?, ?, ?)", (kern, disp, name, float(v)))
+    con.commit()
+    con.close()
+    out = tmp_path / "sq.txt"
+    bench.summarize_counters(str(tmp_path / "sq.db"), str(out), "cmd")
+    rec = _kv(out)
+    assert float(rec["forward_SQ_INSTS_VALU"]) == per["SQ_INSTS_VALU"][FWD][0]
+    assert float(rec["grad_SQ_INSTS_VALU"]) == per["SQ_INSTS_VALU"][GRAD][0]
+    assert rec["kernel_source_sha256"] == bench.kernel_source_hash()
