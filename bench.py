@@ -200,8 +200,8 @@ def cpu_baseline(inp, work_bytes, seconds):
     log(f"cpu_baseline: float64 oracle fwd+bwd over the whole workload ({planes} planes), {threads} threads")
     reps, t0 = 0, time.perf_counter()
     while True:
-        oracle.forward(inp.x, inp.base_w, inp.base_scale, inp.level_w, inp.level_scale)
-        oracle.backward(inp.x, inp.dy, inp.base_w, inp.base_scale, inp.level_w, inp.level_scale)
+        y_ref = oracle.forward(inp.x, inp.base_w, inp.base_scale, inp.level_w, inp.level_scale)
+        g_ref = oracle.backward(inp.x, inp.dy, inp.base_w, inp.base_scale, inp.level_w, inp.level_scale)
         reps += 1
         el = time.perf_counter() - t0
         if el >= seconds:
@@ -214,13 +214,36 @@ def cpu_baseline(inp, work_bytes, seconds):
     el1 = time.perf_counter() - t1
     oracle.set_num_threads(threads)
     fwd1_s = el1 * WORKLOAD["B"] / nb
-    return {"value": round(work_bytes * reps / el / 1e9, 4), "unit": "GB/s", "cores": threads,
+    refs = {"y": y_ref, "dx": g_ref["dx"], "d_base_w": g_ref["d_base_w"], "d_base_scale": g_ref["d_base_scale"],
+            "d_level_w": g_ref["d_level_w"], "d_level_scale": g_ref["d_level_scale"]}
+    return refs, {"value": round(work_bytes * reps / el / 1e9, 4), "unit": "GB/s", "cores": threads,
             "kind": "oracle", "cpu_model": cpu_model(),
             "sample": f"the full workload ({planes} planes of 56x56, k=5, L=3), forward and backward, "
                       f"{reps} repetitions in {el:.1f} s, float64; {el / reps * 1e3:.1f} ms per step",
             "fwd_1thread_s": round(fwd1_s, 3),
             "fwd_1thread_sample": f"forward of {nb} of {WORKLOAD['B']} images ({nb * WORKLOAD['C']} planes) on one "
                                   f"thread in {el1:.2f} s, scaled to the whole batch"}
+
+
+def full_size_parity(refs, x, dy, bw, bs, lw, ls):
+    """Every output of one forward and one backward of the library on the
+    benchmark's own inputs against the float64 oracle's (the cpu_baseline run):
+    max |got - ref| / max |ref| per tensor, against the fp32 tolerance 1e-5."""
+    import numpy as np
+
+    from paper_2608_10805_amd import binding
+    y = binding.forward(x, bw, bs, lw, ls)
+    dx, dbw, dbs, dlw, dls = binding.backward(x, dy, bw, bs, lw, ls, need_dx=True)
+    got = {"y": [y], "dx": [dx], "d_base_w": [dbw], "d_base_scale": [dbs], "d_level_w": dlw, "d_level_scale": dls}
+    errs = {}
+    for name, ts in got.items():
+        ref = refs[name] if isinstance(refs[name], list) else [refs[name]]
+        g = np.concatenate([t.detach().cpu().double().numpy().ravel() for t in ts])
+        r = np.concatenate([np.asarray(a, dtype=np.float64).ravel() for a in ref])
+        errs[name] = float(np.max(np.abs(g - r)) / max(float(np.max(np.abs(r))), 1e-30))
+    tol = 1e-5
+    return {"vs": "float64 oracle, whole workload", "max_rel_err": {k: float(f"{v:.3g}") for k, v in errs.items()},
+            "tol": tol, "pass": all(v < tol for v in errs.values())}
 
 
 def copy_ceiling_gbps(dev, gib=1):
@@ -557,8 +580,11 @@ def main():
     if not args.no_config_table:
         table = config_table(args.table_steps, dev)
     cpu = None
+    parity = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(inp, work.bytes_fwdbwd, args.cpu_seconds)
+        refs, cpu = cpu_baseline(inp, work.bytes_fwdbwd, args.cpu_seconds)
+        parity = full_size_parity(refs, x0, dy0, bw, bs, lw, ls)
+        log(f"parity vs the float64 oracle (whole workload): {parity}")
     out = {
         "metric": METRIC, "value": round(value, 2), "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(ms_step, 5), "higher_is_better": True, "scaling": "weak",
@@ -582,6 +608,7 @@ def main():
                                                                    if traffic is not None else None)},
         "roofline": roofline,
         "cpu_baseline": cpu,
+        "parity": parity,
         "N": N,
         "configs": table,
         "paper_layer_sweep_geomean": paper_sweep_summary(table) if table else None,
