@@ -460,3 +460,25 @@ def test_large_plane_determinism_bitwise():
     g1, g2 = dev.backward(), dev.backward()
     for a, b in zip([g1[0], g1[1], g1[2]] + g1[3] + g1[4], [g2[0], g2[1], g2[2]] + g2[3] + g2[4]):
         assert torch.equal(a, b)
+
+
+def _random_cases(seed, n):
+    """Seeded random shapes across every execution path: tiny, resident with one
+    or several planes, split, gradient pass (one block per thread or block
+    rounds), fused backward; odd, even and 4-multiple widths; all k, L and
+    storage types."""
+    import random
+    rng = random.Random(seed)
+    sizes = [1, 2, 3, 5, 7, 8, 9, 12, 14, 15, 16, 17, 20, 23, 28, 30, 31, 33, 40, 46, 47, 56, 63, 64, 66, 70, 95, 97]
+    cases = []
+    for _ in range(n):
+        cases.append((rng.choice([1, 2, 3, 5, 7, 9, 16]), rng.choice([1, 2, 3, 4, 8, 64, 130]), rng.choice(sizes),
+                      rng.choice(sizes), rng.choice([1, 3, 5, 7]), rng.choice([0, 1, 2, 3, 4, 5, 6]),
+                      rng.choice(["f32", "f32", "bf16", "f16"])))
+    return cases
+
+
+@pytest.mark.parametrize("B,C,H,W,k,L,dtype", _random_cases(2026, 180))
+def test_random_shapes(B, C, H, W, k, L, dtype):
+    check_forward(B, C, H, W, k, L, dtype)
+    check_backward(B, C, H, W, k, L, dtype)
