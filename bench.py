@@ -181,6 +181,72 @@ def config_table(steps, dev):
     return rows
 
 
+def memory_table(dev):
+    """Peak allocated device memory of the layer (`WTConv2d`) over one training
+    step (forward, then backward from a given dy) and over one inference
+    forward, for the paper's nine layer shapes, L = 1..5, fp32 and fp16.
+
+    Each peak is divided by the compulsory footprint: inference x, y and the
+    parameters; training x, y, dy, dx, the parameters and their gradients,
+    which is about what a plain depthwise convolution of the same shape holds.
+    Reported per dtype and L as the geometric mean and the maximum over the
+    shapes, with the largest workspace (peak minus compulsory) in bytes."""
+    import math
+
+    import torch
+
+    from paper_2608_10805_amd import iomodel
+    from paper_2608_10805_amd.autograd import WTConv2d
+
+    tdt = {"f32": torch.float32, "f16": torch.float16}
+    gen = torch.Generator(device=dev)
+    out = {}
+    for dt in ("f32", "f16"):
+        per_l = []
+        for L in range(1, 6):
+            train, infer, extra = [], [], 0
+            for C in (32, 64, 128):
+                for H in (128, 256, 512):
+                    B, k = 8, 5
+                    gen.manual_seed(0)
+                    layer = WTConv2d(C, kernel_size=k, levels=L, device=dev)
+                    nparam = sum(p.numel() for p in layer.parameters()) * 4
+                    act = B * C * H * H * iomodel.elem_bytes(dt)
+                    x = torch.randn(B, C, H, H, generator=gen, device=dev).to(tdt[dt])
+                    dy = torch.randn(B, C, H, H, generator=gen, device=dev).to(tdt[dt])
+                    torch.cuda.synchronize()
+                    base = torch.cuda.memory_allocated(dev) - 2 * act - nparam
+                    torch.cuda.reset_peak_memory_stats(dev)
+                    with torch.no_grad():
+                        y = layer(x)
+                    torch.cuda.synchronize()
+                    peak_inf = torch.cuda.max_memory_allocated(dev) - base - act  # dy is not part of inference
+                    comp_inf = 2 * act + nparam
+                    del y
+                    x.requires_grad_(True)
+                    torch.cuda.synchronize()
+                    torch.cuda.reset_peak_memory_stats(dev)
+                    y = layer(x)
+                    y.backward(dy)
+                    torch.cuda.synchronize()
+                    peak_tr = torch.cuda.max_memory_allocated(dev) - base
+                    comp_tr = 4 * act + 2 * nparam
+                    infer.append(peak_inf / comp_inf)
+                    train.append(peak_tr / comp_tr)
+                    extra = max(extra, peak_tr - comp_tr, peak_inf - comp_inf)
+                    del x, dy, y, layer
+                    torch.cuda.empty_cache()
+            gm = lambda v: math.exp(sum(math.log(t) for t in v) / len(v))  # noqa: E731
+            per_l.append({"L": L, "train_peak_over_compulsory": round(gm(train), 4),
+                          "train_max": round(max(train), 4),
+                          "infer_peak_over_compulsory": round(gm(infer), 4), "infer_max": round(max(infer), 4),
+                          "max_extra_bytes": int(extra)})
+            log(f"memory: {dt} L{L} train {gm(train):.4f} (max {max(train):.4f})  "
+                f"infer {gm(infer):.4f} (max {max(infer):.4f})  extra {extra / 2 ** 20:.1f} MiB")
+        out[dt] = per_l
+    return out
+
+
 def cpu_model():
     try:
         with open("/proc/cpuinfo") as f:
@@ -577,8 +643,10 @@ def main():
                              "achieved_GBps": round(dom_bytes / (dom_ms * 1e-3) / 1e9, 1),
                              "frac": round(dom_bytes / (dom_ms * 1e-3) / 1e9 / iomodel.HBM_PEAK_GBPS, 4)}}
     table = None
+    memory = None
     if not args.no_config_table:
         table = config_table(args.table_steps, dev)
+        memory = memory_table(dev)
     cpu = None
     parity = None
     if not args.no_cpu_baseline:
@@ -612,6 +680,7 @@ def main():
         "N": N,
         "configs": table,
         "paper_layer_sweep_geomean": paper_sweep_summary(table) if table else None,
+        "paper_layer_sweep_peak_memory": memory,
     }
     print(json.dumps(out), flush=True)
 
