@@ -61,6 +61,10 @@ def parse():
     ap.add_argument("--summarize-traffic", nargs=4, metavar=("FETCH_DB", "WRITE_DB", "COPY_FETCH_DB", "COPY_WRITE_DB"),
                     help="write per-launch HBM bytes from rocprofv3 FETCH_SIZE / WRITE_SIZE databases of this "
                          "benchmark and of --copy-calibration-mib runs to --out and exit")
+    ap.add_argument("--traffic-invariance-run", action="store_true",
+                    help="run one forward of each traffic-invariance configuration and exit (for rocprofv3 --pmc)")
+    ap.add_argument("--summarize-invariance", nargs=4, metavar=("FETCH_DB", "WRITE_DB", "COPY_FETCH_DB", "COPY_WRITE_DB"),
+                    help="write the HBM traffic of each --traffic-invariance-run forward, in units of N, to --out and exit")
     ap.add_argument("--copy-mib", type=int, default=256, help="size of the calibration copy behind --summarize-traffic")
     ap.add_argument("--command", default="", help="the profiling command, recorded in the summary")
     ap.add_argument("--out", help="summary file for --summarize-trace / --summarize-traffic")
@@ -82,37 +86,46 @@ def table_configs():
     # the paper's own layer sweep: B=8, C in {32, 64, 128}, H=W in {128, 256, 512},
     # L = 1..5, fp32 and fp16, k = 5 (its latency tables report the geometric
     # mean over the nine shapes)
-    for dt in ("f32", "f16"):
-        for L in range(1, 6):
-            for C in (32, 64, 128):
-                for H in (128, 256, 512):
-                    out.append((f"paper_{H}x{H}_c{C}_L{L}_{dt}", 8, C, H, H, 5, L, dt))
+    for k in (5, 3):
+        for dt in ("f32", "f16"):
+            for L in range(1, 6):
+                for C in (32, 64, 128):
+                    for H in (128, 256, 512):
+                        out.append((f"paper_k{k}_{H}x{H}_c{C}_L{L}_{dt}", 8, C, H, H, k, L, dt))
     return out
 
 
 # The paper's fused-kernel latencies on its RTX A6000 (geometric mean over its
-# nine layer shapes, k = 5, L = 1..5), for context next to the MI355X figures.
+# nine layer shapes, L = 1..5; absolute-latency tables for k = 5 and k = 3), for
+# context next to the MI355X figures.
 PAPER_A6000_MS = {
-    "f32": {"fwd": [2.312, 2.552, 2.634, 2.681, 2.703], "fwdbwd": [7.800, 8.693, 8.995, 9.154, 9.277]},
-    "f16": {"fwd": [1.389, 1.592, 1.668, 1.710, 1.748], "fwdbwd": [5.365, 6.148, 6.442, 6.600, 6.733]},
+    5: {"f32": {"fwd": [2.312, 2.552, 2.634, 2.681, 2.703], "fwdbwd": [7.800, 8.693, 8.995, 9.154, 9.277]},
+        "f16": {"fwd": [1.389, 1.592, 1.668, 1.710, 1.748], "fwdbwd": [5.365, 6.148, 6.442, 6.600, 6.733]}},
+    3: {"f32": {"fwd": [1.667, 1.880, 1.945, 1.979, 2.001], "fwdbwd": [6.081, 6.891, 7.135, 7.248, 7.332]},
+        "f16": {"fwd": [1.029, 1.155, 1.205, 1.234, 1.258], "fwdbwd": [3.908, 4.470, 4.665, 4.773, 4.870]}},
 }
 
 
 def paper_sweep_summary(rows):
-    """Geometric means over the paper's nine layer shapes, per dtype and L."""
+    """Geometric means over the paper's nine layer shapes, per kernel size,
+    dtype and L: {"k5": {"f32": [...], "f16": [...]}, "k3": {...}}."""
     import math
     out = {}
-    for dt in ("f32", "f16"):
-        per_l = []
-        for L in range(1, 6):
-            sel = [r for r in rows if r["name"].startswith("paper_") and r["dtype"] == dt and r["L"] == L]
-            if len(sel) != 9:
-                continue
-            g = lambda key: math.exp(sum(math.log(r[key]) for r in sel) / len(sel))  # noqa: E731
-            per_l.append({"L": L, "fwd_ms": round(g("fwd_ms"), 4), "fwdbwd_ms": round(g("fwdbwd_ms"), 4),
-                          "paper_a6000_fwd_ms": PAPER_A6000_MS[dt]["fwd"][L - 1],
-                          "paper_a6000_fwdbwd_ms": PAPER_A6000_MS[dt]["fwdbwd"][L - 1]})
-        out[dt] = per_l
+    for k in (5, 3):
+        per_dt = {}
+        for dt in ("f32", "f16"):
+            per_l = []
+            for L in range(1, 6):
+                sel = [r for r in rows if r["name"].startswith("paper_") and r["k"] == k and r["dtype"] == dt
+                       and r["L"] == L]
+                if len(sel) != 9:
+                    continue
+                g = lambda key: math.exp(sum(math.log(r[key]) for r in sel) / len(sel))  # noqa: E731
+                per_l.append({"L": L, "fwd_ms": round(g("fwd_ms"), 4), "fwdbwd_ms": round(g("fwdbwd_ms"), 4),
+                              "paper_a6000_fwd_ms": PAPER_A6000_MS[k][dt]["fwd"][L - 1],
+                              "paper_a6000_fwdbwd_ms": PAPER_A6000_MS[k][dt]["fwdbwd"][L - 1]})
+            per_dt[dt] = per_l
+        out[f"k{k}"] = per_dt
     return out
 
 
@@ -470,6 +483,85 @@ def summarize_traffic(fetch_db, write_db, cfetch_db, cwrite_db, copy_mib, out, c
         f.write("\n".join(lines) + "\n")
 
 
+# HBM traffic at L = 3, fp32, across tensor shapes (k = 5) and kernel sizes
+# (C = 64, H = W = 256), B = 8: the paper's traffic-invariance measurement
+# (appendix on traffic), whose fused design moves a predicted 8.25N elements.
+INVARIANCE_CONFIGS = [(8, 32, 512, 512, 5, 3), (8, 64, 256, 256, 5, 3), (8, 128, 128, 128, 5, 3),
+                      (8, 64, 256, 256, 3, 3), (8, 64, 256, 256, 7, 3)]
+
+
+def traffic_invariance_run(dev):
+    """One forward per configuration, each after its own input allocation, so
+    that the library's dispatches of one configuration form one contiguous run
+    between torch's own kernels."""
+    import torch
+
+    from paper_2608_10805_amd import binding
+
+    gen = torch.Generator(device=dev)
+    for B, C, H, W, k, L in INVARIANCE_CONFIGS:
+        gen.manual_seed(0)
+        f32 = dict(device=dev, dtype=torch.float32)
+        bw = torch.rand(C, k, k, generator=gen, **f32) * 0.4 - 0.2
+        bs = torch.rand(C, generator=gen, **f32) + 0.5
+        lw = [torch.rand(4 * C, k, k, generator=gen, **f32) * 0.4 - 0.2 for _ in range(L)]
+        ls = [torch.rand(4 * C, generator=gen, **f32) * 0.15 + 0.05 for _ in range(L)]
+        x = torch.randn(B, C, H, W, generator=gen, **f32)
+        y = torch.empty_like(x)
+        nbytes = binding.wtconv_forward_workspace_bytes(binding.make_desc(B, C, H, W, k, L, binding._dtype_code(x)))
+        ws = torch.empty(max(1, nbytes), dtype=torch.uint8, device=dev)
+        torch.cuda.synchronize()
+        binding.forward(x, bw, bs, lw, ls, out=y, workspace=ws)
+        torch.cuda.synchronize()
+        log(f"invariance: forward B={B} C={C} H=W={H} k={k} L={L} done")
+        del x, y, ws
+        torch.cuda.empty_cache()
+
+
+def _library_dispatch_groups(db, counter):
+    """Per-dispatch totals of `counter` for the library's kernels, grouped into
+    runs of consecutive library dispatches (any other kernel ends a run)."""
+    rows = _rocpd_rows(db, f"select kernel_name, dispatch_id, sum(value) from counters_collection where "
+                           f"counter_name = '{counter}' group by kernel_name, dispatch_id order by dispatch_id")
+    groups, cur = [], None
+    for name, _, v in rows:
+        if "wtc::" in name:
+            if cur is None:
+                cur = []
+                groups.append(cur)
+            cur.append(v)
+        else:
+            cur = None
+    return groups
+
+
+def summarize_invariance(fetch_db, write_db, cfetch_db, cwrite_db, copy_mib, out, command):
+    """HBM traffic of each forward of --traffic-invariance-run, all of the
+    library's kernels of that forward summed, in units of N fp32 elements."""
+    copy_kib = copy_mib * 1024.0
+    cf = max((v for k, v in _counter_per_kernel(cfetch_db, "FETCH_SIZE").items() if "copyBuffer" in k), default=0)
+    cw = max((v for k, v in _counter_per_kernel(cwrite_db, "WRITE_SIZE").items() if "copyBuffer" in k), default=0)
+    fscale, wscale = copy_kib / cf, copy_kib / cw
+    fg = _library_dispatch_groups(fetch_db, "FETCH_SIZE")
+    wg = _library_dispatch_groups(write_db, "WRITE_SIZE")
+    if len(fg) != len(INVARIANCE_CONFIGS) or len(wg) != len(INVARIANCE_CONFIGS):
+        raise SystemExit(f"expected {len(INVARIANCE_CONFIGS)} forwards, found {len(fg)} / {len(wg)}")
+    lines = ["# HBM traffic of one forward at L = 3, fp32, across tensor shapes and kernel sizes (rocprofv3 counters)",
+             f"# commands (one counter per run): {command}",
+             f"# calibration: a {copy_mib} MiB device copy reads and writes {copy_kib:.0f} KiB; FETCH_SIZE reports "
+             f"{cf:.0f} KiB (scale x{fscale:.3f}), WRITE_SIZE reports {cw:.0f} KiB (scale x{wscale:.3f})",
+             "# the paper's fused design: 8.25N predicted; its measurements 8.17N-8.60N",
+             f"kernel_source_sha256: {kernel_source_hash()}",
+             "# B C H W k L | launches | fetch_N | write_N | total_N"]
+    for (B, C, H, W, k, L), f, w in zip(INVARIANCE_CONFIGS, fg, wg):
+        n_bytes = 4.0 * B * C * H * W
+        fn = sum(f) * 1024 * fscale / n_bytes
+        wn = sum(w) * 1024 * wscale / n_bytes
+        lines.append(f"{B} {C} {H} {W} {k} {L} | {len(f)} | {fn:.3f} | {wn:.3f} | {fn + wn:.3f}")
+    with open(out, "w") as fh:
+        fh.write("\n".join(lines) + "\n")
+
+
 SQ_COUNTERS = ("SQ_WAVES", "SQ_INSTS_VALU", "SQ_INSTS_LDS", "SQ_INSTS_SALU", "SQ_WAVE_CYCLES", "SQ_BUSY_CYCLES",
                "SQ_ACTIVE_INST_VALU", "SQ_WAIT_INST_LDS")
 
@@ -522,6 +614,9 @@ def main():
     if args.summarize_traffic:
         summarize_traffic(*args.summarize_traffic, args.copy_mib, args.out, args.command)
         return
+    if args.summarize_invariance:
+        summarize_invariance(*args.summarize_invariance, args.copy_mib, args.out, args.command)
+        return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}, WORLD_SIZE {world}); this operator's "
@@ -545,6 +640,9 @@ def main():
             b.copy_(a)
         torch.cuda.synchronize()
         log(f"copy calibration: 3 copies of {args.copy_calibration_mib} MiB")
+        return
+    if args.traffic_invariance_run:
+        traffic_invariance_run(dev)
         return
     B, C, H, W, k, L = (WORKLOAD[n] for n in ("B", "C", "H", "W", "k", "L"))
     log(f"bench: {WORKLOAD['workload']} B={B} C={C} H={H} W={W} k={k} L={L} f32, steps={args.steps} "

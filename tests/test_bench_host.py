@@ -125,3 +125,73 @@ def test_summarize_counters(tmp_path):
     assert float(rec["forward_SQ_INSTS_VALU"]) == per["SQ_INSTS_VALU"][FWD][0]
     assert float(rec["grad_SQ_INSTS_VALU"]) == per["SQ_INSTS_VALU"][GRAD][0]
     assert rec["kernel_source_sha256"] == bench.kernel_source_hash()
+
+
+def test_summarize_invariance_groups_each_forward(tmp_path):
+    """Library dispatches between torch kernels form one forward each; the
+    summary divides their scaled bytes by 4N."""
+    kib = 64 * 1024.0
+    n_cfg = len(bench.INVARIANCE_CONFIGS)
+
+    def db(path, counter, per_forward):
+        con = sqlite3.connect(path)
+        con.execute("create table counters_collection (kernel_name text, dispatch_id integer, counter_name text, "
+                    "value real)")
+        disp = 0
+        for f in range(n_cfg):
+            disp += 1
+            con.execute("insert into counters_collection values (?, ?, ?, ?)", ("at::randn_kernel", disp, counter, 5.0))
+            for v in per_forward[f]:
+                disp += 1
+                con.execute("insert into counters_collection values (?, ?, ?, ?)", (FWD, disp, counter, v))
+        con.commit()
+        con.close()
+        return str(path)
+
+    # forward f: two library launches (e.g. carrier + fused pass)
+    fetch = db(tmp_path / "f.db", "FETCH_SIZE", [[100.0 * (f + 1), 50.0] for f in range(n_cfg)])
+    write = db(tmp_path / "w.db", "WRITE_SIZE", [[10.0, 20.0 * (f + 1)] for f in range(n_cfg)])
+    cfetch = _counter_db(tmp_path / "cf.db", "FETCH_SIZE", {COPY: [kib / 2]})
+    cwrite = _counter_db(tmp_path / "cw.db", "WRITE_SIZE", {COPY: [kib]})
+    out = tmp_path / "inv.txt"
+    bench.summarize_invariance(fetch, write, cfetch, cwrite, 64, str(out), "cmd")
+    rows = [ln for ln in out.read_text().splitlines() if ln and not ln.startswith("#") and "|" in ln]
+    assert len(rows) == n_cfg
+    for f, (row, cfg) in enumerate(zip(rows, bench.INVARIANCE_CONFIGS)):
+        B, C, H, W, k, L = cfg
+        fields = [x.strip() for x in row.split("|")]
+        assert fields[0].split() == [str(v) for v in cfg]
+        assert fields[1] == "2"
+        n_bytes = 4.0 * B * C * H * W
+        want_f = 2 * (100.0 * (f + 1) + 50.0) * 1024 / n_bytes
+        want_w = (10.0 + 20.0 * (f + 1)) * 1024 / n_bytes
+        assert float(fields[2]) == pytest.approx(want_f, abs=6e-4)
+        assert float(fields[3]) == pytest.approx(want_w, abs=6e-4)
+
+
+def test_summarize_invariance_rejects_a_missing_forward(tmp_path):
+    con = sqlite3.connect(tmp_path / "f.db")
+    con.execute("create table counters_collection (kernel_name text, dispatch_id integer, counter_name text, "
+                "value real)")
+    con.execute("insert into counters_collection values (?, ?, ?, ?)", (FWD, 1, "FETCH_SIZE", 1.0))
+    con.commit()
+    con.close()
+    cf = _counter_db(tmp_path / "cf.db", "FETCH_SIZE", {COPY: [1.0]})
+    cw = _counter_db(tmp_path / "cw.db", "WRITE_SIZE", {COPY: [1.0]})
+    with pytest.raises(SystemExit):
+        bench.summarize_invariance(str(tmp_path / "f.db"), str(tmp_path / "f.db"), cf, cw, 1,
+                                   str(tmp_path / "o.txt"), "cmd")
+
+
+def test_paper_sweep_summary_geomeans():
+    rows = []
+    for name, B, C, H, W, k, L, dt in bench.table_configs():
+        if name.startswith("paper_"):
+            rows.append({"name": name, "k": k, "dtype": dt, "L": L, "fwd_ms": float(C) / 32 * (H / 128),
+                         "fwdbwd_ms": 2.0})
+    s = bench.paper_sweep_summary(rows)
+    # geometric mean of (C/32) * (H/128) over C in {32,64,128}, H in {128,256,512} = 2 * 2
+    assert s["k3"]["f32"][0]["fwd_ms"] == pytest.approx(4.0)
+    assert s["k5"]["f16"][4]["fwdbwd_ms"] == pytest.approx(2.0)
+    assert s["k3"]["f16"][2]["paper_a6000_fwd_ms"] == 1.205
+    assert len(s["k5"]["f32"]) == 5
