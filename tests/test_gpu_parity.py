@@ -453,6 +453,15 @@ def test_paper_layer_sweep_full(C, H, L, dtype):
     check_full_size(8, C, H, H, 5, L, dtype, backward=True, n_planes=4, n_channels=2)
 
 
+@pytest.mark.parametrize("C,H,k,L,dtype", [(64, 256, 3, 3, "f32"), (32, 512, 3, 5, "f16"), (64, 256, 7, 3, "f32"),
+                                           (128, 128, 7, 4, "bf16"), (32, 512, 7, 2, "f32"),
+                                           (128, 128, 3, 1, "f16")])
+def test_paper_layer_sweep_other_k_full(C, H, k, L, dtype):
+    """The paper's sweep shapes at k = 3 (its k = 3 table) and k = 7 (its
+    traffic-invariance configurations), B = 8, forward and backward."""
+    check_full_size(8, C, H, H, k, L, dtype, backward=True, n_planes=4, n_channels=2)
+
+
 def test_large_plane_determinism_bitwise():
     inp, dev = setup(2, 3, 150, 150, 5, 3, "f32", seed=5)
     y1, y2 = dev.forward(), dev.forward()
