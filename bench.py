@@ -169,7 +169,14 @@ def config_table(steps, dev):
 
         res = {}
         for with_bwd in (False, True):
-            run(3, with_bwd)
+            # untimed runs for at least 20 ms first: the GPU clock settles over
+            # tens of ms, and a short configuration is otherwise timed cold
+            t0 = time.perf_counter()
+            while True:
+                run(3, with_bwd)
+                torch.cuda.synchronize()
+                if time.perf_counter() - t0 >= 0.02:
+                    break
             a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             torch.cuda.synchronize()
             a.record()
