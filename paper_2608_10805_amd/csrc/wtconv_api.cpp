@@ -414,11 +414,20 @@ int tiny_level(const wtconv_desc& d)
 // pays when the fused pass loses at least two deep levels (one when those
 // start at level 2, where the fused pass is least efficient), or in the
 // backward pass when it brings the workgroup's LDS under the two-per-CU mark.
+// The tiny kernel runs one lane per plane, so with few planes it cannot fill
+// the chip: a forward that would shed only two levels above m = 1 stays whole
+// below B * C = 32768 (B * C / 64 = 512 wavefronts). Measured forwards, k = 5,
+// fp32, split -> whole: 16 x 16 L = 3 at B64 C192 37.7 -> 29.3 us, 12 x 12
+// L = 3 at B128 C192 44.7 -> 37.9 us, 14 x 14 L = 3 at B64 C384 52.8 -> 51.7
+// us; at B128 C384 the split wins (79.9 against 91.3 us). Three or more shed
+// levels still pay at any size (14 x 14 L = 5 at B64 C384: 55 against 78 us).
+constexpr long kSplitMinPlanes = 32768;
+
 bool want_split(const wtconv_desc& d, bool bwd, int m, int full_lds, int split_lds)
 {
     if (m < 1 || m > 6 || d.L <= m) return false;
     const int deep = d.L - m;
-    if (!bwd) return deep >= (m == 1 ? 2 : 3);
+    if (!bwd) return deep >= (m == 1 ? 2 : 3) && (m > 1 || deep >= 3 || (long)d.B * d.C >= kSplitMinPlanes);
     const int two_per_cu = kLdsFloatsMax / 2;
     return m == 1 || deep >= 2 || (full_lds > two_per_cu && split_lds <= two_per_cu);
 }

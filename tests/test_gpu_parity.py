@@ -379,6 +379,7 @@ def test_tiny_plane_backward_without_dx():
 # passes, every kernel size, B above 64, 16-bit storage.
 SPLIT = [
     (2, 3, 14, 14, 5, 3, "f32"),
+    (2, 3, 14, 14, 5, 4, "f32"),
     (3, 2, 28, 28, 5, 4, "f32"),
     (2, 2, 20, 12, 3, 4, "f32"),
     (2, 2, 56, 56, 5, 5, "f32"),
@@ -403,6 +404,14 @@ def test_split_backward(B, C, H, W, k, L, dtype):
 
 def test_split_backward_without_dx():
     check_backward(3, 2, 28, 28, 5, 4, "f32", need_dx=False)
+
+
+@pytest.mark.parametrize("B,C,H,k,L,dtype", [(64, 192, 16, 5, 3, "f32"), (128, 192, 12, 5, 3, "bf16"),
+                                             (128, 384, 14, 5, 3, "f16")])
+def test_split_rule_shapes_full(B, C, H, k, L, dtype):
+    """Forwards at the sizes where the split rule's plane-count threshold
+    decides (too few planes to fill the chip: whole; B128 C384: split)."""
+    check_full_size(B, C, H, H, k, L, dtype, backward=True, n_planes=6, n_channels=2)
 
 
 # Planes whose working set does not fit one compute unit's LDS take the split
