@@ -99,6 +99,17 @@ def test_forward_workspace_query():
     assert binding.wtconv_forward_workspace_bytes(make_desc(16, 64, 224, 224, 5, 0)) == 0
 
 
+def test_forward_split_needs_planes_to_fill_the_chip():
+    # 14 x 14 at L = 3 sheds two levels above the 7 x 7 level-1 grid: the tiny
+    # sub-problem (one lane per plane) runs only with at least 32768 planes,
+    # and then the carrier and the coarse output take workspace
+    assert binding.wtconv_forward_workspace_bytes(make_desc(128, 384, 14, 14, 5, 3)) > 0
+    assert binding.wtconv_forward_workspace_bytes(make_desc(64, 384, 14, 14, 5, 3)) == 0
+    assert binding.wtconv_forward_workspace_bytes(make_desc(64, 192, 16, 16, 5, 3)) == 0
+    # three shed levels still split at any size
+    assert binding.wtconv_forward_workspace_bytes(make_desc(2, 3, 14, 14, 5, 4)) > 0
+
+
 def test_forward_large_plane_workspace_checks():
     d = make_desc(1, 1, 512, 512, 5, 3)
     need = binding.wtconv_forward_workspace_bytes(d)
