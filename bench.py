@@ -1,23 +1,23 @@
 #!/usr/bin/env python3
 """Benchmark of the fused WTConv forward + backward on one MI355X.
 
-Workload: ConvNeXt-T stage-1 layer shape, B=64, C=96, H=W=56, k=5, L=3,
-float32, seeded synthetic inputs (see paper_2608_10805_amd/inputs.py). One
-step is the whole operator, forward and backward, as the library's entry
-points run it for this shape: wtconv_forward (y), wtconv_backward_partials
-without dx (the kernel-gradient pass), wtconv_backward_data (dx: the forward
-pass on dy with rotated kernels) and wtconv_backward_finalize (fixed-order
-reduction and unfold) -- exactly the kernels wtconv_backward launches here,
-each bracketed by its own HIP events. Inputs are resident in HBM before timing
-starts; steps rotate over several distinct buffer sets so that the 256 MB
-Infinity Cache cannot hold one step's tensors for the next.
+Headline workload: ConvNeXt-T stage-1 layer shape, B=64, C=96, H=W=56, k=5,
+L=3, float32, seeded synthetic inputs (see paper_2608_10805_amd/inputs.py).
+One step is the whole operator, forward and backward: wtconv_forward (y),
+then wtconv_backward_partials with dx and wtconv_backward_finalize (together
+exactly wtconv_backward). Inputs are resident in HBM before timing starts;
+steps rotate over several distinct buffer sets so that the 256 MB Infinity
+Cache cannot hold one step's tensors for the next.
 
-Prints one JSON line. `value` is achieved GB/s: the single-pass algorithmic
-bytes (x, y, dy, dx, each read or written once; parameters and gradients)
-divided by the measured step time. `roofline` describes the dominant kernel (the one
-with the largest share of the step), timed with HIP events on the stream it
-runs on; `kernels` lists every kernel of the step the same way. `cpu_baseline` times the
-float64 CPU oracle on the host cores.
+The last line on stdout is one compact JSON object (a few KB): `value` is
+achieved GB/s, the single-pass algorithmic bytes (x, y, dy, dx, each read or
+written once; parameters and gradients) divided by the measured step time;
+`roofline` describes the dominant kernel, timed with HIP events on the stream
+it runs on, against both the HBM and the fp32 FMA ceilings; `cpu_baseline`
+times the float64 CPU oracle on the host cores; `parity` compares every
+output over the whole workload with that oracle; `configs_summary` holds the
+fwd / fwd+bwd times of every benchmarked configuration. Per-configuration
+rows go to stderr as they are measured (and to --table-out as JSON).
 """
 import argparse
 import json
@@ -30,45 +30,80 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 METRIC = "fused WTConv fwd+bwd ms and achieved HBM GB/s (% of peak), ConvNeXt-T shapes"
-WORKLOAD = {"workload": "wtconv_fwdbwd_convnext_t_stage1", "B": 64, "C": 96, "H": 56, "W": 56, "k": 5, "L": 3,
-            "dtype": "f32", "pass": "fwd+bwd"}
+
+# Workloads one step can be run on: (B, C, H, W, k, L, dtype). The first is
+# the headline; the others exercise the other execution paths for profiling
+# (--workload): the bf16 stage-1 layer at L = 5, the stage-3 planes whose
+# coarse levels run as a tiny sub-problem, the odd 63 x 95 planes with block
+# rounds, and 224 x 224 planes that take the region decomposition.
+WORKLOADS = {
+    "wtconv_fwdbwd_convnext_t_stage1": (64, 96, 56, 56, 5, 3, "f32"),
+    "wtconv_fwdbwd_convnext_t_stage1_bf16_L5": (128, 96, 56, 56, 5, 5, "bf16"),
+    "wtconv_fwdbwd_convnext_t_stage3_L3": (128, 384, 14, 14, 5, 3, "f32"),
+    "wtconv_fwdbwd_odd_63x95_L5": (32, 128, 63, 95, 5, 5, "f32"),
+    "wtconv_fwdbwd_region_224_L3": (16, 64, 224, 224, 5, 3, "f32"),
+}
+HEADLINE = "wtconv_fwdbwd_convnext_t_stage1"
+
+# The untimed warm-up lasts at least this long whatever --warmup says: the
+# GPU clock settles over tens of milliseconds.
+MIN_WARMUP_S = 0.3
 
 
 def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
 
-def parse():
+def workload_config(name):
+    B, C, H, W, k, L, dt = WORKLOADS[name]
+    return {"workload": name, "B": B, "C": C, "H": H, "W": W, "k": k, "L": L, "dtype": dt, "pass": "fwd+bwd"}
+
+
+def parse(argv=None):
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=200,
-                    help="untimed steps before the timed region (the GPU clock settles over tens of ms)")
+                    help=f"untimed steps before the timed region (run for at least {MIN_WARMUP_S} s in any case)")
+    ap.add_argument("--workload", default=HEADLINE, choices=sorted(WORKLOADS))
     ap.add_argument("--sets", type=int, default=4, help="distinct input/output buffer sets rotated over")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="target duration of the oracle timing")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-config-table", action="store_true",
+                    help="skip the per-configuration fwd / fwd+bwd timing table and the memory table")
+    ap.add_argument("--table-steps", type=int, default=10)
+    ap.add_argument("--table-out", help="write every configuration row (JSON) to this file")
+    ap.add_argument("--profile-run", action="store_true",
+                    help="run exactly --warmup + --steps plain steps of --workload and exit (for rocprofv3)")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="only run a plain device-to-device copy of this many MiB (profiler counter calibration)")
-    ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "hbm_traffic_wtconv_convnext_t_stage1.txt"),
-                    help="counter summary with the measured HBM bytes of the dominant kernel")
-    ap.add_argument("--no-config-table", action="store_true",
-                    help="skip the per-configuration fwd / fwd+bwd timing table")
-    ap.add_argument("--table-steps", type=int, default=10)
     ap.add_argument("--summarize-trace", metavar="DB",
                     help="write the kernel statistics of a rocprofv3 --kernel-trace database to --out and exit")
     ap.add_argument("--summarize-counters", metavar="DB",
                     help="write the SQ instruction counters of a rocprofv3 --pmc database to --out and exit")
     ap.add_argument("--summarize-traffic", nargs=4, metavar=("FETCH_DB", "WRITE_DB", "COPY_FETCH_DB", "COPY_WRITE_DB"),
-                    help="write per-launch HBM bytes from rocprofv3 FETCH_SIZE / WRITE_SIZE databases of this "
-                         "benchmark and of --copy-calibration-mib runs to --out and exit")
+                    help="write per-launch and per-step HBM bytes from rocprofv3 FETCH_SIZE / WRITE_SIZE databases "
+                         "of a --profile-run and of --copy-calibration-mib runs to --out and exit")
+    ap.add_argument("--profiled-steps", type=int, default=0,
+                    help="steps the summarized --profile-run executed (warmup + steps)")
     ap.add_argument("--traffic-invariance-run", action="store_true",
                     help="run one forward of each traffic-invariance configuration and exit (for rocprofv3 --pmc)")
     ap.add_argument("--summarize-invariance", nargs=4, metavar=("FETCH_DB", "WRITE_DB", "COPY_FETCH_DB", "COPY_WRITE_DB"),
                     help="write the HBM traffic of each --traffic-invariance-run forward, in units of N, to --out and exit")
-    ap.add_argument("--copy-mib", type=int, default=256, help="size of the calibration copy behind --summarize-traffic")
+    ap.add_argument("--copy-mib", type=int, default=256, help="size of the calibration copy behind the summaries")
     ap.add_argument("--command", default="", help="the profiling command, recorded in the summary")
-    ap.add_argument("--out", help="summary file for --summarize-trace / --summarize-traffic")
-    return ap.parse_args()
+    ap.add_argument("--out", help="summary file for the --summarize-* modes")
+    return ap.parse_args(argv)
+
+
+# ----------------------------------------------------------------------------
+# configurations
+# ----------------------------------------------------------------------------
+
+# The ConvNeXt-T stage shapes and the two extra shapes of the operator's shape
+# sweep (B, C, H, W), timed at L = 1..5 in fp32 and bf16.
+SWEEP_SHAPES = [(128, 96, 56, 56), (128, 192, 28, 28), (128, 384, 14, 14), (128, 768, 7, 7),
+                (32, 128, 63, 95), (16, 64, 224, 224)]
 
 
 # Every benchmarked configuration of the operator (fwd and fwd+bwd timed for each):
@@ -78,14 +113,13 @@ def table_configs():
            ("convnext_s1", 64, 96, 56, 56, 5, 3, "f32")]
     out += [(f"convnext_s2_L{L}", 64, 192, 28, 28, 5, L, "f32") for L in range(1, 6)]
     out += [("convnext_s1_bf16_L5", 128, 96, 56, 56, 5, 5, "bf16")]
-    for (B, C, H, W) in [(128, 96, 56, 56), (128, 192, 28, 28), (128, 384, 14, 14), (128, 768, 7, 7),
-                         (32, 128, 63, 95), (16, 64, 224, 224)]:
+    for (B, C, H, W) in SWEEP_SHAPES:
         for dt in ("f32", "bf16"):
-            for L in (1, 3, 5):
+            for L in range(1, 6):
                 out.append((f"sweep_{H}x{W}_c{C}_L{L}_{dt}", B, C, H, W, 5, L, dt))
     # the paper's own layer sweep: B=8, C in {32, 64, 128}, H=W in {128, 256, 512},
-    # L = 1..5, fp32 and fp16, k = 5 (its latency tables report the geometric
-    # mean over the nine shapes)
+    # L = 1..5, fp32 and fp16, k = 5 and 3 (its latency tables report the
+    # geometric mean over the nine shapes)
     for k in (5, 3):
         for dt in ("f32", "f16"):
             for L in range(1, 6):
@@ -129,7 +163,60 @@ def paper_sweep_summary(rows):
     return out
 
 
-def config_table(steps, dev):
+def configs_summary(rows, memory=None):
+    """Compact view of the table for the headline line: fwd and fwd+bwd ("fb")
+    times of every configuration of the operator's own workloads (the shape
+    sweep in whole microseconds, keyed "HxWcC_dtype"; B = 128 for the
+    ConvNeXt-T stages, 32 at 63 x 95, 16 at 224 x 224), the range of their
+    HBM fractions, the
+    paper-sweep geometric means and the peak-memory ratios."""
+    us = lambda ms: int(round(ms * 1e3))  # noqa: E731
+    by = {r["name"]: r for r in rows}
+    out = {}
+    if "small_fwd" in by:
+        out["small_fwd_ms"] = by["small_fwd"]["fwd_ms"]
+    if "convnext_s1" in by:
+        out["stage1_L3_f32"] = {"fwd_ms": by["convnext_s1"]["fwd_ms"], "fwdbwd_ms": by["convnext_s1"]["fwdbwd_ms"]}
+    s2 = [by.get(f"convnext_s2_L{L}") for L in range(1, 6)]
+    if all(s2):
+        out["stage2_f32_fb_us_L1to5"] = [us(r["fwdbwd_ms"]) for r in s2]
+    if "convnext_s1_bf16_L5" in by:
+        r = by["convnext_s1_bf16_L5"]
+        out["stage1_bf16_L5"] = {"fwd_ms": r["fwd_ms"], "fwdbwd_ms": r["fwdbwd_ms"]}
+    sweep = {}
+    for (B, C, H, W) in SWEEP_SHAPES:
+        for dt in ("f32", "bf16"):
+            sel = [by.get(f"sweep_{H}x{W}_c{C}_L{L}_{dt}") for L in range(1, 6)]
+            if all(sel):
+                sweep[f"{H}x{W}c{C}_{dt}"] = {"fwd": [us(r["fwd_ms"]) for r in sel],
+                                                   "fb": [us(r["fwdbwd_ms"]) for r in sel]}
+    if sweep:
+        out["sweep_us_L1to5"] = sweep
+        fr = [r["fwdbwd_hbm_frac"] for r in rows if r["name"].startswith("sweep_")]
+        out["sweep_fb_hbm_frac_min_max"] = [round(min(fr), 3), round(max(fr), 3)]
+    paper = paper_sweep_summary(rows)
+    if any(paper[k][dt] for k in paper for dt in paper[k]):
+        out["paper_sweep_geomean_us_L1to5"] = {
+            f"{k}_{dt}": {"fwd": [us(v["fwd_ms"]) for v in paper[k][dt]],
+                          "fb": [us(v["fwdbwd_ms"]) for v in paper[k][dt]]}
+            for k in paper for dt in paper[k] if paper[k][dt]}
+    if memory:
+        out["paper_sweep_peak_memory_over_compulsory_L1to5"] = {
+            dt: {"train": [round(v["train_peak_over_compulsory"], 3) for v in memory[dt]],
+                 "infer": [round(v["infer_peak_over_compulsory"], 3) for v in memory[dt]]} for dt in memory}
+    return out
+
+
+def _seeded_params(torch, gen, dev, C, k, L):
+    f32 = dict(device=dev, dtype=torch.float32)
+    bw = torch.rand(C, k, k, generator=gen, **f32) * 0.4 - 0.2
+    bs = torch.rand(C, generator=gen, **f32) + 0.5
+    lw = [torch.rand(4 * C, k, k, generator=gen, **f32) * 0.4 - 0.2 for _ in range(L)]
+    ls = [torch.rand(4 * C, generator=gen, **f32) * 0.15 + 0.05 for _ in range(L)]
+    return bw, bs, lw, ls
+
+
+def config_table(steps, dev, table_out=None):
     """ms, algorithmic GB/s and roofline fractions of fwd and fwd+bwd for every
     configuration. Timing-only inputs are drawn on the device (seeded, with the
     distributions of the parity inputs); buffer sets rotate so that one step's
@@ -143,17 +230,13 @@ def config_table(steps, dev):
     rows = []
     for name, B, C, H, W, k, L, dt in table_configs():
         gen.manual_seed(0)
-        f32 = dict(device=dev, dtype=torch.float32)
-        bw = (torch.rand(C, k, k, generator=gen, **f32) * 0.4 - 0.2)
-        bs = torch.rand(C, generator=gen, **f32) + 0.5
-        lw = [torch.rand(4 * C, k, k, generator=gen, **f32) * 0.4 - 0.2 for _ in range(L)]
-        ls = [torch.rand(4 * C, generator=gen, **f32) * 0.15 + 0.05 for _ in range(L)]
+        bw, bs, lw, ls = _seeded_params(torch, gen, dev, C, k, L)
         act = B * C * H * W * iomodel.elem_bytes(dt)
         nsets = max(1, min(8, -(-600 * 2 ** 20 // (4 * act))))
         sets = []
         for _ in range(nsets):
-            x = torch.randn(B, C, H, W, generator=gen, **f32).to(tdt[dt])
-            dy = torch.randn(B, C, H, W, generator=gen, **f32).to(tdt[dt])
+            x = torch.randn(B, C, H, W, generator=gen, device=dev).to(tdt[dt])
+            dy = torch.randn(B, C, H, W, generator=gen, device=dev).to(tdt[dt])
             sets.append((x, dy, torch.empty_like(x), torch.empty_like(x)))
         fws = torch.empty(max(1, binding.wtconv_forward_workspace_bytes(
             binding.make_desc(B, C, H, W, k, L, binding._dtype_code(sets[0][0])))), dtype=torch.uint8, device=dev)
@@ -192,12 +275,16 @@ def config_table(steps, dev):
                "fwdbwd_GBps": round(work.bytes_fwdbwd / (fb_ms * 1e-3) / 1e9, 1)}
         row["fwd_hbm_frac"] = round(row["fwd_GBps"] / iomodel.HBM_PEAK_GBPS, 4)
         row["fwdbwd_hbm_frac"] = round(row["fwdbwd_GBps"] / iomodel.HBM_PEAK_GBPS, 4)
+        row["fwd_fma_frac"] = round(iomodel.fma_floor_s(work.fma_fwd) / (fwd_ms * 1e-3), 4)
         row["fwdbwd_fma_frac"] = round(iomodel.fma_floor_s(work.fma_fwdbwd) / (fb_ms * 1e-3), 4)
         log(f"table: {name:28s} fwd {fwd_ms * 1e3:8.1f} us  fwd+bwd {fb_ms * 1e3:8.1f} us  "
-            f"{row['fwdbwd_GBps']:7.1f} GB/s  fma {row['fwdbwd_fma_frac']:.3f}")
+            f"{row['fwdbwd_GBps']:7.1f} GB/s  hbm {row['fwdbwd_hbm_frac']:.3f}  fma {row['fwdbwd_fma_frac']:.3f}")
         rows.append(row)
         del sets, bk, fws
         torch.cuda.empty_cache()
+    if table_out:
+        with open(table_out, "w") as f:
+            json.dump(rows, f, indent=0)
     return rows
 
 
@@ -267,6 +354,10 @@ def memory_table(dev):
     return out
 
 
+# ----------------------------------------------------------------------------
+# the CPU oracle as a baseline, and whole-workload parity
+# ----------------------------------------------------------------------------
+
 def cpu_model():
     try:
         with open("/proc/cpuinfo") as f:
@@ -278,10 +369,10 @@ def cpu_model():
     return "unknown"
 
 
-def cpu_baseline(inp, work_bytes, seconds):
+def cpu_baseline(inp, cfg, work_bytes, seconds):
     import oracle
 
-    planes = WORKLOAD["B"] * WORKLOAD["C"]
+    planes = cfg["B"] * cfg["C"]
     threads = oracle.num_threads()
     log(f"cpu_baseline: float64 oracle fwd+bwd over the whole workload ({planes} planes), {threads} threads")
     reps, t0 = 0, time.perf_counter()
@@ -292,29 +383,20 @@ def cpu_baseline(inp, work_bytes, seconds):
         el = time.perf_counter() - t0
         if el >= seconds:
             break
-    # single-thread forward on a 4-image slice of the same workload, scaled to the whole batch
-    nb = 4
-    oracle.set_num_threads(1)
-    t1 = time.perf_counter()
-    oracle.forward(inp.x[:nb], inp.base_w, inp.base_scale, inp.level_w, inp.level_scale)
-    el1 = time.perf_counter() - t1
-    oracle.set_num_threads(threads)
-    fwd1_s = el1 * WORKLOAD["B"] / nb
     refs = {"y": y_ref, "dx": g_ref["dx"], "d_base_w": g_ref["d_base_w"], "d_base_scale": g_ref["d_base_scale"],
             "d_level_w": g_ref["d_level_w"], "d_level_scale": g_ref["d_level_scale"]}
     return refs, {"value": round(work_bytes * reps / el / 1e9, 4), "unit": "GB/s", "cores": threads,
-            "kind": "oracle", "cpu_model": cpu_model(),
-            "sample": f"the full workload ({planes} planes of 56x56, k=5, L=3), forward and backward, "
-                      f"{reps} repetitions in {el:.1f} s, float64; {el / reps * 1e3:.1f} ms per step",
-            "fwd_1thread_s": round(fwd1_s, 3),
-            "fwd_1thread_sample": f"forward of {nb} of {WORKLOAD['B']} images ({nb * WORKLOAD['C']} planes) on one "
-                                  f"thread in {el1:.2f} s, scaled to the whole batch"}
+                  "kind": "oracle", "cpu_model": cpu_model()[:48],
+                  "sample": f"the whole workload ({planes} planes of {cfg['H']}x{cfg['W']}, k={cfg['k']}, "
+                            f"L={cfg['L']}), forward and backward, {reps} repetitions in {el:.1f} s, float64; "
+                            f"{el / reps * 1e3:.1f} ms per step"}
 
 
-def full_size_parity(refs, x, dy, bw, bs, lw, ls):
+def full_size_parity(refs, dtype, x, dy, bw, bs, lw, ls):
     """Every output of one forward and one backward of the library on the
     benchmark's own inputs against the float64 oracle's (the cpu_baseline run):
-    max |got - ref| / max |ref| per tensor, against the fp32 tolerance 1e-5."""
+    max |got - ref| / max |ref| per tensor, against the tolerance of the dtype
+    (1e-5 for fp32, 2e-2 for bf16 / fp16)."""
     import numpy as np
 
     from paper_2608_10805_amd import binding
@@ -324,13 +406,17 @@ def full_size_parity(refs, x, dy, bw, bs, lw, ls):
     errs = {}
     for name, ts in got.items():
         ref = refs[name] if isinstance(refs[name], list) else [refs[name]]
-        g = np.concatenate([t.detach().cpu().double().numpy().ravel() for t in ts])
+        g = np.concatenate([t.detach().float().cpu().double().numpy().ravel() for t in ts])
         r = np.concatenate([np.asarray(a, dtype=np.float64).ravel() for a in ref])
         errs[name] = float(np.max(np.abs(g - r)) / max(float(np.max(np.abs(r))), 1e-30))
-    tol = 1e-5
+    tol = 1e-5 if dtype == "f32" else 2e-2
     return {"vs": "float64 oracle, whole workload", "max_rel_err": {k: float(f"{v:.3g}") for k, v in errs.items()},
             "tol": tol, "pass": all(v < tol for v in errs.values())}
 
+
+# ----------------------------------------------------------------------------
+# ceilings measured on the device
+# ----------------------------------------------------------------------------
 
 def copy_ceiling_gbps(dev, gib=1):
     """Device-to-device copy of `gib` GiB: bytes read + written per second."""
@@ -382,6 +468,10 @@ def valu_probe(dev):
     return {"fp32_TFLOPs": round(2 * fma_s / 1e12, 2), "implied_clock_GHz": round(fma_s / (256 * 64) / 1e9, 3)}
 
 
+# ----------------------------------------------------------------------------
+# rocprofv3 summaries (profiles/) and their lookup
+# ----------------------------------------------------------------------------
+
 def kernel_source_hash():
     """sha256 of the HIP sources the library is built from."""
     import hashlib
@@ -393,27 +483,47 @@ def kernel_source_hash():
     return h.hexdigest()
 
 
-def load_traffic(path, kernel):
-    """Measured HBM bytes per launch of `kernel` from a counter summary under
-    profiles/ ("key: value" lines), if it was taken on the current kernel
-    sources and workload; else None."""
-    if not os.path.exists(path):
-        return None
+# Kernels of the headline step, by the symbol prefix rocprofv3 reports: the
+# fused forward kernel runs twice per step (y, and dx on dy with rotated
+# kernels), the kernel-gradient pass and the finalize once.
+STEP_KERNELS = {"forward": "fused_kernel<5, float, false, true, false>", "grad": "grad_kernel<5, float, false>",
+                "finalize": "reduce_kernel"}
+
+
+def profile_path(kind, workload):
+    return os.path.join(ROOT, "profiles", f"{kind}_{workload}.txt")
+
+
+def _read_kv(path):
     rec = {}
     with open(path) as f:
         for line in f:
             if ":" in line and not line.startswith("#"):
                 k, v = line.split(":", 1)
                 rec[k.strip()] = v.strip()
-    if rec.get("kernel_source_sha256") != kernel_source_hash() or rec.get("workload") != WORKLOAD["workload"]:
+    return rec
+
+
+def load_traffic(path, workload, kernel=None):
+    """From a traffic summary under profiles/ taken on the current kernel
+    sources and `workload`: the measured HBM bytes per launch of the kernel
+    whose symbol starts with `kernel`, or (kernel None) the summed bytes of
+    one whole step. None if the summary is missing or stale."""
+    if not os.path.exists(path):
         return None
-    key = f"{kernel}_hbm_bytes_per_launch"
-    return float(rec[key]) if key in rec else None
+    rec = _read_kv(path)
+    if rec.get("kernel_source_sha256") != kernel_source_hash() or rec.get("workload") != workload:
+        return None
+    if kernel is None:
+        return float(rec["step_hbm_bytes"]) if "step_hbm_bytes" in rec else None
+    for k, v in rec.items():
+        if k.startswith("bytes_per_launch ") and k[len("bytes_per_launch "):].startswith(kernel):
+            return float(v)
+    return None
 
 
-# Kernels of the benchmark step, by the symbol prefix rocprofv3 reports.
-STEP_KERNELS = {"forward": "fused_kernel<5, float, false, true, false>", "grad": "grad_kernel<5, float, false>",
-                "finalize": "reduce_kernel"}
+def _short_name(name):
+    return name.replace("void ", "").replace("wtc::(anonymous namespace)::", "").split("(wtc::")[0].strip()
 
 
 def _rocpd_rows(db, sql):
@@ -425,69 +535,143 @@ def _rocpd_rows(db, sql):
         con.close()
 
 
-def summarize_trace(db, out, command):
-    """Kernel statistics (calls, total and average duration) of a rocprofv3
-    --kernel-trace database, one line per kernel."""
+def summarize_trace(db, out, command, workload, steps):
+    """Kernel statistics (calls, calls per step, total and average duration) of
+    a rocprofv3 --kernel-trace database of a --profile-run, one line per kernel."""
+    B, C, H, W, k, L, dt = WORKLOADS[workload]
     rows = _rocpd_rows(db, "select name, count(*), sum(duration), avg(duration) from kernels group by name "
                            "order by sum(duration) desc")
     total = sum(r[2] for r in rows)
-    lines = ["# rocprofv3 kernel trace statistics, fused WTConv fwd+bwd benchmark step",
-             f"# workload: {WORKLOAD['workload']} B={WORKLOAD['B']} C={WORKLOAD['C']} H=W={WORKLOAD['H']} "
-             f"k={WORKLOAD['k']} L={WORKLOAD['L']} fp32, MI355X",
+    lines = ["# rocprofv3 kernel trace statistics, fused WTConv fwd+bwd steps, MI355X",
+             f"# workload: {workload} B={B} C={C} H={H} W={W} k={k} L={L} {dt}; {steps} steps profiled",
              f"# command: {command}",
+             f"workload: {workload}",
              f"kernel_source_sha256: {kernel_source_hash()}",
-             "# kernel | calls | total_us | average_us | percent"]
+             "# kernel | calls | calls_per_step | total_us | average_us | percent"]
     for name, n, tot, avg in rows:
-        short = name.replace("void ", "").replace("wtc::(anonymous namespace)::", "").split("(wtc::")[0]
-        lines.append(f"{short[:110]} | {n} | {tot / 1e3:.1f} | {avg / 1e3:.3f} | {100.0 * tot / total:.1f}")
+        per = f"{n / steps:.2f}" if steps else "-"
+        lines.append(f"{_short_name(name)[:110]} | {n} | {per} | {tot / 1e3:.1f} | {avg / 1e3:.3f} | "
+                     f"{100.0 * tot / total:.1f}")
     with open(out, "w") as f:
         f.write("\n".join(lines) + "\n")
 
 
 def _counter_per_kernel(db, counter):
-    """Mean value of `counter` per dispatch, by kernel name (rocprofv3 --pmc database)."""
+    """{kernel name: [value per dispatch]} of a rocprofv3 --pmc database (the
+    per-XCD / per-instance rows of one dispatch summed)."""
     rows = _rocpd_rows(db, f"select kernel_name, dispatch_id, sum(value) from counters_collection where "
                            f"counter_name = '{counter}' group by kernel_name, dispatch_id")
     acc = {}
     for name, _, v in rows:
         acc.setdefault(name, []).append(v)
-    return {k: sum(v) / len(v) for k, v in acc.items()}
+    return acc
 
 
-def summarize_traffic(fetch_db, write_db, cfetch_db, cwrite_db, copy_mib, out, command):
-    """Measured HBM bytes per launch of the step's kernels: FETCH_SIZE and
-    WRITE_SIZE (KiB) scaled by what the same counters report for a plain device
-    copy of known size."""
+def _copy_scales(cfetch_db, cwrite_db, copy_mib):
     copy_kib = copy_mib * 1024.0
-    cf = max((v for k, v in _counter_per_kernel(cfetch_db, "FETCH_SIZE").items() if "copyBuffer" in k), default=0)
-    cw = max((v for k, v in _counter_per_kernel(cwrite_db, "WRITE_SIZE").items() if "copyBuffer" in k), default=0)
-    fscale, wscale = copy_kib / cf, copy_kib / cw
+    cf = max((max(v) for k, v in _counter_per_kernel(cfetch_db, "FETCH_SIZE").items() if "copyBuffer" in k), default=0)
+    cw = max((max(v) for k, v in _counter_per_kernel(cwrite_db, "WRITE_SIZE").items() if "copyBuffer" in k), default=0)
+    return copy_kib, cf, cw, copy_kib / cf, copy_kib / cw
+
+
+def summarize_traffic(fetch_db, write_db, cfetch_db, cwrite_db, copy_mib, out, command, workload, steps):
+    """Measured HBM bytes per launch of every library kernel of a --profile-run
+    and per whole step: FETCH_SIZE and WRITE_SIZE (KiB) scaled by what the same
+    counters report for a plain device copy of known size."""
+    from paper_2608_10805_amd import iomodel
+    B, C, H, W, k, L, dt = WORKLOADS[workload]
+    copy_kib, cf, cw, fscale, wscale = _copy_scales(cfetch_db, cwrite_db, copy_mib)
     fetch = _counter_per_kernel(fetch_db, "FETCH_SIZE")
     write = _counter_per_kernel(write_db, "WRITE_SIZE")
-    B, C, H, W, k, L = (WORKLOAD[n] for n in ("B", "C", "H", "W", "k", "L"))
-    from paper_2608_10805_amd import iomodel
-    algo = 2.0 * B * C * H * W * 4 + 4.0 * iomodel.param_count(C, k, L)
-    lines = ["# HBM traffic per kernel launch from rocprofv3 counters, fused WTConv fwd+bwd benchmark step",
-             f"# workload: B={B} C={C} H=W={H} k={k} L={L} fp32 (ConvNeXt-T stage 1), MI355X",
+    N = B * C * H * W
+    e = iomodel.elem_bytes(dt)
+    work = iomodel.single_pass_work(B, C, H, W, k, L, dt)
+    lines = ["# HBM traffic from rocprofv3 counters, fused WTConv fwd+bwd steps, MI355X",
+             f"# workload: {workload} B={B} C={C} H={H} W={W} k={k} L={L} {dt}; {steps} steps profiled",
              f"# commands (one counter per run): {command}",
              f"# calibration: a {copy_mib} MiB device copy reads and writes {copy_kib:.0f} KiB; FETCH_SIZE reports "
              f"{cf:.0f} KiB (scale x{fscale:.3f}), WRITE_SIZE reports {cw:.0f} KiB (scale x{wscale:.3f})",
-             f"workload: {WORKLOAD['workload']}",
+             f"workload: {workload}",
              f"kernel_source_sha256: {kernel_source_hash()}",
              f"fetch_scale: {fscale:.4f}",
-             f"write_scale: {wscale:.4f}"]
-    for key, prefix in STEP_KERNELS.items():
-        fk = [v for n, v in fetch.items() if prefix in n]
-        wk = [v for n, v in write.items() if prefix in n]
-        if not fk or not wk:
+             f"write_scale: {wscale:.4f}",
+             "# kernel: FETCH KiB, WRITE KiB per launch -> HBM bytes per launch; launches per step"]
+    step_bytes = 0.0
+    for name in sorted(set(fetch) & set(write)):
+        if "wtc::" not in name:
             continue
-        f_kib, w_kib = sum(fk) / len(fk), sum(wk) / len(wk)
+        f_kib = sum(fetch[name]) / len(fetch[name])
+        w_kib = sum(write[name]) / len(write[name])
         hbm = f_kib * 1024 * fscale + w_kib * 1024 * wscale
-        note = f"; algorithmic {algo / 1e6:.2f} MB; ratio {hbm / algo:.3f}" if key != "finalize" else ""
-        lines.append(f"# {key} = {prefix}: FETCH {f_kib:.1f} KiB, WRITE {w_kib:.1f} KiB -> {hbm / 1e6:.2f} MB{note}")
-        lines.append(f"{key}_hbm_bytes_per_launch: {hbm:.0f}")
+        per_step = len(fetch[name]) / steps if steps else 0.0
+        step_bytes += hbm * per_step
+        short = _short_name(name)
+        lines.append(f"# {short}: FETCH {f_kib:.1f} KiB, WRITE {w_kib:.1f} KiB -> {hbm / 1e6:.3f} MB; "
+                     f"{per_step:.2f} per step")
+        lines.append(f"bytes_per_launch {short}: {hbm:.0f}")
+    lines.append(f"# one step (all library launches): {step_bytes / 1e6:.2f} MB = {step_bytes / (N * e):.3f} N "
+                 f"elements; the single-pass algorithmic figure is {work.bytes_fwdbwd / 1e6:.2f} MB (5 N + "
+                 f"parameters); the paper's forward models: Q_fused({L}) = {iomodel.q_fused(L):.3f} N, "
+                 f"Q_ref({L}) = {iomodel.q_ref(L):.3f} N")
+    lines.append(f"step_hbm_bytes: {step_bytes:.0f}")
+    lines.append(f"step_hbm_elems_per_N: {step_bytes / (N * e):.4f}")
     with open(out, "w") as f:
         f.write("\n".join(lines) + "\n")
+
+
+SQ_COUNTERS = ("SQ_WAVES", "SQ_INSTS_VALU", "SQ_INSTS_LDS", "SQ_INSTS_SALU", "SQ_WAVE_CYCLES", "SQ_BUSY_CYCLES",
+               "SQ_ACTIVE_INST_VALU", "SQ_WAIT_INST_LDS")
+
+
+def summarize_counters(db, out, command, workload):
+    """Instruction counters per launch of every library kernel (one rocprofv3
+    --pmc run with the eight SQ counters above); for the fused forward and
+    gradient-pass kernels also set against the algorithmic FMA count: each
+    full-lane wavefront FMA does 64 of them, and a SIMD issues one wavefront
+    VALU instruction per 4 cycles."""
+    from paper_2608_10805_amd import iomodel
+    B, C, H, W, k, L, dt = WORKLOADS[workload]
+    work = iomodel.single_pass_work(B, C, H, W, k, L, dt)
+    per = {name: _counter_per_kernel(db, name) for name in SQ_COUNTERS}
+    lines = ["# SQ instruction counters per kernel launch, fused WTConv fwd+bwd steps, MI355X",
+             f"# workload: {workload} B={B} C={C} H={H} W={W} k={k} L={L} {dt}",
+             f"# command: {command}",
+             f"workload: {workload}",
+             f"kernel_source_sha256: {kernel_source_hash()}"]
+    simds = 256 * 4
+    names = sorted({n for d in per.values() for n in d if "wtc::" in n})
+    for name in names:
+        short = _short_name(name)
+        vals = {c: sum(per[c][name]) / len(per[c][name]) for c in SQ_COUNTERS if name in per[c]}
+        lines.append(f"# {short}")
+        for c in SQ_COUNTERS:
+            if c in vals:
+                lines.append(f"{c} {short}: {vals[c]:.0f}")
+        if "SQ_INSTS_VALU" in vals and (short.startswith("fused_kernel") or short.startswith("grad_kernel")) and \
+                "true, true" not in short:
+            fma_wave = work.fma_fwd / 64.0
+            issue = 4.0 * vals["SQ_INSTS_VALU"] / simds
+            lines.append(f"# {short}: one pass's algorithmic FMAs {work.fma_fwd:.4g} = {fma_wave:.4g} full-lane "
+                         f"wavefront FMAs, {fma_wave / vals['SQ_INSTS_VALU']:.3f} of the VALU instructions issued "
+                         f"(if the launch covers the whole pass); VALU issue per SIMD {issue:.4g} cycles = "
+                         f"{issue / 2.2e3:.1f} us at 2.2 GHz")
+    with open(out, "w") as f:
+        f.write("\n".join(lines) + "\n")
+
+
+def load_trace_avg_us(path, workload, kernel):
+    """Average duration (us) of `kernel` in a kernel-trace summary taken on the
+    current sources and workload, or None."""
+    if not os.path.exists(path):
+        return None
+    rec = _read_kv(path)
+    if rec.get("kernel_source_sha256") != kernel_source_hash() or rec.get("workload") != workload:
+        return None
+    with open(path) as f:
+        for line in f:
+            if line.startswith(kernel) and "|" in line:
+                return float(line.split("|")[4])
+    return None
 
 
 # HBM traffic at L = 3, fp32, across tensor shapes (k = 5) and kernel sizes
@@ -508,12 +692,8 @@ def traffic_invariance_run(dev):
     gen = torch.Generator(device=dev)
     for B, C, H, W, k, L in INVARIANCE_CONFIGS:
         gen.manual_seed(0)
-        f32 = dict(device=dev, dtype=torch.float32)
-        bw = torch.rand(C, k, k, generator=gen, **f32) * 0.4 - 0.2
-        bs = torch.rand(C, generator=gen, **f32) + 0.5
-        lw = [torch.rand(4 * C, k, k, generator=gen, **f32) * 0.4 - 0.2 for _ in range(L)]
-        ls = [torch.rand(4 * C, generator=gen, **f32) * 0.15 + 0.05 for _ in range(L)]
-        x = torch.randn(B, C, H, W, generator=gen, **f32)
+        bw, bs, lw, ls = _seeded_params(torch, gen, dev, C, k, L)
+        x = torch.randn(B, C, H, W, generator=gen, device=dev)
         y = torch.empty_like(x)
         nbytes = binding.wtconv_forward_workspace_bytes(binding.make_desc(B, C, H, W, k, L, binding._dtype_code(x)))
         ws = torch.empty(max(1, nbytes), dtype=torch.uint8, device=dev)
@@ -545,10 +725,7 @@ def _library_dispatch_groups(db, counter):
 def summarize_invariance(fetch_db, write_db, cfetch_db, cwrite_db, copy_mib, out, command):
     """HBM traffic of each forward of --traffic-invariance-run, all of the
     library's kernels of that forward summed, in units of N fp32 elements."""
-    copy_kib = copy_mib * 1024.0
-    cf = max((v for k, v in _counter_per_kernel(cfetch_db, "FETCH_SIZE").items() if "copyBuffer" in k), default=0)
-    cw = max((v for k, v in _counter_per_kernel(cwrite_db, "WRITE_SIZE").items() if "copyBuffer" in k), default=0)
-    fscale, wscale = copy_kib / cf, copy_kib / cw
+    copy_kib, cf, cw, fscale, wscale = _copy_scales(cfetch_db, cwrite_db, copy_mib)
     fg = _library_dispatch_groups(fetch_db, "FETCH_SIZE")
     wg = _library_dispatch_groups(write_db, "WRITE_SIZE")
     if len(fg) != len(INVARIANCE_CONFIGS) or len(wg) != len(INVARIANCE_CONFIGS):
@@ -569,57 +746,100 @@ def summarize_invariance(fetch_db, write_db, cfetch_db, cwrite_db, copy_mib, out
         fh.write("\n".join(lines) + "\n")
 
 
-SQ_COUNTERS = ("SQ_WAVES", "SQ_INSTS_VALU", "SQ_INSTS_LDS", "SQ_INSTS_SALU", "SQ_WAVE_CYCLES", "SQ_BUSY_CYCLES",
-               "SQ_ACTIVE_INST_VALU", "SQ_WAIT_INST_LDS")
+# ----------------------------------------------------------------------------
+# the benchmark
+# ----------------------------------------------------------------------------
+
+class Step:
+    """One fwd+bwd step of a workload over rotating buffer sets."""
+
+    def __init__(self, dev, cfg, nsets, seed=0):
+        import numpy as np
+        import torch
+
+        from paper_2608_10805_amd import binding
+        from paper_2608_10805_amd.inputs import make_inputs
+
+        B, C, H, W, k, L, dt = (cfg[n] for n in ("B", "C", "H", "W", "k", "L", "dtype"))
+        self.inp = make_inputs(B, C, H, W, k, L, dt, seed=seed)
+        tdt = {"f32": torch.float32, "bf16": torch.bfloat16, "f16": torch.float16}[dt]
+        t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)  # noqa: E731
+        self.bw, self.bs = t(self.inp.base_w), t(self.inp.base_scale)
+        self.lw, self.ls = [t(a) for a in self.inp.level_w], [t(a) for a in self.inp.level_scale]
+        # storage-rounded activations (make_inputs rounds them, stored as float32 values)
+        self.x0 = t(self.inp.x).to(tdt)
+        self.dy0 = t(self.inp.dy).to(tdt)
+        self.sets = []
+        for s in range(nsets):
+            x = self.x0 if s == 0 else self.x0.clone()
+            dy = self.dy0 if s == 0 else self.dy0.clone()
+            self.sets.append((x, dy, torch.empty_like(x), torch.empty_like(x)))
+        self.fws = torch.empty(max(1, binding.wtconv_forward_workspace_bytes(
+            binding.make_desc(B, C, H, W, k, L, binding._dtype_code(self.x0)))), dtype=torch.uint8, device=dev)
+        self.bk = binding.Backward(self.x0, self.bw, self.bs, self.lw, self.ls, need_dx=True)
+        self.bk_nodx = None  # split(): the gradient pass alone, dx from wtconv_backward_data
+        self.binding = binding
+
+    def __call__(self, i, ev=None):
+        """wtconv_forward, wtconv_backward_partials (with dx) and
+        wtconv_backward_finalize: the whole operator, forward and backward.
+        With `ev` (three events) the forward and the backward phases are
+        bracketed on the library's stream."""
+        x, dy, y, dx = self.sets[i % len(self.sets)]
+        if ev is not None:
+            ev[0].record()
+        self.binding.forward(x, self.bw, self.bs, self.lw, self.ls, out=y, workspace=self.fws)
+        if ev is not None:
+            ev[1].record()
+        self.bk.partials(x, dy, dx)
+        self.bk.finalize()
+        if ev is not None:
+            ev[2].record()
+
+    def split(self, i, ev):
+        """The same kernels as __call__ for shapes whose backward is the
+        kernel-gradient pass plus the forward pass on dy with rotated kernels
+        (the headline's): wtconv_backward_partials without dx, then
+        wtconv_backward_data, then the finalize, with an event between every
+        two calls so that each kernel's duration is measured."""
+        if self.bk_nodx is None:
+            self.bk_nodx = self.binding.Backward(self.x0, self.bw, self.bs, self.lw, self.ls, need_dx=False)
+        bk = self.bk_nodx
+        x, dy, y, dx = self.sets[i % len(self.sets)]
+        ev[0].record()
+        self.binding.forward(x, self.bw, self.bs, self.lw, self.ls, out=y, workspace=self.fws)
+        ev[1].record()
+        bk.partials(x, dy, None)
+        ev[2].record()
+        bk.data(dy, dx)
+        ev[3].record()
+        bk.finalize()
+        ev[4].record()
 
 
-def summarize_counters(db, out, command):
-    """Instruction counters per launch of the step's forward and gradient
-    kernels (one rocprofv3 --pmc run with the eight SQ counters above), set
-    against the algorithmic FMA count: each full-lane wavefront FMA does 64 of
-    them, and a SIMD issues one wavefront VALU instruction per 4 cycles."""
-    from paper_2608_10805_amd import iomodel
-    B, C, H, W, k, L = (WORKLOAD[n] for n in ("B", "C", "H", "W", "k", "L"))
-    work = iomodel.single_pass_work(B, C, H, W, k, L, "f32")
-    per = {name: _counter_per_kernel(db, name) for name in SQ_COUNTERS}
-    lines = ["# SQ instruction counters per kernel launch, fused WTConv fwd+bwd benchmark step",
-             f"# workload: B={B} C={C} H=W={H} k={k} L={L} fp32 (ConvNeXt-T stage 1), MI355X",
-             f"# command: {command}",
-             f"workload: {WORKLOAD['workload']}",
-             f"kernel_source_sha256: {kernel_source_hash()}"]
-    simds = 256 * 4
-    for key in ("forward", "grad"):
-        prefix = STEP_KERNELS[key]
-        vals = {}
-        for name in SQ_COUNTERS:
-            v = [x for n, x in per[name].items() if prefix in n]
-            if v:
-                vals[name] = sum(v) / len(v)
-        if "SQ_INSTS_VALU" not in vals:
-            continue
-        fma_wave = work.fma_fwd / 64.0
-        issue_cycles = 4.0 * vals["SQ_INSTS_VALU"] / simds
-        lines.append(f"# {key} = {prefix}")
-        for name in SQ_COUNTERS:
-            if name in vals:
-                lines.append(f"{key}_{name}: {vals[name]:.0f}")
-        lines.append(f"# {key}: algorithmic FMAs {work.fma_fwd:.4g} = {fma_wave:.4g} full-lane wavefront FMAs, "
-                     f"{fma_wave / vals['SQ_INSTS_VALU']:.3f} of the VALU instructions issued; VALU issue per SIMD "
-                     f"{issue_cycles:.4g} cycles = {issue_cycles / 2.2e3:.1f} us at 2.2 GHz")
-    with open(out, "w") as f:
-        f.write("\n".join(lines) + "\n")
+def warm(step, min_steps, min_s):
+    """At least `min_steps` untimed steps and at least `min_s` seconds of them."""
+    import torch
+    n, t0 = 0, time.perf_counter()
+    while n < min_steps or time.perf_counter() - t0 < min_s:
+        for _ in range(max(1, min(min_steps, 50))):
+            step(n)
+            n += 1
+        torch.cuda.synchronize()
+    return n, time.perf_counter() - t0
 
 
-def main():
-    args = parse()
+def main(argv=None):
+    args = parse(argv)
     if args.summarize_counters:
-        summarize_counters(args.summarize_counters, args.out, args.command)
+        summarize_counters(args.summarize_counters, args.out, args.command, args.workload)
         return
     if args.summarize_trace:
-        summarize_trace(args.summarize_trace, args.out, args.command)
+        summarize_trace(args.summarize_trace, args.out, args.command, args.workload, args.profiled_steps)
         return
     if args.summarize_traffic:
-        summarize_traffic(*args.summarize_traffic, args.copy_mib, args.out, args.command)
+        summarize_traffic(*args.summarize_traffic, args.copy_mib, args.out, args.command, args.workload,
+                          args.profiled_steps)
         return
     if args.summarize_invariance:
         summarize_invariance(*args.summarize_invariance, args.copy_mib, args.out, args.command)
@@ -633,8 +853,7 @@ def main():
     import numpy as np
     import torch
 
-    from paper_2608_10805_amd import binding, iomodel
-    from paper_2608_10805_amd.inputs import make_inputs
+    from paper_2608_10805_amd import iomodel
 
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
@@ -651,42 +870,20 @@ def main():
     if args.traffic_invariance_run:
         traffic_invariance_run(dev)
         return
-    B, C, H, W, k, L = (WORKLOAD[n] for n in ("B", "C", "H", "W", "k", "L"))
-    log(f"bench: {WORKLOAD['workload']} B={B} C={C} H={H} W={W} k={k} L={L} f32, steps={args.steps} "
+    cfg = workload_config(args.workload)
+    B, C, H, W, k, L, dt = WORKLOADS[args.workload]
+    log(f"bench: {args.workload} B={B} C={C} H={H} W={W} k={k} L={L} {dt}, steps={args.steps} "
         f"warmup={args.warmup} sets={args.sets}")
-    inp = make_inputs(B, C, H, W, k, L, "f32", seed=0)
-    t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)  # noqa: E731
-    bw, bs = t(inp.base_w), t(inp.base_scale)
-    lw, ls = [t(a) for a in inp.level_w], [t(a) for a in inp.level_scale]
-    x0, dy0 = t(inp.x), t(inp.dy)
-    sets = []
-    for s in range(args.sets):
-        x = x0 if s == 0 else x0.clone()
-        dy = dy0 if s == 0 else dy0.clone()
-        sets.append((x, dy, torch.empty_like(x), torch.empty_like(x)))
-    bk = binding.Backward(x0, bw, bs, lw, ls, need_dx=False)
+    step = Step(dev, cfg, args.sets)
+    if args.profile_run:
+        for i in range(args.warmup + args.steps):
+            step(i)
+        torch.cuda.synchronize()
+        log(f"bench: profile run of {args.warmup + args.steps} steps done")
+        return
 
-    def step(i, ev=None):
-        x, dy, y, dx = sets[i % len(sets)]
-        if ev is not None:
-            ev[0].record()
-        binding.forward(x, bw, bs, lw, ls, out=y)
-        if ev is not None:
-            ev[1].record()
-        bk.partials(x, dy, None)
-        if ev is not None:
-            ev[2].record()
-        bk.data(dy, dx)
-        if ev is not None:
-            ev[3].record()
-        bk.finalize()
-        if ev is not None:
-            ev[4].record()
-
-    for i in range(args.warmup):
-        step(i)
-    torch.cuda.synchronize()
-    log("bench: warmup done")
+    nwarm, warm_s = warm(step, args.warmup, MIN_WARMUP_S)
+    log(f"bench: warmup {nwarm} steps in {warm_s * 1e3:.0f} ms")
 
     # The timed region: K plain steps (no events between the calls).
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -697,97 +894,106 @@ def main():
     end.record()
     torch.cuda.synchronize()
     ms_step = start.elapsed_time(end) / args.steps
-    # The same K steps again with an event between every two calls, on the
-    # library's stream, for each kernel's duration. The five event records add
-    # a few microseconds per call, so this pass is not the step time.
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+
+    # The same K steps again with events between the calls, on the library's
+    # stream (torch's current stream), for each kernel's duration. The event
+    # records add a few microseconds per call, so this pass is not the step time.
+    headline = args.workload == HEADLINE
+    nev = 5 if headline else 3
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(nev)] for _ in range(args.steps)]
     torch.cuda.synchronize()
     for i in range(args.steps):
-        step(i, evs[i])
+        if headline:
+            step.split(i, evs[i])
+        else:
+            step(i, evs[i])
     torch.cuda.synchronize()
-    per_step = [e[0].elapsed_time(e[4]) for e in evs]
-    fwd_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
-    grad_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
-    data_ms = float(np.mean([e[2].elapsed_time(e[3]) for e in evs]))
-    fin_ms = float(np.mean([e[3].elapsed_time(e[4]) for e in evs]))
-    log(f"bench: {ms_step * 1e3:.1f} us/step; with events between the calls {np.mean(per_step) * 1e3:.1f} us = "
-        f"forward {fwd_ms * 1e3:.1f}, kernel-gradient pass {grad_ms * 1e3:.1f}, dx pass {data_ms * 1e3:.1f}, "
-        f"finalize {fin_ms * 1e3:.1f}")
-
-    work = iomodel.single_pass_work(B, C, H, W, k, L, "f32")
-    value = work.bytes_fwdbwd / (ms_step * 1e-3) / 1e9
-    # Kernels of the step for this workload (each entry point is one launch
-    # here): the fused forward kernel runs twice (y, and dx on dy with rotated
-    # kernels), the kernel-gradient pass once. Algorithmic work per launch:
-    # the forward k^2 (N + coefficient sites) FMAs, moving x (or dy) in and y
-    # (or dx) out; the gradient pass the same FMA count, reading x and dy.
+    mean = lambda a, b: float(np.mean([e[a].elapsed_time(e[b]) for e in evs]))  # noqa: E731
+    inst_ms = mean(0, nev - 1)
+    fwd_ms = mean(0, 1)
+    work = iomodel.single_pass_work(B, C, H, W, k, L, dt)
     N = B * C * H * W
-    fwd_bytes = 2.0 * N * 4 + 4.0 * iomodel.param_count(C, k, L)
-    kernels = {
-        "forward": {"launches_per_step": 2, "ms": (fwd_ms + data_ms) / 2, "fma": work.fma_fwd, "bytes": fwd_bytes},
-        "grad": {"launches_per_step": 1, "ms": grad_ms, "fma": work.fma_fwd, "bytes": fwd_bytes},
-    }
-    for kv in kernels.values():
-        kv["TFLOPs"] = round(2.0 * kv["fma"] / (kv["ms"] * 1e-3) / 1e12, 3)
-        kv["fma_frac"] = round(iomodel.fma_floor_s(kv["fma"]) / (kv["ms"] * 1e-3), 4)
-        kv["GBps"] = round(kv["bytes"] / (kv["ms"] * 1e-3) / 1e9, 1)
-        kv["ms"] = round(kv["ms"], 5)
-    kernels["finalize"] = {"launches_per_step": 1, "ms": round(fin_ms, 5)}
-    dom = max(("forward", "grad"), key=lambda n: kernels[n]["ms"] * kernels[n]["launches_per_step"])
-    dom_ms, dom_fma, dom_bytes = kernels[dom]["ms"], kernels[dom]["fma"], kernels[dom]["bytes"]
+    e = iomodel.elem_bytes(dt)
+    fwd_bytes = 2.0 * N * e + 4.0 * iomodel.param_count(C, k, L)
+    kernels = {}
+    if headline:
+        grad_ms, data_ms, fin_ms = mean(1, 2), mean(2, 3), mean(3, 4)
+        log(f"bench: {ms_step * 1e3:.1f} us/step; with events between the calls {inst_ms * 1e3:.1f} us = "
+            f"forward {fwd_ms * 1e3:.1f}, kernel-gradient pass {grad_ms * 1e3:.1f}, dx pass {data_ms * 1e3:.1f}, "
+            f"finalize {fin_ms * 1e3:.1f}")
+        # Algorithmic work per launch: the forward k^2 (N + coefficient sites)
+        # FMAs, moving x (or dy) in and y (or dx) out; the gradient pass the
+        # same FMA count, reading x and dy.
+        kernels = {"forward": {"launches_per_step": 2, "ms": (fwd_ms + data_ms) / 2, "fma": work.fma_fwd,
+                               "bytes": fwd_bytes},
+                   "grad": {"launches_per_step": 1, "ms": grad_ms, "fma": work.fma_fwd, "bytes": fwd_bytes}}
+        for kv in kernels.values():
+            kv["TFLOPs"] = round(2.0 * kv["fma"] / (kv["ms"] * 1e-3) / 1e12, 2)
+            kv["fma_frac"] = round(iomodel.fma_floor_s(kv["fma"]) / (kv["ms"] * 1e-3), 4)
+            kv["hbm_frac"] = round(kv["bytes"] / (kv["ms"] * 1e-3) / 1e9 / iomodel.HBM_PEAK_GBPS, 4)
+            kv["ms"] = round(kv["ms"], 5)
+            del kv["fma"], kv["bytes"]
+        kernels["finalize"] = {"launches_per_step": 1, "ms": round(fin_ms, 5)}
+        dom = max(("forward", "grad"), key=lambda n: kernels[n]["ms"] * kernels[n]["launches_per_step"])
+        dom_ms, dom_fma, dom_bytes = kernels[dom]["ms"], work.fma_fwd, fwd_bytes
+        dom_symbol = STEP_KERNELS[dom]
+    else:
+        bwd_ms = mean(1, 2)
+        log(f"bench: {ms_step * 1e3:.1f} us/step; with events {inst_ms * 1e3:.1f} us = forward "
+            f"{fwd_ms * 1e3:.1f}, backward {bwd_ms * 1e3:.1f}")
+        # the forward call as a whole (one or more launches) is the unit here
+        dom, dom_ms, dom_fma, dom_bytes, dom_symbol = "forward_call", fwd_ms, work.fma_fwd, fwd_bytes, None
     achieved = 2.0 * dom_fma / (dom_ms * 1e-3) / 1e12
     peak = iomodel.FP32_FLOPS / 1e12
-    traffic = load_traffic(args.traffic, dom)
+    traffic = load_traffic(profile_path("hbm_traffic", args.workload), args.workload, dom_symbol) \
+        if dom_symbol else None
+    step_traffic = load_traffic(profile_path("hbm_traffic", args.workload), args.workload)
+    trace_us = load_trace_avg_us(profile_path("kernel_trace", args.workload), args.workload, dom_symbol) \
+        if dom_symbol else None
     copy_gbps = copy_ceiling_gbps(dev)
     probe = valu_probe(dev)
     log(f"bench: copy ceiling {copy_gbps:.0f} GB/s, VALU probe {probe}")
+    dom_gbps = dom_bytes / (dom_ms * 1e-3) / 1e9
     roofline = {"bound": "alu", "achieved": round(achieved, 3), "peak": round(peak, 1), "unit": "TFLOP/s",
-                "frac": round(achieved / peak, 4), "traffic": traffic, "kernel": dom,
-                "kernel_ms": round(dom_ms, 5),
-                "hbm_view": {"algorithmic_bytes": dom_bytes,
-                             "achieved_GBps": round(dom_bytes / (dom_ms * 1e-3) / 1e9, 1),
-                             "frac": round(dom_bytes / (dom_ms * 1e-3) / 1e9 / iomodel.HBM_PEAK_GBPS, 4)}}
-    table = None
-    memory = None
+                "frac": round(achieved / peak, 4), "traffic": traffic,
+                "peak_kind": "non-packed fp32 VALU: 256 CU x 64 lanes x 2 x 2.4 GHz; published 157.3 is packed",
+                "frac_of_published_157_3": round(achieved / (iomodel.FP32_FLOPS_PACKED / 1e12), 4),
+                "kernel": dom_symbol or dom, "kernel_ms": round(dom_ms, 5),
+                "rocprof_avg_ms": round(trace_us * 1e-3, 5) if trace_us else None,
+                "hbm": {"algorithmic_bytes": dom_bytes, "GBps": round(dom_gbps, 1), "peak_GBps": iomodel.HBM_PEAK_GBPS,
+                        "frac": round(dom_gbps / iomodel.HBM_PEAK_GBPS, 4)}}
+    table, memory = None, None
     if not args.no_config_table:
-        table = config_table(args.table_steps, dev)
+        table = config_table(args.table_steps, dev, args.table_out)
         memory = memory_table(dev)
-    cpu = None
-    parity = None
+    cpu, parity = None, None
     if not args.no_cpu_baseline:
-        refs, cpu = cpu_baseline(inp, work.bytes_fwdbwd, args.cpu_seconds)
-        parity = full_size_parity(refs, x0, dy0, bw, bs, lw, ls)
+        refs, cpu = cpu_baseline(step.inp, cfg, work.bytes_fwdbwd, args.cpu_seconds)
+        parity = full_size_parity(refs, dt, step.x0, step.dy0, step.bw, step.bs, step.lw, step.ls)
         log(f"parity vs the float64 oracle (whole workload): {parity}")
+    value = work.bytes_fwdbwd / (ms_step * 1e-3) / 1e9
     out = {
         "metric": METRIC, "value": round(value, 2), "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
-        "warmup": args.warmup, "ms_per_step": round(ms_step, 5), "higher_is_better": True, "scaling": "weak",
-        "vs_baseline": None, "dtype": "f32", "data": "synthetic (seeded; x, dy ~ N(0,1), weights U(-0.2,0.2))",
-        "config": dict(WORKLOAD),
+        "warmup": args.warmup, "warmup_steps_run": nwarm, "warmup_ms": round(warm_s * 1e3, 1),
+        "ms_per_step": round(ms_step, 5), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": dt, "data": "synthetic (seeded; x, dy ~ N(0,1), weights U(-0.2,0.2))",
+        "config": cfg,
         "hbm_frac": round(value / iomodel.HBM_PEAK_GBPS, 4),
-        "ms_mean": round(ms_step, 5),
-        "instrumented_step_ms": {"mean": round(float(np.mean(per_step)), 5),
-                                 "median": round(float(np.median(per_step)), 5),
-                                 "min": round(float(np.min(per_step)), 5)},
-        "copy_ceiling_GBps": round(copy_gbps, 1), "hbm_frac_of_copy": round(value / copy_gbps, 4),
-        "valu_probe": probe,
         "fma_frac": round(iomodel.fma_floor_s(work.fma_fwdbwd) / (ms_step * 1e-3), 4),
-        "fwd_ms": round(fwd_ms, 5), "bwd_ms": round(grad_ms + data_ms + fin_ms, 5), "kernels": kernels,
-        "algorithmic_bytes_per_step": work.bytes_fwdbwd,
         "floors_us": {"hbm": round(iomodel.hbm_floor_s(work.bytes_fwdbwd) * 1e6, 2),
-                      "fp32_fma": round(iomodel.fma_floor_s(work.fma_fwdbwd) * 1e6, 2)},
-        "paper_io_model_elems_per_N": {"Q_ref": round(iomodel.q_ref(L), 3), "Q_fused": round(iomodel.q_fused(L), 3),
-                                       "single_pass_fwd": 2, "single_pass_fwdbwd": 5,
-                                       "rocprof_dominant_kernel": (round(traffic / (N * 4), 3)
-                                                                   if traffic is not None else None)},
+                      "fp32_fma_nonpacked": round(iomodel.fma_floor_s(work.fma_fwdbwd) * 1e6, 2)},
+        "instrumented_step_ms": round(inst_ms, 5), "fwd_ms": round(fwd_ms, 5),
+        "kernels": kernels,
         "roofline": roofline,
+        "step_hbm_elems_per_N": {"rocprof_all_kernels": round(step_traffic / (N * e), 3) if step_traffic else None,
+                                 "single_pass_algorithmic": 5, "paper_Q_fused_fwd": round(iomodel.q_fused(L), 3),
+                                 "paper_Q_ref_fwd": round(iomodel.q_ref(L), 3)},
+        "copy_ceiling_GBps": round(copy_gbps, 1), "valu_probe": probe,
         "cpu_baseline": cpu,
         "parity": parity,
-        "N": N,
-        "configs": table,
-        "paper_layer_sweep_geomean": paper_sweep_summary(table) if table else None,
-        "paper_layer_sweep_peak_memory": memory,
+        "configs_summary": configs_summary(table, memory) if table else None,
     }
-    print(json.dumps(out), flush=True)
+    print(json.dumps(out, separators=(",", ":")), flush=True)
 
 
 if __name__ == "__main__":

@@ -61,33 +61,48 @@ def test_more_than_one_gpu_is_refused():
     assert "one GPU" in r.stderr
 
 
+WL = bench.HEADLINE
+
+
 def test_summarize_trace(tmp_path):
     db = _trace_db(tmp_path / "t.db", [(FWD, 70000), (FWD, 72000), (GRAD, 90000), (RED, 4000)])
     out = tmp_path / "trace.txt"
-    bench.summarize_trace(db, str(out), "the command")
+    bench.summarize_trace(db, str(out), "the command", WL, 1)
     text = out.read_text()
     assert "# command: the command" in text
-    assert _kv(out)["kernel_source_sha256"] == bench.kernel_source_hash()
+    rec = _kv(out)
+    assert rec["kernel_source_sha256"] == bench.kernel_source_hash()
+    assert rec["workload"] == WL
     fwd_line = [ln for ln in text.splitlines() if ln.startswith("fused_kernel<5, float, false, true, false>")][0]
-    name, calls, total, avg, pct = [f.strip() for f in fwd_line.split("|")]
-    assert (calls, total, avg) == ("2", "142.0", "71.000")
+    name, calls, per_step, total, avg, pct = [f.strip() for f in fwd_line.split("|")]
+    assert (calls, per_step, total, avg) == ("2", "2.00", "142.0", "71.000")
     assert abs(float(pct) - 100.0 * 142 / 236) < 0.06
+    assert bench.load_trace_avg_us(str(out), WL, bench.STEP_KERNELS["forward"]) == pytest.approx(71.0)
+    assert bench.load_trace_avg_us(str(out), "other", bench.STEP_KERNELS["forward"]) is None
 
 
 def test_summarize_traffic_scales_by_the_copy(tmp_path):
     # the copy reads 256 MiB but FETCH_SIZE shows half of it; WRITE_SIZE all of it
     kib = 256 * 1024.0
-    fetch = _counter_db(tmp_path / "f.db", "FETCH_SIZE", {FWD: [1000.0, 1000.0], GRAD: [3000.0]})
-    write = _counter_db(tmp_path / "w.db", "WRITE_SIZE", {FWD: [500.0, 500.0], GRAD: [10.0]})
+    fetch = _counter_db(tmp_path / "f.db", "FETCH_SIZE", {FWD: [1000.0, 1000.0], GRAD: [3000.0], RED: [4.0]})
+    write = _counter_db(tmp_path / "w.db", "WRITE_SIZE", {FWD: [500.0, 500.0], GRAD: [10.0], RED: [2.0]})
     cfetch = _counter_db(tmp_path / "cf.db", "FETCH_SIZE", {COPY: [kib / 2]})
     cwrite = _counter_db(tmp_path / "cw.db", "WRITE_SIZE", {COPY: [kib]})
     out = tmp_path / "traffic.txt"
-    bench.summarize_traffic(fetch, write, cfetch, cwrite, 256, str(out), "cmd")
+    bench.summarize_traffic(fetch, write, cfetch, cwrite, 256, str(out), "cmd", WL, 1)
     rec = _kv(out)
     assert float(rec["fetch_scale"]) == pytest.approx(2.0)
     assert float(rec["write_scale"]) == pytest.approx(1.0)
-    assert float(rec["forward_hbm_bytes_per_launch"]) == pytest.approx((2 * 1000 + 500) * 1024, rel=1e-9)
-    assert float(rec["grad_hbm_bytes_per_launch"]) == pytest.approx((2 * 3000 + 10) * 1024, rel=1e-9)
+    fwd = (2 * 1000 + 500) * 1024
+    grad = (2 * 3000 + 10) * 1024
+    red = (2 * 4 + 2) * 1024
+    assert float(rec["bytes_per_launch fused_kernel<5, float, false, true, false>"]) == pytest.approx(fwd, rel=1e-9)
+    assert float(rec["bytes_per_launch grad_kernel<5, float, false>"]) == pytest.approx(grad, rel=1e-9)
+    # one profiled step: the forward kernel twice, the others once
+    step = 2 * fwd + grad + red
+    assert float(rec["step_hbm_bytes"]) == pytest.approx(step, rel=1e-6)
+    B, C, H, W, k, L, dt = bench.WORKLOADS[WL]
+    assert float(rec["step_hbm_elems_per_N"]) == pytest.approx(step / (4.0 * B * C * H * W), abs=1e-4)
 
 
 def test_traffic_lookup_needs_current_sources(tmp_path):
@@ -97,13 +112,16 @@ def test_traffic_lookup_needs_current_sources(tmp_path):
     cfetch = _counter_db(tmp_path / "cf.db", "FETCH_SIZE", {COPY: [kib]})
     cwrite = _counter_db(tmp_path / "cw.db", "WRITE_SIZE", {COPY: [kib]})
     out = tmp_path / "traffic.txt"
-    bench.summarize_traffic(fetch, write, cfetch, cwrite, 1, str(out), "cmd")
-    assert bench.load_traffic(str(out), "forward") == pytest.approx(200 * 1024)
-    assert bench.load_traffic(str(out), "grad") is None  # no counters for it
+    bench.summarize_traffic(fetch, write, cfetch, cwrite, 1, str(out), "cmd", WL, 1)
+    fwd = bench.STEP_KERNELS["forward"]
+    assert bench.load_traffic(str(out), WL, fwd) == pytest.approx(200 * 1024)
+    assert bench.load_traffic(str(out), WL) == pytest.approx(200 * 1024)
+    assert bench.load_traffic(str(out), WL, bench.STEP_KERNELS["grad"]) is None  # no counters for it
+    assert bench.load_traffic(str(out), "another_workload", fwd) is None
     stale = out.read_text().replace(bench.kernel_source_hash(), "0" * 64)
     out.write_text(stale)
-    assert bench.load_traffic(str(out), "forward") is None
-    assert bench.load_traffic(str(tmp_path / "missing.txt"), "forward") is None
+    assert bench.load_traffic(str(out), WL, fwd) is None
+    assert bench.load_traffic(str(tmp_path / "missing.txt"), WL, fwd) is None
 
 
 def test_summarize_counters(tmp_path):
@@ -120,11 +138,46 @@ def test_summarize_counters(tmp_path):
     con.commit()
     con.close()
     out = tmp_path / "sq.txt"
-    bench.summarize_counters(str(tmp_path / "sq.db"), str(out), "cmd")
+    bench.summarize_counters(str(tmp_path / "sq.db"), str(out), "cmd", WL)
     rec = _kv(out)
-    assert float(rec["forward_SQ_INSTS_VALU"]) == per["SQ_INSTS_VALU"][FWD][0]
-    assert float(rec["grad_SQ_INSTS_VALU"]) == per["SQ_INSTS_VALU"][GRAD][0]
+    assert float(rec["SQ_INSTS_VALU fused_kernel<5, float, false, true, false>"]) == per["SQ_INSTS_VALU"][FWD][0]
+    assert float(rec["SQ_INSTS_VALU grad_kernel<5, float, false>"]) == per["SQ_INSTS_VALU"][GRAD][0]
     assert rec["kernel_source_sha256"] == bench.kernel_source_hash()
+
+
+def _fake_rows():
+    rows = []
+    for i, (name, B, C, H, W, k, L, dt) in enumerate(bench.table_configs()):
+        rows.append({"name": name, "B": B, "C": C, "H": H, "W": W, "k": k, "L": L, "dtype": dt,
+                     "fwd_ms": 0.1234 + i * 1e-4, "fwdbwd_ms": 0.4567 + i * 1e-4, "fwd_GBps": 1234.5,
+                     "fwdbwd_GBps": 2345.6, "fwd_hbm_frac": 0.1543, "fwdbwd_hbm_frac": 0.2932,
+                     "fwd_fma_frac": 0.4, "fwdbwd_fma_frac": 0.41})
+    return rows
+
+
+def test_configs_summary_covers_every_sweep_point_compactly():
+    """The headline line carries every (shape, dtype, L = 1..5) point of the
+    shape sweep and stays a few KB, so the whole line survives a tail of the
+    benchmark's output."""
+    import json
+    memory = {dt: [{"L": L, "train_peak_over_compulsory": 1.2, "infer_peak_over_compulsory": 1.3}
+                   for L in range(1, 6)] for dt in ("f32", "f16")}
+    s = bench.configs_summary(_fake_rows(), memory)
+    sweep = s["sweep_us_L1to5"]
+    assert len(sweep) == 2 * len(bench.SWEEP_SHAPES)
+    for v in sweep.values():
+        assert len(v["fwd"]) == len(v["fb"]) == 5
+    assert len(s["stage2_f32_fb_us_L1to5"]) == 5
+    assert set(s["paper_sweep_geomean_us_L1to5"]) == {"k5_f32", "k5_f16", "k3_f32", "k3_f16"}
+    assert len(json.dumps(s, separators=(",", ":"))) < 2000
+
+
+def test_table_has_every_sweep_level():
+    names = {c[0] for c in bench.table_configs()}
+    for (B, C, H, W) in bench.SWEEP_SHAPES:
+        for dt in ("f32", "bf16"):
+            for L in range(1, 6):
+                assert f"sweep_{H}x{W}_c{C}_L{L}_{dt}" in names
 
 
 def test_summarize_invariance_groups_each_forward(tmp_path):
