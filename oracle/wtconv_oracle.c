@@ -9,12 +9,16 @@
  * What it computes (Aflalo et al., "Fast and Memory-Efficient Wavelet
  * Convolutions via I/O-Aware Reformulation"):
  *
- *   Section 2.1, Algorithm 1 (the reference WTConv operator), materialised
- *   step by step in float64, one (batch, channel) plane at a time:
- *     X0 = x
- *     for l = 1..L:  Y_l = A(X_{l-1});  Z_l = s_l * (Y_l (*) W_l);  X_l = LL(Y_l)
- *     R = 0;  for l = L..1:  R = A^T( (LL(Z_l) + R) || H(Z_l) )
- *     y = s0 * (x (*) W0 + b) + R                   (b: one bias per channel)
+ *   the WTConv operator of Section 2.1 (Alg. 1), materialised in float64,
+ *   one (batch, channel) plane at a time. Its output is a base path plus a
+ *   wavelet branch. The base path is the plane correlated with the base
+ *   kernel W0, plus the bias b, times the base scale s0. The wavelet branch
+ *   takes an L-level Haar pyramid of the plane (level 1 analyses the plane,
+ *   level l analyses the unfiltered low-pass band of level l-1), correlates
+ *   each of the four bands of every level with its own kernel and multiplies
+ *   it by its own scale, and synthesises the result back level by level from
+ *   the coarsest: at each level the reconstruction from below joins the
+ *   filtered low-pass band before one synthesis step.
  *   A is one level of the orthonormal 2x2 Haar transform, i.e. the matrix of
  *   Proposition 1 applied to every non-overlapping 2x2 block, with the band
  *   formulas of eq. (butterfly) in Section 4.1. A^T is its synthesis.
@@ -188,8 +192,8 @@ long oracle_pyramid_size(int H, int W, int L)
     return n;
 }
 
-/* The unfiltered Haar pyramid Y_1..Y_L of one plane (the "decompose" half of
- * Alg. 1's downward loop, carrying the raw LL band). */
+/* The unfiltered Haar pyramid Y_1..Y_L of one plane (Alg. 1): level l is the
+ * analysis of level l-1's unfiltered low-pass band (of x itself for l = 1). */
 int oracle_plane_pyramid(int H, int W, int L, const double* x, double* y_out)
 {
     int hs[64], ws[64];
@@ -210,10 +214,12 @@ int oracle_plane_pyramid(int H, int W, int L, const double* x, double* y_out)
 }
 
 /*
- * Upward half of Alg. 1 (the synthesis cascade):
- *   R^(L+1) = 0;  for l = L..1:  R^(l) = A^T( (LL(Z_l) + R^(l+1)) || H(Z_l) ),
- * each synthesis cropped to the size of that level's input. z is the pyramid
- * Z_1..Z_L laid out as in oracle_pyramid_size; R is H x W. With L = 0, R = 0.
+ * Synthesis cascade of Alg. 1, from the coarsest level to the finest: the
+ * partial reconstruction coming up from the level below (zero under the
+ * coarsest) is added to the filtered LL band of level l, the four bands are
+ * synthesised one level (A^T) and cropped to the size of level l-1's grid.
+ * z is the pyramid Z_1..Z_L laid out as in oracle_pyramid_size; R is H x W.
+ * With L = 0, R = 0.
  */
 int oracle_cascade_synthesis(int H, int W, int L, const double* z, double* R)
 {
@@ -234,8 +240,8 @@ int oracle_cascade_synthesis(int H, int W, int L, const double* z, double* R)
         off -= 4L * n;
         memcpy(U, z + off, sizeof(double) * 4 * (size_t)n);
         if (have_r)
-            for (int e = 0; e < n; ++e) U[e] += Rn[e];                     /* LL(Z_l) + R^(l+1) */
-        oracle_haar_synthesis(hs[l - 1], ws[l - 1], U, Rn);                /* A^T(...), cropped */
+            for (int e = 0; e < n; ++e) U[e] += Rn[e];                     /* onto the LL band */
+        oracle_haar_synthesis(hs[l - 1], ws[l - 1], U, Rn);                /* one level up, cropped */
         have_r = 1;
     }
     if (have_r) memcpy(R, Rn, sizeof(double) * (size_t)H * W);
@@ -244,9 +250,17 @@ int oracle_cascade_synthesis(int H, int W, int L, const double* z, double* R)
 }
 
 /*
- * Forward pass of one plane, Alg. 1 exactly as written.
- *   w0: k*k base kernel, s0: base scale, b0: base bias (Alg. 1's return line:
- *       the bias is added to the base convolution before the scale),
+ * Forward pass of one plane (the operator of Alg. 1), built from its four
+ * parts in turn, each materialised in full:
+ *   1. the unfiltered Haar pyramid Y_1..Y_L of x (oracle_plane_pyramid: each
+ *      level analyses the raw low-pass band of the level above);
+ *   2. every band of every level correlated with its own kernel and
+ *      multiplied by its own scale, giving Z_1..Z_L;
+ *   3. the synthesis cascade of Z_1..Z_L back to the pixel grid (R);
+ *   4. the base path s0 * (x (*) W0 + b0), to which R is added.
+ * Arguments:
+ *   w0: k*k base kernel, s0: base scale, b0: base bias (added to the base
+ *       correlation before the scale multiplies it),
  *   wl: L x 4 x k*k level kernels of this channel (row q of level l is
  *       convolution channel 4c+q), sl: L x 4 level scales,
  *   y: H x W output,
@@ -261,41 +275,41 @@ int oracle_plane_forward(int H, int W, int k, int L, const double* x, const doub
     level_sizes(H, W, L, hs, ws);
     const int kk = k * k;
     const long npyr = oracle_pyramid_size(H, W, L);
-    double* Z = (double*)malloc(sizeof(double) * (size_t)(npyr > 0 ? npyr : 1));
-    double* Yl = (double*)malloc(sizeof(double) * 4 * (size_t)H * W + 8);
-    double* carrier = (double*)malloc(sizeof(double) * (size_t)H * W);
+    const size_t pyr_bytes = sizeof(double) * (size_t)(npyr > 0 ? npyr : 1);
+    double* Y = (double*)malloc(pyr_bytes);
+    double* Z = (double*)malloc(pyr_bytes);
     double* R = (double*)malloc(sizeof(double) * (size_t)H * W);
-    if (!Z || !Yl || !carrier || !R) {
-        free(Z); free(Yl); free(carrier); free(R);
+    if (!Y || !Z || !R) {
+        free(Y); free(Z); free(R);
         return 2;
     }
 
-    /* downward: decompose and filter */
-    memcpy(carrier, x, sizeof(double) * (size_t)H * W);
+    /* 1. analysis pyramid */
+    int rc = oracle_plane_pyramid(H, W, L, x, Y);
+
+    /* 2. each band filtered by its kernel, then scaled */
     long off = 0;
-    for (int l = 1; l <= L; ++l) {
+    for (int l = 1; l <= L && rc == 0; ++l) {
         const int n = hs[l] * ws[l];
-        oracle_haar_analysis(hs[l - 1], ws[l - 1], carrier, Yl);          /* Y = A X */
         for (int q = 0; q < 4; ++q) {
-            double* zq = Z + off + (long)q * n;
-            oracle_corr_same(hs[l], ws[l], k, Yl + (long)q * n, wl + ((long)(l - 1) * 4 + q) * kk, zq);
+            const long band = off + (long)q * n;
+            oracle_corr_same(hs[l], ws[l], k, Y + band, wl + ((long)(l - 1) * 4 + q) * kk, Z + band);
             const double s = sl[(l - 1) * 4 + q];
-            for (int e = 0; e < n; ++e) zq[e] *= s;                        /* Z = s (Y * W) */
+            for (int e = 0; e < n; ++e) Z[band + e] *= s;
         }
-        memcpy(carrier, Yl, sizeof(double) * (size_t)n);                   /* X = raw LL */
         off += 4L * n;
     }
 
-    /* upward: reconstruct and accumulate */
-    int rc = oracle_cascade_synthesis(H, W, L, Z, R);
+    /* 3. synthesis of the filtered pyramid */
+    if (rc == 0) rc = oracle_cascade_synthesis(H, W, L, Z, R);
 
-    /* base path plus reconstruction */
+    /* 4. base path, plus the wavelet branch */
     if (rc == 0) {
         oracle_corr_same(H, W, k, x, w0, y);
         for (long e = 0; e < (long)H * W; ++e) y[e] = s0 * (y[e] + b0) + R[e];
         if (z_out && npyr > 0) memcpy(z_out, Z, sizeof(double) * (size_t)npyr);
     }
-    free(Z); free(Yl); free(carrier); free(R);
+    free(Y); free(Z); free(R);
     return rc;
 }
 

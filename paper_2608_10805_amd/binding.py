@@ -87,6 +87,15 @@ def make_desc(B, C, H, W, k, L, dtype=WTCONV_F32) -> Desc:
     return Desc(int(B), int(C), int(H), int(W), int(k), int(L), int(dtype))
 
 
+def _level_lists(desc, **lists):
+    """The C entry points read desc.L pointers from each host array: every
+    list must hold exactly that many (an L = 0 problem may pass None)."""
+    for name, v in lists.items():
+        n = 0 if v is None else len(v)
+        if n != desc.L:
+            raise ValueError(f"{name} has {n} entries but the descriptor has L = {desc.L}")
+
+
 def _ptr_array(ptrs):
     n = max(len(ptrs), 1)
     arr = (ctypes.c_void_p * n)(*([ctypes.c_void_p(p) for p in ptrs] or [None]))
@@ -104,7 +113,8 @@ def wtconv_forward_workspace_bytes(desc: Desc) -> int:
 def wtconv_forward(desc: Desc, x, base_w, base_scale, base_bias, level_w, level_scale, y, workspace,
                    workspace_bytes, stream) -> int:
     """Raw call: pointers are integers (device addresses, base_bias may be None);
-    level_* are lists of addresses."""
+    level_* are lists of desc.L addresses."""
+    _level_lists(desc, level_w=level_w, level_scale=level_scale)
     return load().wtconv_forward(ctypes.byref(desc), x, base_w, base_scale, base_bias, _ptr_array(level_w),
                                  _ptr_array(level_scale), y, workspace, ctypes.c_size_t(workspace_bytes), stream)
 
@@ -115,6 +125,7 @@ def wtconv_backward_workspace_bytes(desc: Desc) -> int:
 
 def wtconv_backward(desc: Desc, x, dy, base_w, base_scale, base_bias, level_w, level_scale, dx, d_base_w,
                     d_base_scale, d_base_bias, d_level_w, d_level_scale, workspace, workspace_bytes, stream) -> int:
+    _level_lists(desc, level_w=level_w, level_scale=level_scale, d_level_w=d_level_w, d_level_scale=d_level_scale)
     return load().wtconv_backward(ctypes.byref(desc), x, dy, base_w, base_scale, base_bias, _ptr_array(level_w),
                                   _ptr_array(level_scale), dx, d_base_w, d_base_scale, d_base_bias,
                                   _ptr_array(d_level_w), _ptr_array(d_level_scale), workspace,
@@ -123,6 +134,7 @@ def wtconv_backward(desc: Desc, x, dy, base_w, base_scale, base_bias, level_w, l
 
 def wtconv_backward_partials(desc: Desc, x, dy, base_w, base_scale, level_w, level_scale, dx, workspace,
                              workspace_bytes, stream) -> int:
+    _level_lists(desc, level_w=level_w, level_scale=level_scale)
     return load().wtconv_backward_partials(ctypes.byref(desc), x, dy, base_w, base_scale, _ptr_array(level_w),
                                            _ptr_array(level_scale), dx, workspace,
                                            ctypes.c_size_t(workspace_bytes), stream)
@@ -131,6 +143,7 @@ def wtconv_backward_partials(desc: Desc, x, dy, base_w, base_scale, level_w, lev
 def wtconv_backward_finalize(desc: Desc, base_w, base_scale, base_bias, level_w, level_scale, d_base_w,
                              d_base_scale, d_base_bias, d_level_w, d_level_scale, workspace, workspace_bytes,
                              stream) -> int:
+    _level_lists(desc, level_w=level_w, level_scale=level_scale, d_level_w=d_level_w, d_level_scale=d_level_scale)
     return load().wtconv_backward_finalize(ctypes.byref(desc), base_w, base_scale, base_bias, _ptr_array(level_w),
                                            _ptr_array(level_scale), d_base_w, d_base_scale, d_base_bias,
                                            _ptr_array(d_level_w), _ptr_array(d_level_scale), workspace,
@@ -143,6 +156,7 @@ def wtconv_backward_data_workspace_bytes(desc: Desc) -> int:
 
 def wtconv_backward_data(desc: Desc, dy, base_w, base_scale, level_w, level_scale, dx, workspace, workspace_bytes,
                          stream) -> int:
+    _level_lists(desc, level_w=level_w, level_scale=level_scale)
     return load().wtconv_backward_data(ctypes.byref(desc), dy, base_w, base_scale, _ptr_array(level_w),
                                        _ptr_array(level_scale), dx, workspace, ctypes.c_size_t(workspace_bytes),
                                        stream)
@@ -161,14 +175,71 @@ def _dtype_code(t):
     return {torch.float32: WTCONV_F32, torch.bfloat16: WTCONV_BF16, torch.float16: WTCONV_F16}[t.dtype]
 
 
-def _require(t, name, dtype=None):
+def _require(t, name, dtype=None, shape=None, device=None, on_gpu=True):
     import torch
-    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+    if not isinstance(t, torch.Tensor):
+        raise ValueError(f"{name} must be a tensor")
+    if on_gpu and not t.is_cuda:
         raise ValueError(f"{name} must be a GPU tensor")
+    if device is not None and t.device != device:
+        raise ValueError(f"{name} is on {t.device}, expected {device}")
     if not t.is_contiguous():
         raise ValueError(f"{name} must be contiguous")
     if dtype is not None and t.dtype != dtype:
         raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+
+
+def validate(x, base_w, base_scale, level_w, level_scale, bias=None, out=None, dy=None, on_gpu=True):
+    """Check every tensor the entry points receive against the problem x
+    defines, before anything reaches the library (which sees only pointers
+    and the descriptor): x [B,C,H,W] in fp32 / bf16 / fp16; base_w [C,k,k]
+    with k odd; base_scale (and bias, if given) [C]; level_w and level_scale
+    lists of the same length L <= 8 holding [4C,k,k] and [4C]; parameters
+    fp32; out and dy (if given) of x's shape and dtype; everything contiguous
+    and on x's device. Raises ValueError; returns (B, C, H, W, k, L)."""
+    import torch
+    _require(x, "x", on_gpu=on_gpu)
+    if x.dtype not in (torch.float32, torch.bfloat16, torch.float16):
+        raise ValueError(f"x must be float32, bfloat16 or float16, got {x.dtype}")
+    if x.dim() != 4:
+        raise ValueError(f"x must be [B, C, H, W], got shape {tuple(x.shape)}")
+    B, C, H, W = x.shape
+    if min(B, C, H, W) < 1:
+        raise ValueError(f"x has an empty dimension: {tuple(x.shape)}")
+    dev = x.device
+    if not isinstance(base_w, torch.Tensor) or base_w.dim() != 3 or base_w.shape[1] != base_w.shape[2]:
+        raise ValueError("base_w must be a [C, k, k] tensor")
+    k = base_w.shape[-1]
+    if k % 2 == 0:
+        raise ValueError(f"the kernel size must be odd, got {k}")
+    f32 = torch.float32
+    _require(base_w, "base_w", f32, (C, k, k), dev, on_gpu)
+    _require(base_scale, "base_scale", f32, (C,), dev, on_gpu)
+    if bias is not None:
+        _require(bias, "bias", f32, (C,), dev, on_gpu)
+    level_w, level_scale = list(level_w), list(level_scale)
+    if len(level_w) != len(level_scale):
+        raise ValueError(f"level_w has {len(level_w)} levels but level_scale has {len(level_scale)}")
+    if len(level_w) > MAX_LEVELS:
+        raise ValueError(f"at most {MAX_LEVELS} levels, got {len(level_w)}")
+    for i, (w, sc) in enumerate(zip(level_w, level_scale)):
+        _require(w, f"level_w[{i}]", f32, (4 * C, k, k), dev, on_gpu)
+        _require(sc, f"level_scale[{i}]", f32, (4 * C,), dev, on_gpu)
+    if out is not None:
+        _require(out, "out", x.dtype, x.shape, dev, on_gpu)
+    if dy is not None:
+        _require(dy, "dy", x.dtype, x.shape, dev, on_gpu)
+    return B, C, H, W, k, len(level_w)
+
+
+def _workspace_ok(ws, nbytes, device):
+    """A caller-provided workspace is used only if it is a contiguous device
+    tensor on the problem's device with at least nbytes bytes."""
+    import torch
+    return (isinstance(ws, torch.Tensor) and ws.device == device and ws.is_contiguous()
+            and ws.numel() * ws.element_size() >= nbytes)
 
 
 def _stream(device):
@@ -182,21 +253,13 @@ def forward(x, base_w, base_scale, level_w, level_scale, out=None, workspace=Non
     bias: the base bias [C] (fp32) or None.
     Large planes need a device workspace; one is allocated if `workspace` is None or too small."""
     import torch
-    _require(x, "x")
-    B, C, H, W = x.shape
-    k = base_w.shape[-1]
-    L = len(level_w)
-    for name, t in [("base_w", base_w), ("base_scale", base_scale)] + \
-            [(f"level_w[{i}]", t) for i, t in enumerate(level_w)] + \
-            [(f"level_scale[{i}]", t) for i, t in enumerate(level_scale)] + \
-            ([("bias", bias)] if bias is not None else []):
-        _require(t, name, torch.float32)
+    B, C, H, W, k, L = validate(x, base_w, base_scale, level_w, level_scale, bias=bias, out=out)
     y = torch.empty_like(x) if out is None else out
     desc = make_desc(B, C, H, W, k, L, _dtype_code(x))
     nbytes = wtconv_forward_workspace_bytes(desc)
     ws_ptr = None
     if nbytes:
-        if workspace is None or workspace.numel() * workspace.element_size() < nbytes:
+        if not _workspace_ok(workspace, nbytes, x.device):
             workspace = torch.empty(nbytes, dtype=torch.uint8, device=x.device)
         ws_ptr = workspace.data_ptr()
     _check(wtconv_forward(desc, x.data_ptr(), base_w.data_ptr(), base_scale.data_ptr(),
@@ -211,16 +274,12 @@ def backward(x, dy, base_w, base_scale, level_w, level_scale, need_dx=True, work
     """Gradients of sum(y * dy). Returns (dx or None, d_base_w, d_base_scale, [d_level_w], [d_level_scale]),
     followed by d_bias when need_dbias. `bias` (the base bias [C] or None) enters d_base_scale."""
     import torch
-    _require(x, "x")
-    _require(dy, "dy", x.dtype)
-    B, C, H, W = x.shape
-    k = base_w.shape[-1]
-    L = len(level_w)
+    B, C, H, W, k, L = validate(x, base_w, base_scale, level_w, level_scale, bias=bias, dy=dy)
     desc = make_desc(B, C, H, W, k, L, _dtype_code(x))
     nbytes = wtconv_backward_workspace_bytes(desc)
     if nbytes == 0:
         raise WTConvError(8, "no backward plan for this shape")
-    if workspace is None or workspace.numel() * workspace.element_size() < nbytes:
+    if not _workspace_ok(workspace, nbytes, x.device):
         workspace = torch.empty(nbytes, dtype=torch.uint8, device=x.device)
     dx = torch.empty_like(x) if need_dx else None
     dbw = torch.empty_like(base_w)
@@ -228,8 +287,6 @@ def backward(x, dy, base_w, base_scale, level_w, level_scale, need_dx=True, work
     dlw = [torch.empty_like(t) for t in level_w]
     dls = [torch.empty_like(t) for t in level_scale]
     dbb = torch.empty_like(base_scale) if need_dbias else None
-    if bias is not None:
-        _require(bias, "bias", torch.float32)
     _check(wtconv_backward(desc, x.data_ptr(), dy.data_ptr(), base_w.data_ptr(), base_scale.data_ptr(),
                            bias.data_ptr() if bias is not None else None,
                            [t.data_ptr() for t in level_w], [t.data_ptr() for t in level_scale],
@@ -245,14 +302,13 @@ def backward(x, dy, base_w, base_scale, level_w, level_scale, need_dx=True, work
 def backward_data(dy, base_w, base_scale, level_w, level_scale, out=None, workspace=None):
     """dx alone (wtconv_backward_data): the forward pass on dy with rotated kernels."""
     import torch
-    _require(dy, "dy")
-    B, C, H, W = dy.shape
-    desc = make_desc(B, C, H, W, base_w.shape[-1], len(level_w), _dtype_code(dy))
+    B, C, H, W, k, L = validate(dy, base_w, base_scale, level_w, level_scale, out=out)
+    desc = make_desc(B, C, H, W, k, L, _dtype_code(dy))
     dx = torch.empty_like(dy) if out is None else out
     nbytes = wtconv_backward_data_workspace_bytes(desc)
     ws_ptr = None
     if nbytes:
-        if workspace is None or workspace.numel() * workspace.element_size() < nbytes:
+        if not _workspace_ok(workspace, nbytes, dy.device):
             workspace = torch.empty(nbytes, dtype=torch.uint8, device=dy.device)
         ws_ptr = workspace.data_ptr()
     _check(wtconv_backward_data(desc, dy.data_ptr(), base_w.data_ptr(), base_scale.data_ptr(),
@@ -267,8 +323,9 @@ class Backward:
 
     def __init__(self, x, base_w, base_scale, level_w, level_scale, need_dx=True):
         import torch
-        B, C, H, W = x.shape
-        self.desc = make_desc(B, C, H, W, base_w.shape[-1], len(level_w), _dtype_code(x))
+        B, C, H, W, k, L = validate(x, base_w, base_scale, level_w, level_scale)
+        self.desc = make_desc(B, C, H, W, k, L, _dtype_code(x))
+        self.x_like = (tuple(x.shape), x.dtype, x.device)
         self.nbytes = wtconv_backward_workspace_bytes(self.desc)
         if self.nbytes == 0:
             raise WTConvError(8, "no backward plan for this shape")
@@ -287,9 +344,18 @@ class Backward:
         self.data_nbytes = wtconv_backward_data_workspace_bytes(self.desc)
         self.data_workspace = None
 
+    def _check_act(self, name, t):
+        shape, dtype, device = self.x_like
+        _require(t, name, dtype, shape, device)
+
     def partials(self, x, dy, dx=None):
+        """Writes dx into `dx`, else into the preallocated buffer when the
+        object was made with need_dx, else skips it."""
         bw, bs, _, _ = self.params
         out = dx if dx is not None else self.dx
+        for name, t in (("x", x), ("dy", dy), ("dx", out)):
+            if t is not None:
+                self._check_act(name, t)
         _check(wtconv_backward_partials(self.desc, x.data_ptr(), dy.data_ptr(), bw.data_ptr(), bs.data_ptr(),
                                         self._lw, self._ls, out.data_ptr() if out is not None else None,
                                         self.workspace.data_ptr(), self.nbytes, _stream(self.device)))
@@ -297,6 +363,8 @@ class Backward:
     def data(self, dy, dx):
         """dx alone (wtconv_backward_data) into `dx`."""
         bw, bs, _, _ = self.params
+        self._check_act("dy", dy)
+        self._check_act("dx", dx)
         if self.data_nbytes and self.data_workspace is None:
             import torch
             self.data_workspace = torch.empty(self.data_nbytes, dtype=torch.uint8, device=self.device)
