@@ -39,14 +39,16 @@
  *   - level_w / level_scale (and their gradients) are HOST arrays of L DEVICE
  *     pointers: level_w[l-1] -> [4C][k][k], level_scale[l-1] -> [4C].
  *   - The caller owns every buffer. The library allocates no device memory;
- *     scratch space comes from a caller-provided workspace.
+ *     scratch space comes from a caller-provided workspace (or, for
+ *     wtconv_backward_noalloc, from a static device array in the library).
  *   - Work is enqueued on `stream` and is asynchronous. Argument errors are
  *     detected on the host before any HIP call and returned synchronously;
  *     launch errors are returned as WTCONV_ERR_HIP; device faults surface at
  *     the caller's next synchronisation.
  *   - Gradient outputs are overwritten, not accumulated into.
- *   - Entry points are reentrant; the library keeps no mutable global state.
- *     Results are bitwise reproducible for identical inputs and shapes.
+ *   - Entry points are reentrant; the library's only global state is the
+ *     static scratch of wtconv_backward_noalloc (see there). Results are
+ *     bitwise reproducible for identical inputs and shapes.
  *   - Supported: B, C, H, W >= 1; k in {1, 3, 5, 7}; 0 <= L <= 8. Planes whose
  *     fused working set fits one compute unit's 160 KB of LDS (float32, k = 5:
  *     forward up to about 120 x 120 pixels, backward up to about 112 x 112, or
@@ -82,7 +84,9 @@ typedef enum {
     WTCONV_ERR_ALIAS = 6,       /* an output overlaps an input or another output  */
     WTCONV_ERR_WORKSPACE = 7,   /* workspace NULL or smaller than required        */
     WTCONV_ERR_UNSUPPORTED = 8, /* no execution plan for this shape               */
-    WTCONV_ERR_HIP = 9          /* a HIP runtime call or kernel launch failed     */
+    WTCONV_ERR_HIP = 9,         /* a HIP runtime call or kernel launch failed     */
+    WTCONV_ERR_SCRATCH = 10     /* wtconv_backward_noalloc: the problem needs more
+                                   workspace than WTCONV_NOALLOC_SCRATCH_BYTES     */
 } wtconv_status;
 
 /* Problem descriptor (host memory). */
@@ -200,6 +204,32 @@ wtconv_status wtconv_backward_data(const wtconv_desc* desc, const void* dy, cons
                                    const float* base_scale, const float* const* level_w,
                                    const float* const* level_scale, void* dx, void* workspace,
                                    size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * wtconv_backward without a workspace argument, for callers that cannot
+ * allocate device memory: code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation. Same arguments, checks, kernels and
+ * results as wtconv_backward; the workspace is a static device array of
+ * WTCONV_NOALLOC_SCRATCH_BYTES inside the library (one per GPU it runs on,
+ * held until the process ends), so the call allocates nothing.
+ *   Returns WTCONV_ERR_SCRATCH, before any HIP call, when
+ *   wtconv_backward_workspace_bytes(desc) exceeds that size (it covers every
+ *   ConvNeXt-T stage shape at B = 128, L <= 5; large planes split into
+ *   carriers and exceed it).
+ *   The array is shared by every call on one GPU and keeps the last call's
+ *   contents (each call overwrites what it reads): calls that overlap on one
+ *   GPU, e.g. on two streams at once, race and must be ordered by the caller.
+ *   The device is the one `stream` belongs to; the array's address there is
+ *   looked up on the first call on that device.
+ */
+#define WTCONV_NOALLOC_SCRATCH_BYTES ((size_t)32 << 20)
+
+wtconv_status wtconv_backward_noalloc(const wtconv_desc* desc, const void* x, const void* dy,
+                                      const float* base_w, const float* base_scale, const float* base_bias,
+                                      const float* const* level_w, const float* const* level_scale,
+                                      void* dx, float* d_base_w, float* d_base_scale, float* d_base_bias,
+                                      float* const* d_level_w, float* const* d_level_scale,
+                                      hipStream_t stream);
 
 /* Static, human-readable name of a status code. */
 const char* wtconv_status_string(wtconv_status status);

@@ -15,11 +15,12 @@ WTCONV_F32, WTCONV_BF16, WTCONV_F16 = 0, 1, 2
 STATUS = {
     0: "WTCONV_OK", 1: "WTCONV_ERR_NULL", 2: "WTCONV_ERR_SHAPE", 3: "WTCONV_ERR_KSIZE",
     4: "WTCONV_ERR_LEVELS", 5: "WTCONV_ERR_DTYPE", 6: "WTCONV_ERR_ALIAS", 7: "WTCONV_ERR_WORKSPACE",
-    8: "WTCONV_ERR_UNSUPPORTED", 9: "WTCONV_ERR_HIP",
+    8: "WTCONV_ERR_UNSUPPORTED", 9: "WTCONV_ERR_HIP", 10: "WTCONV_ERR_SCRATCH",
 }
 EXPORTS = ["wtconv_forward_workspace_bytes", "wtconv_forward", "wtconv_backward", "wtconv_backward_workspace_bytes",
            "wtconv_backward_partials", "wtconv_backward_finalize", "wtconv_backward_data_workspace_bytes",
-           "wtconv_backward_data", "wtconv_status_string", "wtconv_version"]
+           "wtconv_backward_data", "wtconv_backward_noalloc", "wtconv_status_string", "wtconv_version"]
+NOALLOC_SCRATCH_BYTES = 32 << 20  # WTCONV_NOALLOC_SCRATCH_BYTES
 MAX_LEVELS = 8
 
 
@@ -67,6 +68,9 @@ def load():
     lib.wtconv_backward_data_workspace_bytes.restype = ctypes.c_size_t
     lib.wtconv_backward_data.argtypes = [ctypes.POINTER(Desc), _P, _P, _P, _PP, _PP, _P, _P, ctypes.c_size_t, _P]
     lib.wtconv_backward_data.restype = ctypes.c_int
+    lib.wtconv_backward_noalloc.argtypes = [ctypes.POINTER(Desc), _P, _P, _P, _P, _P, _PP, _PP, _P, _P, _P, _P,
+                                            _PP, _PP, _P]
+    lib.wtconv_backward_noalloc.restype = ctypes.c_int
     lib.wtconv_status_string.argtypes = [ctypes.c_int]
     lib.wtconv_status_string.restype = ctypes.c_char_p
     lib.wtconv_version.restype = ctypes.c_int
@@ -130,6 +134,15 @@ def wtconv_backward(desc: Desc, x, dy, base_w, base_scale, base_bias, level_w, l
                                   _ptr_array(level_scale), dx, d_base_w, d_base_scale, d_base_bias,
                                   _ptr_array(d_level_w), _ptr_array(d_level_scale), workspace,
                                   ctypes.c_size_t(workspace_bytes), stream)
+
+
+def wtconv_backward_noalloc(desc: Desc, x, dy, base_w, base_scale, base_bias, level_w, level_scale, dx, d_base_w,
+                            d_base_scale, d_base_bias, d_level_w, d_level_scale, stream) -> int:
+    """wtconv_backward with the library's static scratch as its workspace."""
+    _level_lists(desc, level_w=level_w, level_scale=level_scale, d_level_w=d_level_w, d_level_scale=d_level_scale)
+    return load().wtconv_backward_noalloc(ctypes.byref(desc), x, dy, base_w, base_scale, base_bias,
+                                          _ptr_array(level_w), _ptr_array(level_scale), dx, d_base_w, d_base_scale,
+                                          d_base_bias, _ptr_array(d_level_w), _ptr_array(d_level_scale), stream)
 
 
 def wtconv_backward_partials(desc: Desc, x, dy, base_w, base_scale, level_w, level_scale, dx, workspace,

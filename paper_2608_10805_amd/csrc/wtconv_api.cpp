@@ -1064,6 +1064,8 @@ const char* wtconv_status_string(wtconv_status s)
         case WTCONV_ERR_WORKSPACE: return "workspace missing, misaligned or too small";
         case WTCONV_ERR_UNSUPPORTED: return "no execution plan for this shape";
         case WTCONV_ERR_HIP: return "HIP runtime error";
+        case WTCONV_ERR_SCRATCH: return "the problem needs more workspace than the static scratch of "
+                                        "wtconv_backward_noalloc holds";
     }
     return "unknown status";
 }

@@ -34,7 +34,7 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_status_strings():
-    for code in range(10):
+    for code in range(11):
         s = binding.status_string(code)
         assert isinstance(s, str) and s
     assert binding.status_string(0) == "ok"
@@ -193,3 +193,35 @@ def test_backward_data_checks():
 
 def test_descriptor_layout_matches_header():
     assert ctypes.sizeof(Desc) == 7 * 4
+
+
+def noalloc(desc, L=None):
+    L = desc.L if L is None else L
+    lib = binding.load()
+    ptrs = lambda base: binding._ptr_array([base + 64 * i for i in range(L)])  # noqa: E731
+    return lib.wtconv_backward_noalloc(ctypes.byref(desc) if desc is not None else None, FAKE, FAKE + (1 << 36),
+                                       FAKE + 4096, FAKE + 8192, None, ptrs(FAKE + 16384), ptrs(FAKE + 32768),
+                                       FAKE + (2 << 36), FAKE + (3 << 36), FAKE + (3 << 36) + 65536, None,
+                                       ptrs(FAKE + (4 << 36)), ptrs(FAKE + (5 << 36)), None)
+
+
+def test_noalloc_rejects_problems_beyond_its_scratch_before_any_hip_call():
+    # 224 x 224 planes at L = 3 split into carriers: about 148 MiB of workspace
+    d = make_desc(16, 64, 224, 224, 5, 3)
+    assert binding.wtconv_backward_workspace_bytes(d) > binding.NOALLOC_SCRATCH_BYTES
+    assert noalloc(d) == 10
+    assert binding.status_string(10).startswith("the problem needs more workspace")
+
+
+@pytest.mark.parametrize("shape,code", [((0, 1, 8, 8, 5, 1), 2), ((1, 1, 8, 8, 4, 1), 3), ((1, 1, 8, 8, 5, 9), 4)])
+def test_noalloc_reports_descriptor_errors(shape, code):
+    assert noalloc(make_desc(*shape), L=max(0, min(shape[5], 8))) == code
+
+
+def test_noalloc_scratch_covers_the_convnext_stage_shapes():
+    """Every ConvNeXt-T stage shape at B = 128, L = 1..5, fits the static scratch."""
+    for (C, H) in [(96, 56), (192, 28), (384, 14), (768, 7)]:
+        for L in range(1, 6):
+            for dt in (0, 1):
+                n = binding.wtconv_backward_workspace_bytes(make_desc(128, C, H, H, 5, L, dt))
+                assert 0 < n <= binding.NOALLOC_SCRATCH_BYTES, (C, H, L, dt, n)
