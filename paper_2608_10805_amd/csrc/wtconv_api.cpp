@@ -148,13 +148,16 @@ bool single_round(const wtconv_desc& d, int PP, const PlaneGeom& g)
 }
 
 // Workgroups (4 wavefronts) per CU that the forward kernel's registers allow:
-// 512 registers per SIMD lane over its VGPR count as compiled for gfx950
-// (single round: 55 / 63-68 / 100-103 / 147-148 for k = 1 / 3 / 5 / 7;
-// general: 123 / 137 / 148-149 / 173). A planning estimate only.
-int forward_wgs_by_regs(int k, bool one)
+// 512 registers per SIMD lane over the kernel's VGPR count, queried from the
+// HIP runtime for the compiled kernel. Without a device to ask, the counts of
+// one gfx950 build stand in (single round: 55 / 63-68 / 100-103 / 147-148
+// VGPRs for k = 1 / 3 / 5 / 7; general: 123 / 137 / 148-149 / 173); the
+// forward workspace size does not depend on this choice.
+int forward_wgs(const wtconv_desc& d, bool one)
 {
-    if (one) return k <= 1 ? 8 : (k <= 3 ? 7 : (k <= 5 ? 4 : 3));
-    return k <= 1 ? 4 : (k <= 5 ? 3 : 2);
+    const int k = d.k;
+    const int fallback = one ? (k <= 1 ? 8 : (k <= 3 ? 7 : (k <= 5 ? 4 : 3))) : (k <= 1 ? 4 : (k <= 5 ? 3 : 2));
+    return wtc::forward_wgs_by_regs(k, d.dtype, one, fallback);
 }
 
 // Lane use of one workgroup's output-tile rounds with PP resident planes.
@@ -203,7 +206,7 @@ bool make_plan(const wtconv_desc& d, bool bwd, Plan& pl)
                 const int lds = lds_floats_for(d, bwd, pp, g);
                 if (lds > kLdsFloatsMax) continue;
                 const bool one = single_round(d, pp, g);
-                const int wgs = std::min(forward_wgs_by_regs(d.k, one), kLdsFloatsMax / lds);
+                const int wgs = std::min(forward_wgs(d, one), kLdsFloatsMax / lds);
                 const double score = tile_use(g, pp) * wgs * (one ? 1.0 : 0.75);
                 if (score >= best) {
                     best = score;

@@ -1027,8 +1027,8 @@ template <int K, typename ST, bool BWD, bool ONE, bool RGN>
 hipError_t launch_variant(const FusedArgs& a, int grid, hipStream_t s)
 {
     const size_t bytes = (size_t)a.lds_floats * sizeof(float);
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&fused_kernel<K, ST, BWD, ONE, RGN>),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
+    static std::atomic<unsigned long long> lds_done{0};
+    const hipError_t e = allow_full_lds(reinterpret_cast<const void*>(&fused_kernel<K, ST, BWD, ONE, RGN>), lds_done);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL((fused_kernel<K, ST, BWD, ONE, RGN>), dim3(grid), dim3(kThreads), bytes, s, a);
     return hipGetLastError();

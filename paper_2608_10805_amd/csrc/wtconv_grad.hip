@@ -394,8 +394,8 @@ template <int K, typename ST, bool MR>
 hipError_t launch_grad_v(const GradArgs& a, int grid, hipStream_t s)
 {
     const size_t bytes = (size_t)a.lds_floats * sizeof(float);
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&grad_kernel<K, ST, MR>),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
+    static std::atomic<unsigned long long> lds_done{0};
+    const hipError_t e = allow_full_lds(reinterpret_cast<const void*>(&grad_kernel<K, ST, MR>), lds_done);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL((grad_kernel<K, ST, MR>), dim3(grid), dim3(kThreads), bytes, s, a);
     return hipGetLastError();

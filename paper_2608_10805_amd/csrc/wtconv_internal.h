@@ -2,11 +2,55 @@
 // gfx950 kernels (wtconv_kernels.hip). Not part of the public ABI.
 #pragma once
 
+#include <algorithm>
+#include <atomic>
+
 #include <hip/hip_runtime.h>
 
 #include "wtconv.h"
 
 namespace wtc {
+
+constexpr int kLdsBytesMax = 160 * 1024;  // one compute unit's LDS
+
+// Lets kernel `fn` launch with up to a whole compute unit's LDS, on the
+// current device. The attribute persists for the process, so it is set once
+// per (kernel, device): `done` is the calling kernel's own set of devices
+// (bit d for device d < 64; larger ids set it on every launch). Two threads
+// racing both set it, which is harmless.
+inline hipError_t allow_full_lds(const void* fn, std::atomic<unsigned long long>& done)
+{
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    const unsigned long long bit = (dev >= 0 && dev < 64) ? 1ull << dev : 0ull;
+    if (bit && (done.load(std::memory_order_relaxed) & bit)) return hipSuccess;
+    e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, kLdsBytesMax);
+    if (e == hipSuccess && bit) done.fetch_or(bit, std::memory_order_relaxed);
+    return e;
+}
+
+// Workgroups per compute unit that a 256-thread kernel's registers allow, from
+// its compiled VGPR count (512 per SIMD lane, allocated in blocks of 8, at
+// most 8 wavefronts per SIMD), or `fallback` if the HIP runtime cannot report
+// it (no device). The answer is cached in `cache` (0: not asked yet, -1: the
+// runtime could not tell).
+inline int wgs_by_regs(const void* fn, std::atomic<int>& cache, int fallback)
+{
+    int v = cache.load(std::memory_order_relaxed);
+    if (v > 0) return v;
+    if (v < 0) return fallback;
+    hipFuncAttributes attr;
+    if (hipFuncGetAttributes(&attr, fn) != hipSuccess || attr.numRegs <= 0) {
+        (void)hipGetLastError();  // clear the error state left by a failed query
+        cache.store(-1, std::memory_order_relaxed);
+        return fallback;
+    }
+    const int regs = (attr.numRegs + 7) / 8 * 8;
+    v = std::max(1, std::min(8, 512 / regs));
+    cache.store(v, std::memory_order_relaxed);
+    return v;
+}
 
 constexpr int kMaxLevels = WTCONV_MAX_LEVELS;
 constexpr int kThreads = 256;  // 4 wavefronts of 64 lanes per workgroup
@@ -161,6 +205,9 @@ struct GradArgs {
 __host__ __device__ inline int partial_floats_per_channel(int k, int L) { return k * k * (1 + 4 * L) + 1; }
 
 hipError_t launch_forward(int k, wtconv_dtype dt, const FusedArgs& a, int grid, hipStream_t s);
+// Workgroups per CU that the registers of the forward kernel for (k, dt,
+// single-round variant) allow; `fallback` if the runtime cannot tell.
+int forward_wgs_by_regs(int k, wtconv_dtype dt, bool one, int fallback);
 hipError_t launch_backward(int k, wtconv_dtype dt, const FusedArgs& a, int grid, hipStream_t s);
 hipError_t launch_reduce(const ReduceArgs& a, hipStream_t s);
 hipError_t launch_grad(int k, wtconv_dtype dt, const GradArgs& a, int grid, hipStream_t s);

@@ -549,8 +549,8 @@ template <int K, typename ST, bool BWD>
 hipError_t launch_tiny_variant(const TinyArgs& a, hipStream_t s)
 {
     const size_t bytes = tiny_lds_bytes(K, a.L, BWD);
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&tiny_kernel<K, ST, BWD>),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
+    static std::atomic<unsigned long long> lds_done{0};
+    const hipError_t e = allow_full_lds(reinterpret_cast<const void*>(&tiny_kernel<K, ST, BWD>), lds_done);
     if (e != hipSuccess) return e;
     const int grid = ((a.C + 3) / 4) * ((a.B + 63) / 64);
     hipLaunchKernelGGL((tiny_kernel<K, ST, BWD>), dim3(grid), dim3(256), bytes, s, a);
