@@ -228,6 +228,14 @@ __global__ void __launch_bounds__(kThreads, grad_waves_per_simd<K>()) grad_kerne
     const int per = g.tiles_x * g.tiles_y;
     for (int b0 = b_begin; b0 < b_end; b0 += a.PP) {
         const int np = min(a.PP, b_end - b0);
+        // Per-thread LDS addresses depend only on the thread index; taking it
+        // through an opaque copy inside this loop keeps the compiler from
+        // hoisting them out of the loop, which would hold them across it next
+        // to the 3 k^2 kernel-gradient sums and spill them (k <= 5; at k = 7
+        // the sums alone nearly fill the registers and hoisting spills less).
+        int tl = threadIdx.x;
+        if constexpr (K <= 5) asm volatile("" : "+v"(tl));
+        const int ll = tl & 63;
         // dy levels 1-2 of one block -> the compact pyramid
         auto dy_levels = [&](const TileIdx& ti, const float (&dyb)[4][4]) {
             float* reg = planes + ti.p * stride;
@@ -264,12 +272,12 @@ __global__ void __launch_bounds__(kThreads, grad_waves_per_simd<K>()) grad_kerne
         };
 
         if constexpr (!MR) {
-            const bool mine = tid < np * per;  // at most one block per thread (planned on the host)
-            const TileIdx ti = tile_at(mine ? tid : 0, per, g.r_tiles, g.tiles_x, g.r_tiles_x, 4);
+            const bool mine = tl < np * per;  // at most one block per thread (planned on the host)
+            const TileIdx ti = tile_at(mine ? tl : 0, per, g.r_tiles, g.tiles_x, g.r_tiles_x, 4);
 
             // 1. x block -> LDS with its levels 1-2; dy block in registers
             if (alias1 && b0 != b_begin)
-                for (int p = 0; p < np; ++p) zero_x_ring(planes + p * stride, g, R, a.r_ring, tid);
+                for (int p = 0; p < np; ++p) zero_x_ring(planes + p * stride, g, R, a.r_ring, tl);
             float dyb[4][4];
             if (mine) {
                 const long plane = (long)(b0 + ti.p) * C + c;
@@ -285,7 +293,7 @@ __global__ void __launch_bounds__(kThreads, grad_waves_per_simd<K>()) grad_kerne
             if (L >= 3) {
                 const LevelGeom& lg = g.lv[3];
                 const LevelGeom& lp = g.lv[2];
-                analysis_level(planes + lp.off, lp.pitch, planes + lg.off, lg, R, np, stride, tid);
+                analysis_level(planes + lp.off, lp.pitch, planes + lg.off, lg, R, np, stride, tl);
             }
             __syncthreads();
 
@@ -297,9 +305,9 @@ __global__ void __launch_bounds__(kThreads, grad_waves_per_simd<K>()) grad_kerne
             // cannot stay in registers across rounds). Every base correlation
             // reads the x plane before the barrier after which dy level 1 may
             // be stored over it.
-            if (alias1 && b0 != b_begin) zero_x_ring(planes, g, R, a.r_ring, tid);
+            if (alias1 && b0 != b_begin) zero_x_ring(planes, g, R, a.r_ring, tl);
             const long plane = (long)b0 * C + c;
-            for (int it = tid; it < per; it += kThreads) {
+            for (int it = tl; it < per; it += kThreads) {
                 const TileIdx ti = tile_at(it, per, g.r_tiles, g.tiles_x, g.r_tiles_x, 4);
                 float v[4][4];
                 fetch_block<ST>(xs + plane * HW, g.H, g.W, ti.j0, ti.i0, vw, v);
@@ -307,7 +315,7 @@ __global__ void __launch_bounds__(kThreads, grad_waves_per_simd<K>()) grad_kerne
             }
             __syncthreads();
             if (!skip_base) {
-                for (int it = tid; it < per; it += kThreads) {
+                for (int it = tl; it < per; it += kThreads) {
                     const TileIdx ti = tile_at(it, per, g.r_tiles, g.tiles_x, g.r_tiles_x, 4);
                     float dyb[4][4];
                     fetch_block<ST>(dys + plane * HW, g.H, g.W, ti.j0, ti.i0, vw, dyb);
@@ -317,10 +325,10 @@ __global__ void __launch_bounds__(kThreads, grad_waves_per_simd<K>()) grad_kerne
             if (L >= 3) {
                 const LevelGeom& lg = g.lv[3];
                 const LevelGeom& lp = g.lv[2];
-                analysis_level(planes + lp.off, lp.pitch, planes + lg.off, lg, R, np, stride, tid);
+                analysis_level(planes + lp.off, lp.pitch, planes + lg.off, lg, R, np, stride, tl);
             }
             __syncthreads();
-            for (int it = tid; it < per; it += kThreads) {
+            for (int it = tl; it < per; it += kThreads) {
                 const TileIdx ti = tile_at(it, per, g.r_tiles, g.tiles_x, g.r_tiles_x, 4);
                 float dyb[4][4];
                 fetch_block<ST>(dys + plane * HW, g.H, g.W, ti.j0, ti.i0, vw, dyb);
@@ -330,7 +338,7 @@ __global__ void __launch_bounds__(kThreads, grad_waves_per_simd<K>()) grad_kerne
         if (L >= 4) {
             const LevelGeom& lg = g.lv[4];
             const LevelGeom& lp = g.lv[3];
-            analysis_level(planes + lp.off, lp.pitch, planes + lg.off, lg, R, np, stride, tid);
+            analysis_level(planes + lp.off, lp.pitch, planes + lg.off, lg, R, np, stride, tl);
         }
         __syncthreads();
 
@@ -339,11 +347,11 @@ __global__ void __launch_bounds__(kThreads, grad_waves_per_simd<K>()) grad_kerne
             LevelGeom dg = g.lv[l];
             dg.pitch = a.dy_pitch[l];
             dg.band = a.dy_band[l];
-            analysis_level(planes + a.dy_off[l - 1], a.dy_pitch[l - 1], planes + a.dy_off[l], dg, 0, np, stride, tid);
+            analysis_level(planes + a.dy_off[l - 1], a.dy_pitch[l - 1], planes + a.dy_off[l], dg, 0, np, stride, tl);
             if (l + 2 <= L) {
                 const LevelGeom& lg = g.lv[l + 2];
                 const LevelGeom& lp = g.lv[l + 1];
-                analysis_level(planes + lp.off, lp.pitch, planes + lg.off, lg, R, np, stride, tid);
+                analysis_level(planes + lp.off, lp.pitch, planes + lg.off, lg, R, np, stride, tl);
             }
             __syncthreads();
         }
@@ -353,11 +361,11 @@ __global__ void __launch_bounds__(kThreads, grad_waves_per_simd<K>()) grad_kerne
             const LevelGeom& xl = g.lv[l];
             const DyLevel dl = {a.dy_off[l], a.dy_pitch[l], a.dy_band[l]};
             if (l == 1)
-                grad_band<K>(planes, stride, xl, dl, q, np, g1, lane);
+                grad_band<K>(planes, stride, xl, dl, q, np, g1, ll);
             else if (l == 2)
-                grad_band<K>(planes, stride, xl, dl, q, np, g2, lane);
+                grad_band<K>(planes, stride, xl, dl, q, np, g2, ll);
             else
-                grad_band_rows<K>(planes, stride, xl, dl, q, np, gco + ((l - 3) * 4 + q) * KK, lane);
+                grad_band_rows<K>(planes, stride, xl, dl, q, np, gco + ((l - 3) * 4 + q) * KK, ll);
         }
         __syncthreads();
     }
