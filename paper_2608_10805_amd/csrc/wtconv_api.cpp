@@ -77,7 +77,11 @@ int pick_tile(int h, int w, int PP, int k, bool bwd, bool one_pref = false)
 
 // Lay out one plane's input array and pyramid for a given number of resident
 // planes. Returns false if a level cannot be tiled within the register caps.
-bool layout(const wtconv_desc& d, int PP, bool bwd, PlaneGeom& g, bool t4_deep = false, bool one_pref = false)
+// rows_from: the first level whose kernel-gradient correlation walks whole
+// rows (the fused backward: 2; the gradient pass: 3, its level 2 goes by tiles);
+// those levels' rows are padded to whole row chunks.
+bool layout(const wtconv_desc& d, int PP, bool bwd, PlaneGeom& g, bool t4_deep = false, bool one_pref = false,
+            int rows_from = 2)
 {
     const int R = d.k / 2;
     memset(&g, 0, sizeof(g));
@@ -102,7 +106,7 @@ bool layout(const wtconv_desc& d, int PP, bool bwd, PlaneGeom& g, bool t4_deep =
         lg.ew = ceil_to(w, lg.T);
         const int rows = R + std::max(lg.eh + R, h + 1);
         int pitch = std::max(lg.ew - lg.T + window_floats(lg.T, R), R + std::max(lg.ew + R, w + 1));
-        if (l >= 2) {  // whole-row chunks of the coarse kernel-gradient pass stay inside the row
+        if (l >= rows_from) {  // whole-row chunks of the coarse kernel-gradient pass stay inside the row
             const int cw = w <= 8 ? 8 : 16;
             pitch = std::max(pitch, ceil_to(w, cw) - cw + ceil_to(cw + 2 * R, 4));
         }
@@ -475,6 +479,7 @@ Exec choose(const wtconv_desc& d, bool bwd)
 // ----------------------------------------------------------------------------
 struct GradPlan {
     PlaneGeom g;  // x side (zero-haloed)
+    int tail0 = 0, tail1 = 0;  // x-plane floats past dy level 1 that hold deeper dy levels
     int dy_off[kMaxLevels + 1] = {}, dy_pitch[kMaxLevels + 1] = {}, dy_band[kMaxLevels + 1] = {};
     int stride = 0, PP = 1, nb = 1, nchunks = 1, lds_floats = 0;
     int rounds = 1;  // 4x4 block rounds per plane (more than one only with PP = 1)
@@ -496,10 +501,11 @@ bool grad_layout(const wtconv_desc& d, int PP, GradPlan& gp)
     // halo ring per batch; it pays for large planes (one resident plane), where
     // it decides the number of workgroups per CU
     const bool may_alias = PP == 1;
-    if (!layout(d, PP, true, gp.g)) return false;
+    if (!layout(d, PP, true, gp.g, false, false, 3)) return false;
     const PlaneGeom& g = gp.g;
     const long xplane = (long)g.xrows * g.xpitch;
     long extra = 0;
+    long xfree = -1;  // with dy level 1 over the x plane: the first float of the x plane it leaves free
     for (int l = 1; l <= d.L; ++l) {
         const LevelGeom& lg = g.lv[l];
         int rows = std::max(lg.eh, l == 1 ? 2 * g.tiles_y : (l == 2 ? g.tiles_y : lg.h));
@@ -515,6 +521,18 @@ bool grad_layout(const wtconv_desc& d, int PP, GradPlan& gp)
         gp.dy_band[l] = rows * pitch;
         if (l == 1 && may_alias && size <= xplane && lg.eh <= 2 * g.tiles_y && lg.ew <= 2 * g.tiles_x) {
             gp.dy_off[l] = 0;
+            xfree = size;
+        } else if (l >= 3 && xfree >= 0 && xfree + size <= xplane) {
+            // the x plane is dead once dy level 1 is written over it (every
+            // dy level is written after the base correlation has read it), and
+            // the next batch's block loads and halo re-zeroing rewrite all of it;
+            // the kernel clears this tail in the phase that writes dy levels 1-2,
+            // before levels >= 3 are built in it (after a barrier), so that their
+            // sites past the grid read as zero
+            if (gp.tail1 == 0) gp.tail0 = (int)xfree;
+            gp.dy_off[l] = (int)xfree;
+            xfree += size;
+            gp.tail1 = (int)xfree;
         } else {
             gp.dy_off[l] = (int)(g.plane_floats + extra);
             extra += size;
@@ -598,13 +616,18 @@ constexpr int kGradSplitMinShed = 2;
 // plane's first level at most 8 x 8 is level 2 or deeper (planes above 16 x 16)
 // and there is at least one level (L = 1, k = 5: 28 x 28 115 -> 94 us, 40 x 40
 // 130 -> 80 us, 56 x 56 B = 128 252 -> 231 us); it then handles every level
-// itself. For smaller planes (whose coarse levels the fused backward runs as a
-// tiny sub-problem) and for L = 0 the fused backward runs.
+// itself. Planes whose level 1 is already at most 8 x 8 (9 x 9 to 16 x 16) take
+// it at L <= 2, where it runs without a coarse sub-problem (B128 C384 14 x 14,
+// k = 5: L = 1 139 -> 131 us, L = 2 196 -> 156 us); at L >= 3 the split it
+// would need (carriers and the tiny kernels, for dx too) is slower than the
+// fused backward (L = 3 201 -> 212 us, L = 5 205 -> 221 us). Smaller planes
+// and L = 0 run the fused backward.
 GradExec choose_grad(const wtconv_desc& d)
 {
     GradExec ge;
-    if (use_tiny(d) || tiny_level(d) < 2 || d.L < 1) return ge;
+    if (use_tiny(d) || d.L < 1) return ge;
     const int m = tiny_level(d);
+    if (m < 1 || (m == 1 && d.L > 2)) return ge;
     wtconv_desc f = d;
     if (d.L - m >= kGradSplitMinShed) {
         GradPlan full;
@@ -845,6 +868,8 @@ wtconv_status grad_pass(const wtconv_desc& d, const GradExec& ge, const void* x,
     a.skip_base = skip_base;
     a.stride = ge.gp.stride;
     a.r_ring = 1.0f / (float)(ge.gp.g.xpitch - 4 * ge.gp.g.tiles_x);
+    a.tail0 = ge.gp.tail0;
+    a.tail1 = ge.gp.tail1;
     for (int l = 0; l <= kMaxLevels; ++l) {
         a.dy_off[l] = ge.gp.dy_off[l];
         a.dy_pitch[l] = ge.gp.dy_pitch[l];

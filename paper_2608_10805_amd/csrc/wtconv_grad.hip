@@ -297,7 +297,9 @@ __global__ void __launch_bounds__(kThreads, grad_waves_per_simd<K>()) grad_kerne
             }
             __syncthreads();
 
-            // 3. dy levels 1-2 -> compact pyramid
+            // 3. dy levels 1-2 -> compact pyramid (and a clean x-plane tail
+            //    for the deeper dy levels stored there)
+            for (int i = a.tail0 + tl; i < a.tail1; i += kThreads) planes[i] = 0.f;
             if (mine) dy_levels(ti, dyb);
         } else {
             // One resident plane with more 4x4 blocks than threads: each phase
@@ -328,6 +330,7 @@ __global__ void __launch_bounds__(kThreads, grad_waves_per_simd<K>()) grad_kerne
                 analysis_level(planes + lp.off, lp.pitch, planes + lg.off, lg, R, np, stride, tl);
             }
             __syncthreads();
+            for (int i = a.tail0 + tl; i < a.tail1; i += kThreads) planes[i] = 0.f;
             for (int it = tl; it < per; it += kThreads) {
                 const TileIdx ti = tile_at(it, per, g.r_tiles, g.tiles_x, g.r_tiles_x, 4);
                 float dyb[4][4];

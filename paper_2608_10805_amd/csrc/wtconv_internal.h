@@ -195,6 +195,11 @@ struct GradArgs {
     int skip_base;   // 1: no base-kernel gradient (coarse sub-problem)
     int stride;      // floats per plane region (x side + dy side)
     float r_ring;    // 1 / (xpitch - 4 * tiles_x): ring columns of a middle row of the x plane
+    // [tail0, tail1): floats of the x plane past dy level 1 that hold deeper
+    // dy levels (when dy level 1 is stored over the x plane); cleared every
+    // batch before those levels are built, so that their sites past the grid
+    // read as zero; tail0 == tail1 when unused
+    int tail0, tail1;
     int dy_off[kMaxLevels + 1], dy_pitch[kMaxLevels + 1], dy_band[kMaxLevels + 1];
     PlaneGeom g;
 };

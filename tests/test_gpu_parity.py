@@ -193,6 +193,11 @@ GRAD = [
     (1, 2, 70, 66, 7, 1, "f16"),
     (1, 2, 97, 90, 3, 2, "bf16"),  # three block rounds
     (1, 3, 112, 112, 5, 3, "f32"),  # four block rounds
+    (5, 3, 14, 14, 5, 2, "f32"),  # level 1 at most 8 x 8, L <= 2: several resident planes
+    (3, 4, 11, 13, 3, 1, "bf16"),
+    (2, 3, 16, 16, 7, 2, "f16"),
+    (1, 2, 63, 95, 5, 4, "f32"),  # dy levels 3-4 stored past dy level 1 over the x plane
+    (2, 3, 63, 95, 3, 5, "bf16"),
 ]
 
 
