@@ -650,6 +650,11 @@ long level_floats(const wtconv_desc& d, int m)
     return (long)d.B * d.C * h * w;
 }
 
+// The coarse sub-problem of a split at level m: the operator (without base
+// path) on the level-m carriers, in the problem's storage type (the carriers,
+// the coarse contribution and, in the backward, the coarse dx are held in it:
+// half the workspace of fp32 for 16-bit problems, at one extra rounding of
+// those intermediates).
 wtconv_desc coarse_desc(const wtconv_desc& d, int m)
 {
     wtconv_desc s = d;
@@ -658,8 +663,13 @@ wtconv_desc coarse_desc(const wtconv_desc& d, int m)
         s.W = (s.W + 1) / 2;
     }
     s.L = d.L - m;
-    s.dtype = WTCONV_F32;
     return s;
+}
+
+// Bytes of one level-m carrier-sized buffer of the whole tensor (storage type).
+size_t level_bytes(const wtconv_desc& d, int m)
+{
+    return align256((size_t)level_floats(d, m) * elem_size(d.dtype));
 }
 
 wtc::TinyArgs tiny_args(const wtconv_desc& d, const void* in, const void* aux, void* out, float* partial,
@@ -711,7 +721,7 @@ size_t forward_ws(const wtconv_desc& d)
     if (!ex.coarse) return 0;
     const size_t sub = forward_ws(coarse_desc(d, ex.m));
     if (sub == kUnsupported) return kUnsupported;
-    return 2 * align256(level_floats(d, ex.m) * 4) + sub;
+    return 2 * level_bytes(d, ex.m) + sub;
 }
 
 size_t backward_ws(const wtconv_desc& d);
@@ -728,7 +738,7 @@ size_t grad_coarse_bytes(const wtconv_desc& d, const GradExec& ge)
     if (!ge.coarse) return 0;
     const size_t sub = backward_ws(coarse_desc(d, ge.Lf));
     if (sub == kUnsupported) return kUnsupported;
-    return 2 * align256(level_floats(d, ge.Lf) * 4) + sub;
+    return 2 * level_bytes(d, ge.Lf) + sub;
 }
 
 size_t backward_ws(const wtconv_desc& d)
@@ -746,7 +756,7 @@ size_t backward_ws(const wtconv_desc& d)
     if (!ex.coarse) return part;
     const size_t sub = backward_ws(coarse_desc(d, ex.m));
     if (sub == kUnsupported) return kUnsupported;
-    return part + 3 * align256(level_floats(d, ex.m) * 4) + sub;
+    return part + 3 * level_bytes(d, ex.m) + sub;
 }
 
 FusedArgs base_args(const wtconv_desc& d, const Plan& pl, const void* in, const void* aux, void* out,
@@ -783,7 +793,7 @@ void set_region(FusedArgs& a, const wtconv_desc& d, const RegionPlan& rp)
     a.rg_r_itiles = 1.0f / (float)((rp.T / 4) * (rp.T / 4));
 }
 
-void set_carry(FusedArgs& a, const wtconv_desc& d, int m, const float* carry)
+void set_carry(FusedArgs& a, const wtconv_desc& d, int m, const void* carry)
 {
     const wtconv_desc c = coarse_desc(d, m);
     a.carry = carry;
@@ -794,7 +804,7 @@ void set_carry(FusedArgs& a, const wtconv_desc& d, int m, const float* carry)
 
 wtconv_status hip_status(hipError_t e) { return e == hipSuccess ? WTCONV_OK : WTCONV_ERR_HIP; }
 
-wtconv_status carrier(const wtconv_desc& d, int m, const void* in, float* out, hipStream_t stream)
+wtconv_status carrier(const wtconv_desc& d, int m, const void* in, void* out, hipStream_t stream)
 {
     const wtconv_desc cd = coarse_desc(d, m);
     wtc::CarrierArgs c;
@@ -832,11 +842,11 @@ wtconv_status forward_impl(const wtconv_desc& d, const void* x, const wtc::Param
     if (ex.mode == Mode::Tiny)
         return hip_status(
             wtc::launch_tiny(d.k, d.dtype, false, tiny_args(d, x, nullptr, y, nullptr, p, skip_base), stream));
-    const float* carry = nullptr;
+    const void* carry = nullptr;
     if (ex.coarse) {
-        const size_t n1 = align256(level_floats(d, ex.m) * 4);
-        float* x1 = reinterpret_cast<float*>(ws);
-        float* c1 = reinterpret_cast<float*>(ws + n1);
+        const size_t n1 = level_bytes(d, ex.m);
+        void* x1 = ws;
+        void* c1 = ws + n1;
         wtconv_status st = carrier(d, ex.m, x, x1, stream);
         if (st != WTCONV_OK) return st;
         st = forward_impl(coarse_desc(d, ex.m), x1, shift_params(p, ex.m), c1, ws + 2 * n1, 1, stream);
@@ -889,9 +899,9 @@ wtconv_status partials_impl(const wtconv_desc& d, const void* x, const void* dy,
         if (ge.coarse) {
             // kernel gradients of levels Lf+1..L: the coarse sub-problem's on
             // the level-Lf carriers of x and dy (no dx, no base path)
-            const size_t n1 = align256(level_floats(d, ge.Lf) * 4);
-            float* x1 = reinterpret_cast<float*>(ws + part);
-            float* dy1 = reinterpret_cast<float*>(ws + part + n1);
+            const size_t n1 = level_bytes(d, ge.Lf);
+            void* x1 = ws + part;
+            void* dy1 = ws + part + n1;
             st = carrier(d, ge.Lf, x, x1, stream);
             if (st == WTCONV_OK) st = carrier(d, ge.Lf, dy, dy1, stream);
             if (st == WTCONV_OK)
@@ -913,12 +923,12 @@ wtconv_status partials_impl(const wtconv_desc& d, const void* x, const void* dy,
         return hip_status(wtc::launch_tiny(
             d.k, d.dtype, true, tiny_args(d, dy, x, dx, reinterpret_cast<float*>(ws), p, skip_base), stream));
     const size_t part = pass_partial_bytes(d, ex);
-    const float* carry = nullptr;
+    const void* carry = nullptr;
     if (ex.coarse) {
-        const size_t n1 = align256(level_floats(d, ex.m) * 4);
-        float* x1 = reinterpret_cast<float*>(ws + part);
-        float* dy1 = reinterpret_cast<float*>(ws + part + n1);
-        float* dx1 = dx ? reinterpret_cast<float*>(ws + part + 2 * n1) : nullptr;
+        const size_t n1 = level_bytes(d, ex.m);
+        void* x1 = ws + part;
+        void* dy1 = ws + part + n1;
+        void* dx1 = dx ? ws + part + 2 * n1 : nullptr;
         wtconv_status st = carrier(d, ex.m, x, x1, stream);
         if (st == WTCONV_OK) st = carrier(d, ex.m, dy, dy1, stream);
         if (st == WTCONV_OK)
@@ -964,7 +974,7 @@ wtconv_status finalize_impl(const wtconv_desc& d, const wtc::ParamPtrs& p, const
     if (ge.use) {
         if (ge.coarse) {
             const size_t part = grad_partial_bytes(d, ge);
-            const size_t n1 = align256(level_floats(d, ge.Lf) * 4);
+            const size_t n1 = level_bytes(d, ge.Lf);
             const wtconv_status st = finalize_impl(coarse_desc(d, ge.Lf), shift_params(p, ge.Lf),
                                                    shift_grads(gr, ge.Lf), ws + part + 2 * n1, 1, stream);
             if (st != WTCONV_OK) return st;
@@ -980,7 +990,7 @@ wtconv_status finalize_impl(const wtconv_desc& d, const wtc::ParamPtrs& p, const
     }
     if (ex.coarse) {
         const size_t part = pass_partial_bytes(d, ex);
-        const size_t n1 = align256(level_floats(d, ex.m) * 4);
+        const size_t n1 = level_bytes(d, ex.m);
         const wtconv_status st = finalize_impl(coarse_desc(d, ex.m), shift_params(p, ex.m), shift_grads(gr, ex.m),
                                                ws + part + 3 * n1, 1, stream);
         if (st != WTCONV_OK) return st;

@@ -674,24 +674,25 @@ DEV void base_tile(const float* __restrict__ xa, int xpitch, int y0, int x0, con
 // sum for a quadrant is simply added to that quadrant's level-1 LL.
 // `carry` (nullable) is the contribution of the levels above m = cr.m (the
 // synthesis of a coarse sub-problem, in orthonormal units, on the level-m
-// grid); it enters level m's LL, i.e. with the factor 2^-m of m synthesis
+// grid, in the pass's storage type); it enters level m's LL, i.e. with the factor 2^-m of m synthesis
 // steps: per quadrant for m = 1, tile-wide for m >= 2 (a 4x4 tile lies inside
 // one level-2 site). (cy, cx) is the tile's first level-m site in it.
 struct Carry {
-    const float* p;
+    const void* p;  // elements of the pass's storage type CT
     int H, W, cy, cx, m;
 };
 
-template <int K>
+template <int K, typename CT>
 DEV void synth_tile(const float* __restrict__ reg, const PlaneGeom& g, int y0, int x0, float (&acc)[4][4],
                     const Carry& cr)
 {
+    const CT* carry = reinterpret_cast<const CT*>(cr.p);
     constexpr int R = K / 2;
     const int L = g.L;
     if (L < 1) return;
     float coarse = 0.f;
     if (cr.p && cr.m >= 2 && cr.cy < cr.H && cr.cx < cr.W)
-        coarse = __builtin_ldexpf(cr.p[(long)cr.cy * cr.W + cr.cx], -cr.m);
+        coarse = __builtin_ldexpf(to_f32(carry[(long)cr.cy * cr.W + cr.cx]), -cr.m);
     for (int l = 3; l <= L; ++l) {
         const LevelGeom& lg = g.lv[l];
         const float* z = reg + lg.off + ((y0 >> l) + R) * lg.pitch + (x0 >> l) + R;
@@ -720,7 +721,7 @@ DEV void synth_tile(const float* __restrict__ reg, const PlaneGeom& g, int y0, i
 #pragma unroll
             for (int b = 0; b < 2; ++b) {
                 const int j = cr.cy + a, i = cr.cx + b;
-                if (j < cr.H && i < cr.W) quad[a][b] += 0.5f * cr.p[(long)j * cr.W + i];
+                if (j < cr.H && i < cr.W) quad[a][b] += 0.5f * to_f32(carry[(long)j * cr.W + i]);
             }
     }
     const LevelGeom& lg = g.lv[1];
@@ -967,14 +968,14 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(const FusedArgs a)
                     }
                     Carry cr = {nullptr, 0, 0, 0, 0, 0};
                     if (a.carry) {
-                        cr.p = a.carry + plane * a.carry_H * a.carry_W;
+                        cr.p = reinterpret_cast<const ST*>(a.carry) + plane * a.carry_H * a.carry_W;
                         cr.H = a.carry_H;
                         cr.W = a.carry_W;
                         cr.m = a.carry_level;
                         cr.cy = (oy + ti.j0) >> cr.m;
                         cr.cx = (ox + ti.i0) >> cr.m;
                     }
-                    synth_tile<K>(reg, g, ti.j0, ti.i0, acc, cr);
+                    synth_tile<K, ST>(reg, g, ti.j0, ti.i0, acc, cr);
                     store_tile<ST>(out + plane * HW, PH, PW, oy + ti.j0, ox + ti.i0, acc, vw);
                 } else if (!skip_base) {
                     load_center<K, 4>(reg, g.xpitch, ti.j0, ti.i0, ctr);

@@ -130,17 +130,18 @@ struct FusedArgs {
     int real_H, real_W;
     float rg_r_itx;      // 1 / (rg_T / 4): inner output tiles per tile row
     float rg_r_itiles;   // 1 / (rg_T / 4)^2
-    const float* carry;
+    const void* carry;  // storage type of the pass
     int carry_H, carry_W, carry_level;
     PlaneGeom g;
 };
 
 // Level-m raw LL carrier of every plane: 2^-m times the sum of each 2^m x 2^m
-// block of the zero-extended input, an fp32 [planes][H1][W1] array (H1, W1 =
-// ceil(H / 2^m), ceil(W / 2^m)).
+// block of the zero-extended input, a [planes][H1][W1] array in the input's
+// storage type (H1, W1 = ceil(H / 2^m), ceil(W / 2^m)), summed in fp32 and
+// rounded once.
 struct CarrierArgs {
     const void* in;
-    float* out;
+    void* out;
     long planes;
     int H, W, H1, W1;
     int m;

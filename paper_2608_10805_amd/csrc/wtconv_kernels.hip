@@ -75,7 +75,8 @@ __global__ void __launch_bounds__(64) reduce_kernel(const ReduceArgs a)
 
 // Raw LL carrier of level M (1 <= M <= 6): M levels of the orthonormal
 // butterfly's LL compose to 2^-M times the sum of each 2^M x 2^M pixel block
-// (zero outside the plane). One thread per output site. A workgroup covers
+// (zero outside the plane), written in the input's storage type. One thread
+// per output site. A workgroup covers
 // 256 consecutive sites: the (plane, row, column) of its first site is
 // computed once (uniformly), and each thread steps from there with fp32
 // reciprocals of small offsets (exact below 2^20). The block's loads are all
@@ -128,7 +129,7 @@ __global__ void __launch_bounds__(256) carrier_kernel(const CarrierArgs a)
             }
             s += rs;
         }
-        a.out[e] = __builtin_ldexpf(s, -M);
+        reinterpret_cast<T*>(a.out)[e] = from_f32<T>(__builtin_ldexpf(s, -M));
     }
 }
 
