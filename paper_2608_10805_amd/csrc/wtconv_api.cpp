@@ -22,8 +22,19 @@ constexpr int kBackwardTargetWorkgroups = 1536;
 int ceil_to(int v, int m) { return (v + m - 1) / m * m; }
 int cdiv(long a, long b) { return (int)((a + b - 1) / b); }
 
+// Mixed task rounds (wtconv_mixed.hip) of a forward plan: see pack_mixed().
+struct MixedPlan {
+    int rounds = 0;  // 0: the plan runs fused_kernel
+    int first_out = 0;
+    int seg0[wtc::kMixedMaxRounds + 1] = {};
+    int ntask[wtc::kMixedMaxRounds] = {};
+    int out0[wtc::kMixedMaxRounds] = {};
+    int seg[wtc::kMixedMaxSegs] = {};
+};
+
 struct Plan {
     PlaneGeom g;
+    MixedPlan mx;
     int one_round = 0;  // every level filtered in one register-tile round per lane
     int merge_deep = 0;  // forward: levels 1 and >= 3 filtered in one round (4x4 tiles)
     int PP = 1;        // planes resident at once
@@ -81,7 +92,7 @@ int pick_tile(int h, int w, int PP, int k, bool bwd, bool one_pref = false)
 // rows (the fused backward: 2; the gradient pass: 3, its level 2 goes by tiles);
 // those levels' rows are padded to whole row chunks.
 bool layout(const wtconv_desc& d, int PP, bool bwd, PlaneGeom& g, bool t4_deep = false, bool one_pref = false,
-            int rows_from = 2)
+            int rows_from = 2, bool t4_all = false)
 {
     const int R = d.k / 2;
     memset(&g, 0, sizeof(g));
@@ -100,7 +111,7 @@ bool layout(const wtconv_desc& d, int PP, bool bwd, PlaneGeom& g, bool t4_deep =
         LevelGeom& lg = g.lv[l];
         lg.h = h;
         lg.w = w;
-        lg.T = (t4_deep && l >= 3) ? 4 : pick_tile(h, w, PP, d.k, bwd, one_pref);
+        lg.T = (t4_all || (t4_deep && l >= 3)) ? 4 : pick_tile(h, w, PP, d.k, bwd, one_pref);
         if (lg.T == 0) return false;
         lg.eh = ceil_to(h, lg.T);
         lg.ew = ceil_to(w, lg.T);
@@ -171,7 +182,117 @@ double tile_use(const PlaneGeom& g, int PP)
     return (double)nt / ((double)wtc::kThreads * cdiv(nt, wtc::kThreads));
 }
 
-bool make_plan(const wtconv_desc& d, bool bwd, Plan& pl)
+// ----------------------------------------------------------------------------
+// Mixed task rounds (forward, resident planes; wtconv_mixed.hip). The output
+// tiles and the 4x4 site tiles of every (level, band) are equal tasks of 16
+// k^2 FMAs, dealt to 256 lanes per round. Whole (level, band) groups are packed
+// into rounds first-fit by decreasing size (a group's tiles share a round: its
+// band is written in place after that round's barrier, and no other round
+// reads it); the output tiles then fill the rounds from the last one holding a
+// group on (they need every level filtered). Fails if a group exceeds a round,
+// or more than kMixedMaxRounds rounds are needed.
+// ----------------------------------------------------------------------------
+bool pack_mixed(const wtconv_desc& d, int PP, const PlaneGeom& g, MixedPlan& mp)
+{
+    constexpr int cap = wtc::kThreads;
+    constexpr int RM = wtc::kMixedMaxRounds;
+    struct Grp {
+        int l, q, n;
+    };
+    Grp grp[4 * kMaxLevels];
+    int ng = 0;
+    for (int l = 1; l <= d.L; ++l) {
+        const LevelGeom& lg = g.lv[l];
+        if (lg.T != 4) return false;
+        const long n = (long)PP * (lg.eh / 4) * (lg.ew / 4);
+        if (n > cap) return false;
+        for (int q = 0; q < 4; ++q) grp[ng++] = {l, q, (int)n};
+    }
+    std::stable_sort(grp, grp + ng, [](const Grp& a, const Grp& b) { return a.n > b.n; });
+    int used[RM] = {};
+    int rnd[4 * kMaxLevels] = {};
+    int nr = 0;  // rounds holding groups
+    for (int i = 0; i < ng; ++i) {
+        int r = 0;
+        while (r < nr && used[r] + grp[i].n > cap) ++r;
+        if (r == RM) return false;
+        if (r == nr) ++nr;
+        used[r] += grp[i].n;
+        rnd[i] = r;
+    }
+    const int F = nr > 0 ? nr - 1 : 0;
+    long left = (long)PP * g.tiles_x * g.tiles_y;
+    int outs[RM] = {};
+    int r = F;
+    for (; left > 0; ++r) {
+        if (r >= RM) return false;
+        const int take = (int)std::min<long>(left, cap - used[r]);
+        outs[r] = take;
+        used[r] += take;
+        left -= take;
+    }
+    const int rounds = std::max(nr, r);
+    int ns = 0, out0 = 0;
+    for (int rr = 0; rr < rounds; ++rr) {
+        mp.seg0[rr] = ns;
+        mp.ntask[rr] = used[rr];
+        mp.out0[rr] = out0;
+        for (int i = 0; i < ng; ++i)
+            if (rnd[i] == rr) mp.seg[ns++] = 2 | (grp[i].l << 2) | (grp[i].q << 6) | (grp[i].n << 8);
+        if (outs[rr] > 0) mp.seg[ns++] = 1 | (outs[rr] << 8);
+        out0 += outs[rr];
+    }
+    mp.seg0[rounds] = ns;
+    mp.rounds = rounds;
+    mp.first_out = F;
+    return true;
+}
+
+// Modeled FMA issue per wavefront and resident plane of a forward plan, in
+// FMAs per lane: a round of T x T site tiles costs T^2 k^2 on every lane of
+// the wavefronts it occupies (masked lanes included).
+double issue_fused(const wtconv_desc& d, int PP, const PlaneGeom& g, bool merged)
+{
+    const int KK = d.k * d.k;
+    double c = (double)cdiv((long)PP * g.tiles_x * g.tiles_y, wtc::kThreads) * 16 * KK;
+    for (int l = 1; l <= d.L; ++l) {
+        const LevelGeom& lg = g.lv[l];
+        if (merged && l != 2) {
+            if (l == 1) c += 16.0 * KK;  // level 1 and the levels from 3 on: one round
+            continue;
+        }
+        c += (double)cdiv((long)PP * (lg.eh / lg.T) * (lg.ew / lg.T), 64) * lg.T * lg.T * KK;
+    }
+    return c / PP;
+}
+
+double issue_mixed(const wtconv_desc& d, int PP, const MixedPlan& mp)
+{
+    return (double)mp.rounds * 16 * d.k * d.k / PP;
+}
+
+// Workgroups per CU that the mixed kernel's registers allow (queried from the
+// runtime; without a device, the counts of one gfx950 build stand in: 75-125
+// VGPRs over k = 1..7 and one to four rounds).
+int mixed_wgs(const wtconv_desc& d, int rounds)
+{
+    return wtc::mixed_wgs_by_regs(d.k, d.dtype, rounds, d.k <= 3 ? 5 : 4);
+}
+
+// The mixed variant replaces a forward plan for planes of at most 16 x 16
+// pixels (level 1 at most 8 x 8) when its modeled issue per plane is at most
+// this fraction of the plan's and it keeps enough workgroups per CU. Measured
+// on MI355X (k = 5 fp32 unless noted, us per forward, fused -> mixed): 14 x 14
+// B128 C384 L1 46.0 -> 41.9, L2 73.2 -> 53.7, the split L3 76.1 -> 72.2, k = 7
+// L3 115.5 -> 95.8; 16 x 16 B128 C384 L1 41.3 -> 38.4, L2 67.5 -> 49.2; 15 x 15
+// and 13 x 13 at B128 C192 4-6 % faster; with fewer planes (B * C = 12288 or
+// 24576) within 1 %. On larger planes the fused kernel's lane use is already
+// 80-90 % and the extra barriers cost more than the mixed rounds save: 56 x 56
+// L3 B64 C96 68.0 -> 69.2, 20 x 20 L3 36.3 -> 41.5, 63 x 95 L3 149.7 -> 176.9.
+constexpr double kMixedGain = 0.95;
+constexpr int kMixedMaxEdge = 16;
+
+bool make_plan(const wtconv_desc& d, bool bwd, Plan& pl, bool allow_mixed = true)
 {
     const long px = (long)ceil_to(d.H, 4) * ceil_to(d.W, 4);
     int want = std::max(1, cdiv(4096, px));  // aim for >= 256 output tiles per workgroup
@@ -240,6 +361,44 @@ bool make_plan(const wtconv_desc& d, bool bwd, Plan& pl)
                 pl.lds_floats = lds;
                 pl.merge_deep = 1;
             }
+        }
+    }
+    // Forward: the mixed task rounds, at the plane count that minimises their
+    // modeled issue (more workgroups per CU on ties), if they beat the plan.
+    if (!bwd && allow_mixed && d.L >= 1 && d.H <= kMixedMaxEdge && d.W <= kMixedMaxEdge) {
+        const double cost_f = issue_fused(d, PP, pl.g, pl.merge_deep != 0);
+        const int wgs_f = std::min(forward_wgs(d, pl.one_round != 0), kLdsFloatsMax / pl.lds_floats);
+        const long tiles = (long)ceil_to(d.H, 4) * ceil_to(d.W, 4) / 16;
+        const int ppmax = (int)std::max(1L, std::min<long>(d.B, (long)wtc::kMixedMaxRounds * wtc::kThreads / tiles));
+        double best = -1.0;
+        int best_wgs = 0;
+        Plan mp;
+        for (int pp = 1; pp <= ppmax; ++pp) {
+            PlaneGeom g;
+            if (!layout(d, pp, false, g, false, false, kMaxLevels + 1, true)) continue;
+            MixedPlan m;
+            if (!pack_mixed(d, pp, g, m)) continue;
+            const int KP = ceil_to(d.k * d.k, 4);
+            const long lds = (long)(1 + 4 * d.L) * KP + (long)pp * g.plane_floats;
+            if (lds > kLdsFloatsMax) continue;
+            const int wgs = std::min(mixed_wgs(d, m.rounds), (int)(kLdsFloatsMax / lds));
+            const double cost = issue_mixed(d, pp, m);
+            if (best < 0 || cost < best || (cost == best && wgs > best_wgs)) {
+                best = cost;
+                best_wgs = wgs;
+                mp.g = g;
+                mp.mx = m;
+                mp.PP = pp;
+                mp.lds_floats = (int)lds;
+            }
+        }
+        if (best >= 0 && best <= kMixedGain * cost_f && best_wgs >= std::min(wgs_f, 3)) {
+            pl.g = mp.g;
+            pl.mx = mp.mx;
+            pl.PP = PP = mp.PP;
+            pl.lds_floats = mp.lds_floats;
+            pl.one_round = 0;
+            pl.merge_deep = 0;
         }
     }
     const int target = bwd ? kBackwardTargetWorkgroups : kForwardTargetWorkgroups;
@@ -373,7 +532,7 @@ bool make_region_plan(const wtconv_desc& d, bool bwd, RegionPlan& rp)
         rd.H = rd.W = T + 2 * rp.h;
         rd.L = m;
         Plan pl;
-        if (!make_plan(rd, bwd, pl) || pl.PP != 1) continue;
+        if (!make_plan(rd, bwd, pl, false) || pl.PP != 1) continue;
         rp.T = T;
         rp.ntx = cdiv(d.W, T);
         rp.nty = cdiv(d.H, T);
@@ -777,6 +936,12 @@ FusedArgs base_args(const wtconv_desc& d, const Plan& pl, const void* in, const 
     a.one_round = pl.one_round;
     a.merge_deep = pl.merge_deep;
     a.skip_base = skip_base;
+    a.mx_rounds = pl.mx.rounds;
+    a.mx_first_out = pl.mx.first_out;
+    memcpy(a.mx_seg0, pl.mx.seg0, sizeof(a.mx_seg0));
+    memcpy(a.mx_ntask, pl.mx.ntask, sizeof(a.mx_ntask));
+    memcpy(a.mx_out0, pl.mx.out0, sizeof(a.mx_out0));
+    memcpy(a.mx_seg, pl.mx.seg, sizeof(a.mx_seg));
     a.g = pl.g;
     return a;
 }

@@ -5,6 +5,7 @@ namespace wtc {
 
 hipError_t launch_forward(int k, wtconv_dtype dt, const FusedArgs& a, int grid, hipStream_t s)
 {
+    if (a.mx_rounds > 0) return launch_forward_mixed(k, dt, a, grid, s);
     return dispatch<false>(k, dt, a, grid, s);
 }
 

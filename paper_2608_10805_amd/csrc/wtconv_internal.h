@@ -62,6 +62,10 @@ constexpr int kWaves = kThreads / 64;
 constexpr int kMaxRounds4 = 4;   // 4x4-site tiles
 constexpr int kMaxRounds2 = 8;   // 2x2-site tiles
 constexpr int kMaxRounds1 = 16;  // single sites
+// Task rounds per lane of the mixed forward kernel (its results stay in
+// registers until every window has been read).
+constexpr int kMixedMaxRounds = 4;
+constexpr int kMixedMaxSegs = 4 * kMaxLevels + 4;
 
 // On-chip layout of one level of the Haar pyramid of one plane: four
 // band-planar arrays, each with a zero halo of R sites on every side.
@@ -132,6 +136,18 @@ struct FusedArgs {
     float rg_r_itiles;   // 1 / (rg_T / 4)^2
     const void* carry;  // storage type of the pass
     int carry_H, carry_W, carry_level;
+    // Mixed task rounds (forward, resident planes, every level in 4x4 site
+    // tiles; wtconv_mixed.hip): mx_rounds > 0 selects it. Round r runs the
+    // segments mx_seg[mx_seg0[r] .. mx_seg0[r + 1]), each a run of tasks:
+    // every 4x4 tile (over the PP planes) of one band of one level, or the
+    // next `count` output tiles. Packed: kind (1 output, 2 band) | level << 2 |
+    // band << 6 | count << 8. Band segments sit in rounds <= mx_first_out,
+    // output segments in rounds >= mx_first_out. mx_ntask[r]: tasks of round r;
+    // mx_out0[r]: output tiles in the rounds before r.
+    int mx_rounds, mx_first_out;
+    int mx_seg0[kMixedMaxRounds + 1];
+    int mx_ntask[kMixedMaxRounds], mx_out0[kMixedMaxRounds];
+    int mx_seg[kMixedMaxSegs];
     PlaneGeom g;
 };
 
@@ -214,6 +230,11 @@ hipError_t launch_forward(int k, wtconv_dtype dt, const FusedArgs& a, int grid, 
 // Workgroups per CU that the registers of the forward kernel for (k, dt,
 // single-round variant) allow; `fallback` if the runtime cannot tell.
 int forward_wgs_by_regs(int k, wtconv_dtype dt, bool one, int fallback);
+// The forward with mixed task rounds (a.mx_rounds in 1..kMixedMaxRounds).
+hipError_t launch_forward_mixed(int k, wtconv_dtype dt, const FusedArgs& a, int grid, hipStream_t s);
+// Workgroups per CU that the registers of the mixed forward kernel for (k, dt,
+// rounds) allow; `fallback` if the runtime cannot tell.
+int mixed_wgs_by_regs(int k, wtconv_dtype dt, int rounds, int fallback);
 hipError_t launch_backward(int k, wtconv_dtype dt, const FusedArgs& a, int grid, hipStream_t s);
 hipError_t launch_reduce(const ReduceArgs& a, hipStream_t s);
 hipError_t launch_grad(int k, wtconv_dtype dt, const GradArgs& a, int grid, hipStream_t s);

@@ -15,6 +15,8 @@ hipError_t launch_carrier(wtconv_dtype, const CarrierArgs&, hipStream_t) { retur
 hipError_t launch_tiny(int, wtconv_dtype, bool, const TinyArgs&, hipStream_t) { return hipSuccess; }
 size_t tiny_lds_bytes(int, int, bool) { return 0; }
 int forward_wgs_by_regs(int, wtconv_dtype, bool, int fallback) { return fallback; }
+hipError_t launch_forward_mixed(int, wtconv_dtype, const FusedArgs&, int, hipStream_t) { return hipSuccess; }
+int mixed_wgs_by_regs(int, wtconv_dtype, int, int fallback) { return fallback; }
 }  // namespace wtc
 
 static const char* mode_name(Mode m)
@@ -37,7 +39,19 @@ int main()
         const Exec f = choose(d, false);
         const GradExec ge = choose_grad(d);
         const Exec b = choose(d, true);
-        printf("{\"fwd_mode\": \"%s\", \"fwd_m\": %d, \"fwd_PP\": %d, \"fwd_one_round\": %d, \"fwd_merge_deep\": %d, "
+        printf("{\"fwd_mx_rounds\": %d, \"fwd_mx_first_out\": %d, \"fwd_mx_seg\": [", f.pl.mx.rounds,
+               f.pl.mx.first_out);
+        for (int r = 0; r < f.pl.mx.rounds; ++r) {
+            printf("%s[", r ? ", " : "");
+            for (int i = f.pl.mx.seg0[r]; i < f.pl.mx.seg0[r + 1]; ++i) {
+                const int sg = f.pl.mx.seg[i];
+                printf("%s[%d, %d, %d, %d]", i > f.pl.mx.seg0[r] ? ", " : "", sg & 3, (sg >> 2) & 15, (sg >> 6) & 3,
+                       sg >> 8);
+            }
+            printf("]");
+        }
+        printf("], ");
+        printf("\"fwd_mode\": \"%s\", \"fwd_m\": %d, \"fwd_PP\": %d, \"fwd_one_round\": %d, \"fwd_merge_deep\": %d, "
                "\"fwd_lds_floats\": %d, \"fwd_nb\": %d, \"fwd_nchunks\": %d, \"grad_pass\": %d, \"grad_levels\": %d, "
                "\"grad_coarse\": %d, \"grad_PP\": %d, \"grad_rounds\": %d, \"grad_lds_floats\": %d, "
                "\"grad_nchunks\": %d, \"bwd_mode\": \"%s\", \"fwd_ws\": %zu, \"bwd_ws\": %zu}\n",

@@ -93,6 +93,7 @@ BIAS = [
     (2, 2, 56, 56, 5, 5, "f32"),      # split levels
     (1, 2, 130, 126, 5, 3, "f32"),    # region tiles
     (2, 4, 28, 28, 3, 2, "bf16"),
+    (10, 3, 14, 14, 5, 2, "f32"),     # mixed forward rounds
 ]
 
 
@@ -161,6 +162,36 @@ DATA = [
 def test_backward_data(B, C, H, W, k, L, dtype):
     from paper_2608_10805_amd import binding
 
+    inp, dev = setup(B, C, H, W, k, L, dtype)
+    dx = binding.backward_data(dev.dy, dev.bw, dev.bs, dev.lw, dev.ls)
+    torch.cuda.synchronize()
+    ref = oracle.backward(inp.x, inp.dy, inp.base_w, inp.base_scale, inp.level_w, inp.level_scale)
+    e = rel_err(to_np(dx), ref["dx"])
+    assert e < TOL[dtype], f"dx rel err {e:.3e}"
+
+
+# Planes of at most 16 x 16 take the forward with mixed task rounds (output
+# tiles and every (level, band) tile packed into rounds of 256 lanes): several
+# resident planes with a partial last batch, odd sizes, k = 1..7, levels down
+# to 1 x 1 grids, 16-bit storage; y, and dx (the same kernel on dy with
+# rotated taps), against the oracle element by element.
+MIXED = [
+    (9, 6, 14, 14, 5, 1, "f32"),
+    (11, 7, 14, 14, 5, 3, "f32"),
+    (13, 5, 14, 14, 5, 2, "bf16"),
+    (17, 3, 13, 15, 5, 1, "f32"),
+    (5, 4, 16, 16, 7, 2, "f16"),
+    (33, 2, 12, 12, 3, 2, "f32"),
+    (6, 3, 9, 11, 1, 4, "f32"),
+    (20, 2, 16, 10, 5, 8, "f32"),
+]
+
+
+@pytest.mark.parametrize("B,C,H,W,k,L,dtype", MIXED)
+def test_mixed_rounds_forward_and_dx(B, C, H, W, k, L, dtype):
+    from paper_2608_10805_amd import binding
+
+    check_forward(B, C, H, W, k, L, dtype)
     inp, dev = setup(B, C, H, W, k, L, dtype)
     dx = binding.backward_data(dev.dy, dev.bw, dev.bs, dev.lw, dev.ls)
     torch.cuda.synchronize()

@@ -4,6 +4,7 @@ asked for the plan of each descriptor. These pin the execution paths that the
 measurements in the design notes were taken on, and check that every plan
 fits one compute unit's LDS and the chip's resident workgroup slots."""
 import json
+import random
 import os
 import shutil
 import subprocess
@@ -54,6 +55,51 @@ def test_headline_workload_plan(planner):
 def test_convnext_stage_modes(planner, C, H, L, fwd_mode):
     p = planner(128, C, H, H, 5, L)
     assert p["fwd_mode"] == fwd_mode
+
+
+def test_small_planes_take_mixed_rounds(planner):
+    """Planes of at most 16 x 16 run the forward with mixed task rounds: at
+    14 x 14 L = 1, eight planes' 128 output tiles and 128 level-1 tiles fill
+    one round of 256 lanes; the split 14 x 14 L = 3 forward's level-1 pass is
+    the same plan. Larger planes keep the fused kernel."""
+    p = planner(128, 384, 14, 14, 5, 1)
+    assert p["fwd_mode"] == "resident" and p["fwd_mx_rounds"] == 1 and p["fwd_PP"] == 8
+    assert sorted(map(tuple, p["fwd_mx_seg"][0])) == [(1, 0, 0, 128)] + [(2, 1, q, 32) for q in range(4)]
+    p = planner(128, 384, 14, 14, 5, 3)
+    assert p["fwd_mode"] == "split" and p["fwd_mx_rounds"] == 1
+    for H, L in [(56, 3), (28, 3), (20, 3)]:
+        assert planner(64, 96, H, H, 5, L)["fwd_mx_rounds"] == 0
+
+
+@pytest.fixture(scope="module")
+def mixed_check(tmp_path_factory):
+    gxx = shutil.which("g++")
+    if gxx is None:
+        pytest.skip("needs g++")
+    exe = str(tmp_path_factory.mktemp("mixed") / "mixed_check")
+    subprocess.run([gxx, "-O1", "-std=c++17", "-D__HIP_PLATFORM_AMD__", "-I", "/opt/rocm/include",
+                    "-I", os.path.join(ROOT, "include"), "-I", CSRC, "-x", "c++",
+                    os.path.join(ROOT, "tests", "planner", "mixed_check.cpp"), "-o", exe,
+                    "-L", "/opt/rocm/lib", "-lamdhip64", "-Wl,-rpath,/opt/rocm/lib"], check=True,
+                   capture_output=True)
+    return exe
+
+
+def test_mixed_round_plans_hold_their_invariants(mixed_check):
+    """Every mixed-round plan over 3000 seeded random small-plane problems
+    (and the ConvNeXt-T 14 x 14 stage) keeps what the kernel relies on: whole
+    (level, band) groups per round before the output rounds, every tile and
+    group covered once, at most 256 tasks a round, every window and write-back
+    inside its array and the LDS (tests/planner/mixed_check.cpp)."""
+    rng = random.Random(7)
+    lines = [f"{rng.randint(1, 140)} {rng.randint(1, 400)} {rng.randint(9, 16)} {rng.randint(9, 16)} "
+             f"{rng.choice([1, 3, 5, 7])} {rng.randint(1, 8)} {rng.randint(0, 2)}" for _ in range(3000)]
+    lines += [f"128 384 14 14 {k} {L} 0" for k in (3, 5, 7) for L in range(1, 6)]
+    out = subprocess.run([mixed_check], input="\n".join(lines) + "\n", capture_output=True, text=True,
+                         check=True, timeout=120).stdout.split("\n")[:len(lines)]
+    fails = [(l, o) for l, o in zip(lines, out) if not (o.startswith("ok") or o == "fused")]
+    assert not fails, fails[:5]
+    assert sum(o.startswith("ok") for o in out) > 1000
 
 
 def test_odd_shape_block_rounds(planner):
