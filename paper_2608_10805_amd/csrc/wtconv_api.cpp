@@ -777,16 +777,28 @@ constexpr int kGradSplitMinShed = 2;
 // 130 -> 80 us, 56 x 56 B = 128 252 -> 231 us); it then handles every level
 // itself. Planes whose level 1 is already at most 8 x 8 (9 x 9 to 16 x 16) take
 // it at L <= 2, where it runs without a coarse sub-problem (B128 C384 14 x 14,
-// k = 5: L = 1 139 -> 131 us, L = 2 196 -> 156 us); at L >= 3 the split it
-// would need (carriers and the tiny kernels, for dx too) is slower than the
-// fused backward (L = 3 201 -> 212 us, L = 5 205 -> 221 us). Smaller planes
-// and L = 0 run the fused backward.
+// k = 5: L = 1 139 -> 131 us, L = 2 196 -> 156 us). At L >= 3 it needs the
+// split (carriers and the tiny kernels, for dx too), which pays only where
+// the fused backward is weakest: at k = 7 (whose fused backward holds 3 x 49
+// kernel-gradient sums per lane and runs one wavefront per SIMD; B128 C384
+// 14 x 14 L = 3 623 -> 288 us, L = 5 629 -> 299 us, bf16 L = 3 696 -> 317 us,
+// 12 x 12 and 16 x 16 L = 3 -38 %) and at k = 5 on planes of at most 3 x 3
+// pixel blocks (B128 C192 L = 3: 10 x 10 126 -> 112 us, 11 x 11 140 -> 122 us,
+// 12 x 12 124 -> 109 us; 10 x 10 L = 5 129 -> 124 us). It loses at k = 5 from
+// 13 x 13 on (13 x 13 143 -> 158 us, 14 x 14 B128 C384 202 -> 210 us, 16 x 16
+// B64 C192 99 -> 108 us) and at k = 3 (12 x 12 within 2 %, 14 x 14 +5 %).
+// L = 0 runs the fused backward.
+bool grad_pass_pays_deep(const wtconv_desc& d)
+{
+    return d.k >= 7 || (d.k == 5 && ceil_to(d.H, 4) <= 12 && ceil_to(d.W, 4) <= 12);
+}
+
 GradExec choose_grad(const wtconv_desc& d)
 {
     GradExec ge;
     if (use_tiny(d) || d.L < 1) return ge;
     const int m = tiny_level(d);
-    if (m < 1 || (m == 1 && d.L > 2)) return ge;
+    if (m < 1 || (m == 1 && d.L > 2 && !grad_pass_pays_deep(d))) return ge;
     wtconv_desc f = d;
     if (d.L - m >= kGradSplitMinShed) {
         GradPlan full;

@@ -229,6 +229,12 @@ GRAD = [
     (2, 3, 16, 16, 7, 2, "f16"),
     (1, 2, 63, 95, 5, 4, "f32"),  # dy levels 3-4 stored past dy level 1 over the x plane
     (2, 3, 63, 95, 3, 5, "bf16"),
+    # small planes with deep levels: the split at m = 1 (k = 7, and k = 5 on
+    # planes of at most 3 x 3 pixel blocks)
+    (3, 4, 12, 12, 5, 3, "f32"),
+    (2, 3, 14, 14, 7, 3, "f32"),
+    (2, 2, 16, 16, 7, 5, "bf16"),
+    (5, 3, 11, 10, 5, 4, "f32"),
 ]
 
 
