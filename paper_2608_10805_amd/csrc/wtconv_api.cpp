@@ -92,6 +92,13 @@ int pick_tile(int h, int w, int PP, int k, bool bwd, bool one_pref = false)
     return best;
 }
 
+void set_tile_lanes(PlaneGeom& g, int lanes)
+{
+    g.tiles_xl = lanes;
+    g.r_tiles_xl = 1.0f / (float)lanes;
+    g.r_tiles_l = 1.0f / (float)(lanes * g.tiles_y);
+}
+
 // Lay out one plane's input array and pyramid for a given number of resident
 // planes. Returns false if a level cannot be tiled within the register caps.
 // rows_from: the first level whose kernel-gradient correlation walks whole
@@ -141,6 +148,7 @@ bool layout(const wtconv_desc& d, int PP, bool bwd, PlaneGeom& g, bool t4_deep =
     g.r_W = 1.0f / (float)d.W;
     g.r_tiles_x = 1.0f / (float)g.tiles_x;
     g.r_tiles = 1.0f / (float)(g.tiles_x * g.tiles_y);
+    set_tile_lanes(g, g.tiles_x);
     // flat indices decomposed with fp32 reciprocals must stay below 2^20
     if ((long)PP * g.tiles_x * g.tiles_y * 16 >= (1L << 20)) return false;
     return true;
@@ -406,6 +414,20 @@ bool make_plan(const wtconv_desc& d, bool bwd, Plan& pl, bool allow_mixed = true
             pl.one_round = 0;
             pl.merge_deep = 0;
         }
+    }
+    // Forward, single round: the rows of output tiles (and of the blocks the
+    // threads load) padded to a multiple of 8 lanes, so that every group of 8
+    // lanes of a 16-byte LDS access stays inside one tile row, when that keeps
+    // one round and does not put work on more wavefronts. Measured on MI355X
+    // (us per forward, k = 5): 56 x 56 L3 B64 C96 68.3 -> 66.6 (LDS bank
+    // conflict cycles -16 %), 28 x 28 L1 B64 C192 35.4 -> 34.4, k = 3 56 x 56
+    // L1 B128 79.7 -> 77.4; 12 x 12 L3, where it spread 63 tiles over three
+    // wavefronts instead of one, 55.7 -> 57.9 (hence the condition). Padding
+    // the subband tiles of the filter stage the same way changed nothing.
+    if (!bwd && pl.one_round && pl.mx.rounds == 0) {
+        const int xl = ceil_to(pl.g.tiles_x, 8);
+        const long n = (long)PP * pl.g.tiles_y * pl.g.tiles_x, npad = (long)PP * pl.g.tiles_y * xl;
+        if (npad <= wtc::kThreads && cdiv(npad, 64) == cdiv(n, 64)) set_tile_lanes(pl.g, xl);
     }
     const int target = bwd ? kBackwardTargetWorkgroups : kForwardTargetWorkgroups;
     const int chunks_target = std::max(1, cdiv(target, d.C));

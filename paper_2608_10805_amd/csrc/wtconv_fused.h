@@ -882,9 +882,10 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(const FusedArgs a)
 
         // 1. planes -> LDS, with Haar levels 1 and 2 formed on the way in
         {
-            const int tx = g.tiles_x, per = g.tiles_x * g.tiles_y;
+            const int tx = g.tiles_xl, per = g.tiles_xl * g.tiles_y;
             for (int it = tid; it < np * per; it += kThreads) {
-                const TileIdx ti = tile_at(it, per, g.r_tiles, tx, g.r_tiles_x, 4);
+                const TileIdx ti = tile_at(it, per, g.r_tiles_l, tx, g.r_tiles_xl, 4);
+                if (ti.i0 >= 4 * g.tiles_x) continue;  // a padding lane of the tile row
                 const long plane = (long)(b0 + ti.p) * C + c;
                 float v[4][4];
                 fetch_block<ST>(in + plane * HW, PH, PW, oy + ti.j0, ox + ti.i0, vw, v);
@@ -945,11 +946,12 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(const FusedArgs a)
         {
             float w[KK];
             fetch_weights<K>(wtab, 0, BWD, lane, w);
-            const int tx = RGN ? a.rg_T / 4 : g.tiles_x;
-            const int per = RGN ? tx * tx : g.tiles_x * g.tiles_y;
+            const int tx = RGN ? a.rg_T / 4 : g.tiles_xl;
+            const int per = RGN ? tx * tx : g.tiles_xl * g.tiles_y;
             for (int it = tid; it < np * per; it += kThreads) {
                 TileIdx ti = RGN ? tile_at(it, per, a.rg_r_itiles, tx, a.rg_r_itx, 4)
-                                 : tile_at(it, per, g.r_tiles, tx, g.r_tiles_x, 4);
+                                 : tile_at(it, per, g.r_tiles_l, tx, g.r_tiles_xl, 4);
+                if (!RGN && ti.i0 >= 4 * g.tiles_x) continue;  // a padding lane of the tile row
                 if (RGN) {
                     ti.j0 += a.rg_h;
                     ti.i0 += a.rg_h;

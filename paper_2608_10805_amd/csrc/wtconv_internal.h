@@ -95,6 +95,12 @@ struct PlaneGeom {
     float r_W;                     // 1 / W
     float r_tiles_x;               // 1 / tiles_x
     float r_tiles;                 // 1 / (tiles_x * tiles_y)
+    // Lanes per row of output tiles in the forward's block loads and output
+    // tiles (>= tiles_x; the lanes past tiles_x idle). A multiple of 8 keeps
+    // each group of 8 lanes of a 16-byte LDS access inside one tile row.
+    int tiles_xl;
+    float r_tiles_xl;              // 1 / tiles_xl
+    float r_tiles_l;               // 1 / (tiles_xl * tiles_y)
 };
 
 struct ParamPtrs {

@@ -51,6 +51,7 @@ int main()
             printf("]");
         }
         printf("], ");
+        printf("\"fwd_tiles_x\": %d, \"fwd_tiles_xl\": %d, ", f.pl.g.tiles_x, f.pl.g.tiles_xl);
         printf("\"fwd_mode\": \"%s\", \"fwd_m\": %d, \"fwd_PP\": %d, \"fwd_one_round\": %d, \"fwd_merge_deep\": %d, "
                "\"fwd_lds_floats\": %d, \"fwd_nb\": %d, \"fwd_nchunks\": %d, \"grad_pass\": %d, \"grad_levels\": %d, "
                "\"grad_coarse\": %d, \"grad_PP\": %d, \"grad_rounds\": %d, \"grad_lds_floats\": %d, "

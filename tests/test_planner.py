@@ -43,6 +43,8 @@ def test_headline_workload_plan(planner):
     p = planner(64, 96, 56, 56, 5, 3)
     assert p["fwd_mode"] == "resident" and p["fwd_PP"] == 1 and p["fwd_one_round"] == 1
     assert p["fwd_merge_deep"] == 1
+    # 14 output tiles per row, laid out over 16 lanes (one round, four wavefronts either way)
+    assert p["fwd_tiles_x"] == 14 and p["fwd_tiles_xl"] == 16
     assert p["fwd_ws"] == 0
     assert p["grad_pass"] == 1 and p["grad_levels"] == 3 and p["grad_coarse"] == 0
     assert p["grad_PP"] == 1 and p["grad_rounds"] == 1
@@ -55,6 +57,17 @@ def test_headline_workload_plan(planner):
 def test_convnext_stage_modes(planner, C, H, L, fwd_mode):
     p = planner(128, C, H, H, 5, L)
     assert p["fwd_mode"] == fwd_mode
+
+
+def test_tile_row_padding_keeps_the_busy_wavefronts(planner):
+    """Padding tile rows to 8 lanes is skipped where it would put work on more
+    wavefronts: 12 x 12 planes have 3 tiles per row (7 planes: 63 tiles, one
+    wavefront; padded, three)."""
+    p = planner(128, 192, 12, 12, 5, 3)
+    assert p["fwd_mx_rounds"] == 0 and p["fwd_one_round"] == 1
+    assert p["fwd_tiles_xl"] == p["fwd_tiles_x"] == 3
+    p = planner(64, 192, 28, 28, 5, 1)
+    assert p["fwd_tiles_xl"] == 8
 
 
 def test_small_planes_take_mixed_rounds(planner):
