@@ -948,7 +948,16 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(const FusedArgs a)
             fetch_weights<K>(wtab, 0, BWD, lane, w);
             const int tx = RGN ? a.rg_T / 4 : g.tiles_xl;
             const int per = RGN ? tx * tx : g.tiles_xl * g.tiles_y;
-            for (int it = tid; it < np * per; it += kThreads) {
+            // Backward with at most half as many output tiles as threads: a
+            // tile's dx (base correlation with rotated taps and synthesis) and
+            // its base kernel-gradient correlation go to two threads, the
+            // second half of the workgroup taking the correlations, instead of
+            // one thread doing both while the other half idles.
+            const int n = np * per;
+            const bool halves = BWD && have_out && !skip_base && 2 * n <= kThreads;
+            for (int it2 = tid; it2 < (halves ? 2 * n : n); it2 += kThreads) {
+                const bool corr_only = halves && it2 >= n;
+                const int it = corr_only ? it2 - n : it2;
                 TileIdx ti = RGN ? tile_at(it, per, a.rg_r_itiles, tx, a.rg_r_itx, 4)
                                  : tile_at(it, per, g.r_tiles_l, tx, g.r_tiles_xl, 4);
                 if (!RGN && ti.i0 >= 4 * g.tiles_x) continue;  // a padding lane of the tile row
@@ -959,7 +968,7 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(const FusedArgs a)
                 const float* reg = side_in + ti.p * stride;
                 const long plane = (long)(b0 + ti.p) * C + c;
                 float acc[4][4], ctr[4][4];
-                if (!BWD || have_out) {
+                if ((!BWD || have_out) && !corr_only) {
                     if (skip_base) {
 #pragma unroll
                         for (int oy2 = 0; oy2 < 4; ++oy2)
@@ -983,7 +992,7 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(const FusedArgs a)
                     load_center<K, 4>(reg, g.xpitch, ti.j0, ti.i0, ctr);
                 }
                 if constexpr (BWD) {
-                    if (!skip_base) {
+                    if (!skip_base && (corr_only || !halves)) {
                         corr_tile<K, 4>(side_aux + ti.p * stride, g.xpitch, ti.j0, ti.i0, ctr, g0);
 #pragma unroll
                         for (int oy2 = 0; oy2 < 4; ++oy2)
