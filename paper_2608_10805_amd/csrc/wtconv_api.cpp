@@ -932,12 +932,23 @@ size_t grad_partial_bytes(const wtconv_desc& d, const GradExec& ge)
 }
 
 
+// The dx pass of a gradient-pass backward with a coarse sub-problem on levels
+// above m: the forward's fused pass on levels 1..m of the resident plane (the
+// coarse levels enter as a carry). False if that pass has no resident plan.
+bool dx_pass_plan(const wtconv_desc& d, int m, Plan& pl)
+{
+    wtconv_desc f = d;
+    f.L = m;
+    return m >= 1 && !use_tiny(d) && make_plan(f, false, pl);
+}
+
+// [X_m][dY_m][dX_m][coarse backward]
 size_t grad_coarse_bytes(const wtconv_desc& d, const GradExec& ge)
 {
     if (!ge.coarse) return 0;
     const size_t sub = backward_ws(coarse_desc(d, ge.Lf));
     if (sub == kUnsupported) return kUnsupported;
-    return 2 * level_bytes(d, ge.Lf) + sub;
+    return 3 * level_bytes(d, ge.Lf) + sub;
 }
 
 size_t backward_ws(const wtconv_desc& d)
@@ -1100,26 +1111,44 @@ wtconv_status partials_impl(const wtconv_desc& d, const void* x, const void* dy,
     const GradExec ge = choose_grad(d);
     if (ge.use) {
         const size_t part = grad_partial_bytes(d, ge);
+        // dx is the forward pass on dy with every kernel rotated by 180
+        // degrees. With a coarse sub-problem its levels above Lf are that
+        // sub-problem's input gradient, which the coarse backward forms from
+        // the same carriers (it is the adjoint of the coarse branch applied to
+        // dY_Lf): dx is then one fused pass on levels 1..Lf with that carry,
+        // instead of a forward that would take the dy carrier and run the
+        // coarse forward again.
+        wtc::ParamPtrs pr = p;
+        pr.rot = 1;
+        pr.b0 = nullptr;  // the bias does not reach dx
+        Plan dxp;
+        const bool dx_carry = dx && ge.coarse && dx_pass_plan(d, ge.Lf, dxp);
         wtconv_status st = WTCONV_OK;
+        void* dx1 = nullptr;
         if (ge.coarse) {
-            // kernel gradients of levels Lf+1..L: the coarse sub-problem's on
-            // the level-Lf carriers of x and dy (no dx, no base path)
+            // kernel gradients of levels Lf+1..L (and the coarse part of dx):
+            // the coarse sub-problem's, on the level-Lf carriers of x and dy
+            // (no base path)
             const size_t n1 = level_bytes(d, ge.Lf);
             void* x1 = ws + part;
             void* dy1 = ws + part + n1;
+            dx1 = dx_carry ? ws + part + 2 * n1 : nullptr;
             st = carrier(d, ge.Lf, x, x1, stream);
             if (st == WTCONV_OK) st = carrier(d, ge.Lf, dy, dy1, stream);
             if (st == WTCONV_OK)
-                st = partials_impl(coarse_desc(d, ge.Lf), x1, dy1, shift_params(p, ge.Lf), nullptr, ws + part + 2 * n1,
+                st = partials_impl(coarse_desc(d, ge.Lf), x1, dy1, shift_params(p, ge.Lf), dx1, ws + part + 3 * n1,
                                    1, stream);
             if (st != WTCONV_OK) return st;
         }
         st = grad_pass(d, ge, x, dy, reinterpret_cast<float*>(ws), skip_base, stream);
         if (st != WTCONV_OK || !dx) return st;
-        // dx: the forward pass on dy with every kernel rotated by 180 degrees
-        wtc::ParamPtrs pr = p;
-        pr.rot = 1;
-        pr.b0 = nullptr;  // the bias does not reach dx
+        if (dx_carry) {
+            wtconv_desc f = d;
+            f.L = ge.Lf;
+            FusedArgs a = base_args(f, dxp, dy, nullptr, dx, pr, skip_base);
+            set_carry(a, d, ge.Lf, dx1);
+            return hip_status(wtc::launch_forward(d.k, d.dtype, a, dxp.nchunks * d.C, stream));
+        }
         return forward_impl(d, dy, pr, dx, ws + part + grad_coarse_bytes(d, ge), skip_base, stream);
     }
     const Exec ex = choose(d, true);
@@ -1180,8 +1209,9 @@ wtconv_status finalize_impl(const wtconv_desc& d, const wtc::ParamPtrs& p, const
         if (ge.coarse) {
             const size_t part = grad_partial_bytes(d, ge);
             const size_t n1 = level_bytes(d, ge.Lf);
+            // the coarse sub-problem's workspace follows X_m, dY_m and dX_m (see partials_impl)
             const wtconv_status st = finalize_impl(coarse_desc(d, ge.Lf), shift_params(p, ge.Lf),
-                                                   shift_grads(gr, ge.Lf), ws + part + 2 * n1, 1, stream);
+                                                   shift_grads(gr, ge.Lf), ws + part + 3 * n1, 1, stream);
             if (st != WTCONV_OK) return st;
         }
         return reduce(d, ge.Lf, ge.gp.nchunks, p, gr, ws, skip_base, stream);
