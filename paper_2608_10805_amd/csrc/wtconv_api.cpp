@@ -104,9 +104,15 @@ void set_tile_lanes(PlaneGeom& g, int lanes)
 // rows_from: the first level whose kernel-gradient correlation walks whole
 // rows (the fused backward: 2; the gradient pass: 3, its level 2 goes by tiles);
 // those levels' rows are padded to whole row chunks.
+// compact (forward plans): the four band arrays of a level share their zero
+// halo rows (band q's last R rows are band q + 1's first R: both are zeros
+// that nothing writes, and every window of band q ends within them), and no
+// row is padded for the kernel-gradient row chunks, which only the backward
+// runs.
 bool layout(const wtconv_desc& d, int PP, bool bwd, PlaneGeom& g, bool t4_deep = false, bool one_pref = false,
-            int rows_from = 2, bool t4_all = false)
+            int rows_from = 2, bool t4_all = false, bool compact = false)
 {
+    if (compact) rows_from = kMaxLevels + 1;
     const int R = d.k / 2;
     memset(&g, 0, sizeof(g));
     g.H = d.H;
@@ -135,13 +141,14 @@ bool layout(const wtconv_desc& d, int PP, bool bwd, PlaneGeom& g, bool t4_deep =
             pitch = std::max(pitch, ceil_to(w, cw) - cw + ceil_to(cw + 2 * R, 4));
         }
         lg.pitch = ceil_to(pitch, 4);
-        lg.band = rows * lg.pitch;
+        const int shared = compact ? R : 0;  // halo rows a band shares with the next
+        lg.band = (rows - shared) * lg.pitch;
         lg.off = (int)off;
         lg.r_w = 1.0f / (float)w;
         lg.r_hw = 1.0f / (float)(h * w);
         lg.r_tx = 1.0f / (float)(lg.ew / lg.T);
         lg.r_tper = 1.0f / (float)((lg.ew / lg.T) * (lg.eh / lg.T));
-        off += 4L * lg.band;
+        off += 4L * lg.band + (long)shared * lg.pitch;
         if (off > (1L << 30)) return false;
     }
     g.plane_floats = (int)off;
@@ -314,7 +321,7 @@ bool make_plan(const wtconv_desc& d, bool bwd, Plan& pl, bool allow_mixed = true
     int PP = 0;
     for (int pp = want; pp >= 1; --pp) {
         PlaneGeom g;
-        if (!layout(d, pp, bwd, g)) continue;
+        if (!layout(d, pp, bwd, g, false, false, 2, false, !bwd)) continue;
         const int lds = lds_floats_for(d, bwd, pp, g);
         if (lds <= kLdsFloatsShared || (pp == 1 && lds <= kLdsFloatsMax)) {
             PP = pp;
@@ -341,7 +348,7 @@ bool make_plan(const wtconv_desc& d, bool bwd, Plan& pl, bool allow_mixed = true
         for (int pp = 1; pp <= ppmax; ++pp)
             for (int pref = 0; pref < 2; ++pref) {
                 PlaneGeom g;
-                if (!layout(d, pp, bwd, g, false, pref == 1)) continue;
+                if (!layout(d, pp, bwd, g, false, pref == 1, 2, false, true)) continue;
                 const int lds = lds_floats_for(d, bwd, pp, g);
                 if (lds > kLdsFloatsMax) continue;
                 const bool one = single_round(d, pp, g);
@@ -365,7 +372,7 @@ bool make_plan(const wtconv_desc& d, bool bwd, Plan& pl, bool allow_mixed = true
     // the 7x7 level 3 of a 56x56 plane cost 5 us of a 73 us forward on its own).
     if (!bwd && pl.one_round && d.L >= 3 && pl.g.lv[1].T == 4) {
         PlaneGeom gm;
-        if (layout(d, PP, bwd, gm, true, pref_used)) {
+        if (layout(d, PP, bwd, gm, true, pref_used, 2, false, true)) {
             long lanes = (long)PP * (gm.lv[1].eh / 4) * (gm.lv[1].ew / 4);
             for (int l = 3; l <= d.L; ++l) lanes += (long)PP * (gm.lv[l].eh / 4) * (gm.lv[l].ew / 4);
             const int lds = lds_floats_for(d, bwd, PP, gm);
@@ -389,7 +396,7 @@ bool make_plan(const wtconv_desc& d, bool bwd, Plan& pl, bool allow_mixed = true
         Plan mp;
         for (int pp = 1; pp <= ppmax; ++pp) {
             PlaneGeom g;
-            if (!layout(d, pp, false, g, false, false, kMaxLevels + 1, true)) continue;
+            if (!layout(d, pp, false, g, false, false, kMaxLevels + 1, true, true)) continue;
             MixedPlan m;
             if (!pack_mixed(d, pp, g, m)) continue;
             const int KP = ceil_to(d.k * d.k, 4);

@@ -61,12 +61,14 @@ static const char* check(const wtconv_desc& d, const Plan& pl)
             if (cnt != PP * tx * ty) return "group size";
             if (seen[4 * l + q]++) return "group twice";
             // every tile of the group: window rows [j0, j0 + 4 + 2R), floats
-            // [i0, i0 + ceil4(4 + 2R)) of a band array of `rows` x pitch floats;
+            // [i0, i0 + ceil4(4 + 2R)) of a band array whose rows run to the
+            // next band's origin plus R zero halo rows it may share with it;
             // write-back rows [j0 + R, j0 + R + 4) clipped to the grid
-            const int rows = lg.band / lg.pitch, na = ceil_to(4 + 2 * R, 4);
+            const int rows = lg.band / lg.pitch + R, na = ceil_to(4 + 2 * R, 4);
             for (int t = 0; t < cnt; ++t) {
                 const int p = t / (tx * ty), rem = t % (tx * ty), j0 = 4 * (rem / tx), i0 = 4 * (rem % tx);
                 if (j0 + 4 + 2 * R > rows || i0 + na > lg.pitch) return "window outside its band array";
+                if (j0 + R + std::min(4, lg.h - j0) > lg.band / lg.pitch) return "write-back past the band's own rows";
                 const long base = (long)p * g.plane_floats + lg.off + (long)q * lg.band;
                 if (base + (long)(j0 + 4 + 2 * R - 1) * lg.pitch + i0 + na > planes_floats) return "window outside LDS";
                 if (std::min(4, lg.h - j0) < 1 || std::min(4, lg.w - i0) < 1) return "tile past the grid";
