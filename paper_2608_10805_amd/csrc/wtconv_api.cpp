@@ -104,15 +104,14 @@ void set_tile_lanes(PlaneGeom& g, int lanes)
 // rows_from: the first level whose kernel-gradient correlation walks whole
 // rows (the fused backward: 2; the gradient pass: 3, its level 2 goes by tiles);
 // those levels' rows are padded to whole row chunks.
-// compact (forward plans): the four band arrays of a level share their zero
-// halo rows (band q's last R rows are band q + 1's first R: both are zeros
-// that nothing writes, and every window of band q ends within them), and no
-// row is padded for the kernel-gradient row chunks, which only the backward
-// runs.
+// share_halo: the four band arrays of a level share their zero halo rows
+// (band q's last R rows are band q + 1's first R: both are zeros that nothing
+// writes, and every window or row read of band q ends within them). Forward
+// plans also pass rows_from = kMaxLevels + 1: only the backward runs the
+// kernel-gradient row chunks that the row padding is for.
 bool layout(const wtconv_desc& d, int PP, bool bwd, PlaneGeom& g, bool t4_deep = false, bool one_pref = false,
-            int rows_from = 2, bool t4_all = false, bool compact = false)
+            int rows_from = 2, bool t4_all = false, bool share_halo = false)
 {
-    if (compact) rows_from = kMaxLevels + 1;
     const int R = d.k / 2;
     memset(&g, 0, sizeof(g));
     g.H = d.H;
@@ -141,7 +140,7 @@ bool layout(const wtconv_desc& d, int PP, bool bwd, PlaneGeom& g, bool t4_deep =
             pitch = std::max(pitch, ceil_to(w, cw) - cw + ceil_to(cw + 2 * R, 4));
         }
         lg.pitch = ceil_to(pitch, 4);
-        const int shared = compact ? R : 0;  // halo rows a band shares with the next
+        const int shared = share_halo ? R : 0;  // halo rows a band shares with the next
         lg.band = (rows - shared) * lg.pitch;
         lg.off = (int)off;
         lg.r_w = 1.0f / (float)w;
@@ -321,7 +320,7 @@ bool make_plan(const wtconv_desc& d, bool bwd, Plan& pl, bool allow_mixed = true
     int PP = 0;
     for (int pp = want; pp >= 1; --pp) {
         PlaneGeom g;
-        if (!layout(d, pp, bwd, g, false, false, 2, false, !bwd)) continue;
+        if (!layout(d, pp, bwd, g, false, false, bwd ? 2 : kMaxLevels + 1, false, !bwd)) continue;
         const int lds = lds_floats_for(d, bwd, pp, g);
         if (lds <= kLdsFloatsShared || (pp == 1 && lds <= kLdsFloatsMax)) {
             PP = pp;
@@ -348,7 +347,7 @@ bool make_plan(const wtconv_desc& d, bool bwd, Plan& pl, bool allow_mixed = true
         for (int pp = 1; pp <= ppmax; ++pp)
             for (int pref = 0; pref < 2; ++pref) {
                 PlaneGeom g;
-                if (!layout(d, pp, bwd, g, false, pref == 1, 2, false, true)) continue;
+                if (!layout(d, pp, bwd, g, false, pref == 1, kMaxLevels + 1, false, true)) continue;
                 const int lds = lds_floats_for(d, bwd, pp, g);
                 if (lds > kLdsFloatsMax) continue;
                 const bool one = single_round(d, pp, g);
@@ -372,7 +371,7 @@ bool make_plan(const wtconv_desc& d, bool bwd, Plan& pl, bool allow_mixed = true
     // the 7x7 level 3 of a 56x56 plane cost 5 us of a 73 us forward on its own).
     if (!bwd && pl.one_round && d.L >= 3 && pl.g.lv[1].T == 4) {
         PlaneGeom gm;
-        if (layout(d, PP, bwd, gm, true, pref_used, 2, false, true)) {
+        if (layout(d, PP, bwd, gm, true, pref_used, kMaxLevels + 1, false, true)) {
             long lanes = (long)PP * (gm.lv[1].eh / 4) * (gm.lv[1].ew / 4);
             for (int l = 3; l <= d.L; ++l) lanes += (long)PP * (gm.lv[l].eh / 4) * (gm.lv[l].ew / 4);
             const int lds = lds_floats_for(d, bwd, PP, gm);
