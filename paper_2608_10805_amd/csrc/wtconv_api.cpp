@@ -575,7 +575,7 @@ bool make_region_plan(const wtconv_desc& d, bool bwd, RegionPlan& rp)
         const long chunks_target = std::max(1L, (target + d.C * ntiles - 1) / (d.C * ntiles));
         pl.nb = (int)((d.B + chunks_target - 1) / chunks_target);
         pl.nchunks = cdiv(d.B, pl.nb);
-        pl.one_round = 0;
+        if (bwd) pl.one_round = 0;  // the forward keeps its single-round variant
         if ((long)pl.nchunks * ntiles * d.C > INT32_MAX) return false;  // grid size
         rp.pl = pl;
         return true;

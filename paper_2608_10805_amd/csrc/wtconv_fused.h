@@ -1049,7 +1049,11 @@ hipError_t launch_variant(const FusedArgs& a, int grid, hipStream_t s)
 template <int K, typename ST, bool BWD>
 hipError_t launch_one(const FusedArgs& a, int grid, hipStream_t s)
 {
-    if (a.rg_ntx > 0) return launch_variant<K, ST, BWD, false, true>(a, grid, s);
+    if (a.rg_ntx > 0) {
+        if constexpr (!BWD)  // forward regions whose level fits one register-tile round
+            if (a.one_round) return launch_variant<K, ST, BWD, true, true>(a, grid, s);
+        return launch_variant<K, ST, BWD, false, true>(a, grid, s);
+    }
     return a.one_round ? launch_variant<K, ST, BWD, true, false>(a, grid, s)
                        : launch_variant<K, ST, BWD, false, false>(a, grid, s);
 }
