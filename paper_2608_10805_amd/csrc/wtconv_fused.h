@@ -664,6 +664,33 @@ DEV void base_tile(const float* __restrict__ xa, int xpitch, int y0, int x0, con
     }
 }
 
+// base_tile for TR output rows (a half tile: TR = 2), without the centre.
+template <int K, int TR>
+DEV void base_rows(const float* __restrict__ xa, int xpitch, int y0, int x0, const float (&w)[K * K], float init,
+                   float (&acc)[TR][4])
+{
+    constexpr int N = TR + 2 * (K / 2);
+#pragma unroll
+    for (int oy = 0; oy < TR; ++oy)
+#pragma unroll
+        for (int ox = 0; ox < 4; ++ox) acc[oy][ox] = 0.f;
+#pragma unroll
+    for (int r = 0; r < N; ++r) {
+        float row[Win<K, 4>::NA];
+        load_row<K, 4>(xa + (y0 + r) * xpitch + x0, row);
+#pragma unroll
+        for (int oy = 0; oy < TR; ++oy) {
+            const int p = r - oy;
+            if (p < 0 || p >= K) continue;
+#pragma unroll
+            for (int ox = 0; ox < 4; ++ox)
+#pragma unroll
+                for (int t = 0; t < K; ++t)
+                    acc[oy][ox] = __builtin_fmaf(w[p * K + t], row[ox + t], (p == 0 && t == 0) ? init : acc[oy][ox]);
+        }
+    }
+}
+
 // Proposition 2 for the 4x4 tile at (y0, x0), y0 and x0 multiples of 4, added
 // to acc. Every coefficient has its 4^-l already folded into the kernels, so
 // each level contributes LL + sy*LH + sx*HL + sy*sx*HH at (y >> l, x >> l) with
@@ -739,13 +766,67 @@ DEV void synth_tile(const float* __restrict__ reg, const PlaneGeom& g, int y0, i
         }
 }
 
+// synth_tile for half a (tile rows 2a and 2a + 1, i.e. level-1 quadrant row a)
+// of the 4x4 tile at (y0, x0): the same operations, in the same order, for
+// those eight pixels; acc holds their two rows.
+template <int K, typename CT>
+DEV void synth_half(const float* __restrict__ reg, const PlaneGeom& g, int y0, int x0, int a, float (&acc)[2][4],
+                    const Carry& cr)
+{
+    const CT* carry = reinterpret_cast<const CT*>(cr.p);
+    constexpr int R = K / 2;
+    const int L = g.L;
+    if (L < 1) return;
+    float coarse = 0.f;
+    if (cr.p && cr.m >= 2 && cr.cy < cr.H && cr.cx < cr.W)
+        coarse = __builtin_ldexpf(to_f32(carry[(long)cr.cy * cr.W + cr.cx]), -cr.m);
+    for (int l = 3; l <= L; ++l) {
+        const LevelGeom& lg = g.lv[l];
+        const float* z = reg + lg.off + ((y0 >> l) + R) * lg.pitch + (x0 >> l) + R;
+        const float ll = z[0], lh = z[lg.band], hl = z[2 * lg.band], hh = z[3 * lg.band];
+        const bool by = (y0 >> (l - 1)) & 1, bx = (x0 >> (l - 1)) & 1;
+        const float t1 = by ? ll - lh : ll + lh;
+        const float t2 = by ? hl - hh : hl + hh;
+        coarse += bx ? t1 - t2 : t1 + t2;
+    }
+    float quad[2];
+    if (L >= 2) {
+        const LevelGeom& lg = g.lv[2];
+        const float* z = reg + lg.off + ((y0 >> 2) + R) * lg.pitch + (x0 >> 2) + R;
+        const float ll = z[0] + coarse, lh = z[lg.band], hl = z[2 * lg.band], hh = z[3 * lg.band];
+        const float u = ll + lh, v = ll - lh, s = hl + hh, d = hl - hh;
+        quad[0] = a ? v + d : u + s;
+        quad[1] = a ? v - d : u - s;
+    } else {
+        quad[0] = quad[1] = coarse;
+    }
+    if (cr.p && cr.m == 1) {
+#pragma unroll
+        for (int b = 0; b < 2; ++b) {
+            const int j = cr.cy + a, i = cr.cx + b;
+            if (j < cr.H && i < cr.W) quad[b] += 0.5f * to_f32(carry[(long)j * cr.W + i]);
+        }
+    }
+    const LevelGeom& lg = g.lv[1];
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+        const float* z = reg + lg.off + ((y0 >> 1) + a + R) * lg.pitch + (x0 >> 1) + b + R;
+        const float ll = z[0] + quad[b], lh = z[lg.band], hl = z[2 * lg.band], hh = z[3 * lg.band];
+        const float u = ll + lh, v = ll - lh, s = hl + hh, d = hl - hh;
+        acc[0][2 * b] += u + s;
+        acc[0][2 * b + 1] += u - s;
+        acc[1][2 * b] += v + d;
+        acc[1][2 * b + 1] += v - d;
+    }
+}
+
 // Store a 4x4 output tile at (y0, x0) (non-negative, x0 a multiple of 4) of an
 // H x W plane, cropped to the plane; vw as for fetch_block.
-template <typename T>
-DEV void store_tile(T* __restrict__ plane, int H, int W, int y0, int x0, const float (&v)[4][4], int vw)
+template <typename T, int TR = 4>
+DEV void store_tile(T* __restrict__ plane, int H, int W, int y0, int x0, const float (&v)[TR][4], int vw)
 {
 #pragma unroll
-    for (int oy = 0; oy < 4; ++oy) {
+    for (int oy = 0; oy < TR; ++oy) {
         const int y = y0 + oy;
         if (y >= H || x0 >= W) break;
         T* row = plane + (long)y * W + x0;
@@ -955,7 +1036,15 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(const FusedArgs a)
             // one thread doing both while the other half idles.
             const int n = np * per;
             const bool halves = BWD && have_out && !skip_base && 2 * n <= kThreads;
-            for (int it2 = tid; it2 < (halves ? 2 * n : n); it2 += kThreads) {
+            // Forward with more output tiles than threads: the tiles past the
+            // last full round, when they fill at most half a round, are taken
+            // as half tiles (two rows each, two threads per tile), so that
+            // every thread's last round costs half a tile rather than half the
+            // threads paying a whole one.
+            const int rem = n % kThreads;
+            const bool tail_halves = !BWD && !ONE && !RGN && n > kThreads && rem != 0 && 2 * rem <= kThreads;
+            const int nmain = tail_halves ? n - rem : n;
+            for (int it2 = tid; it2 < (halves ? 2 * n : nmain); it2 += kThreads) {
                 const bool corr_only = halves && it2 >= n;
                 const int it = corr_only ? it2 - n : it2;
                 TileIdx ti = RGN ? tile_at(it, per, a.rg_r_itiles, tx, a.rg_r_itx, 4)
@@ -997,6 +1086,36 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(const FusedArgs a)
 #pragma unroll
                         for (int oy2 = 0; oy2 < 4; ++oy2)
                             gdy += (ctr[oy2][0] + ctr[oy2][1]) + (ctr[oy2][2] + ctr[oy2][3]);
+                    }
+                }
+            }
+            if constexpr (!BWD && !ONE && !RGN) {
+                if (tail_halves && tid < 2 * rem) {
+                    const int hrow = tid & 1;  // rows 2 hrow, 2 hrow + 1 of the tile
+                    const TileIdx ti = tile_at(nmain + (tid >> 1), per, g.r_tiles_l, tx, g.r_tiles_xl, 4);
+                    if (ti.i0 < 4 * g.tiles_x) {
+                        const float* reg = side_in + ti.p * stride;
+                        const long plane = (long)(b0 + ti.p) * C + c;
+                        float acc2[2][4];
+                        if (skip_base) {
+#pragma unroll
+                            for (int oy2 = 0; oy2 < 2; ++oy2)
+#pragma unroll
+                                for (int ox2 = 0; ox2 < 4; ++ox2) acc2[oy2][ox2] = 0.f;
+                        } else {
+                            base_rows<K, 2>(reg, g.xpitch, ti.j0 + 2 * hrow, ti.i0, w, bias, acc2);
+                        }
+                        Carry cr = {nullptr, 0, 0, 0, 0, 0};
+                        if (a.carry) {
+                            cr.p = reinterpret_cast<const ST*>(a.carry) + plane * a.carry_H * a.carry_W;
+                            cr.H = a.carry_H;
+                            cr.W = a.carry_W;
+                            cr.m = a.carry_level;
+                            cr.cy = ti.j0 >> cr.m;
+                            cr.cx = ti.i0 >> cr.m;
+                        }
+                        synth_half<K, ST>(reg, g, ti.j0, ti.i0, hrow, acc2, cr);
+                        store_tile<ST, 2>(out + plane * HW, PH, PW, ti.j0 + 2 * hrow, ti.i0, acc2, vw);
                     }
                 }
             }
