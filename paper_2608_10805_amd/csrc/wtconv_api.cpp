@@ -639,7 +639,14 @@ Exec choose(const wtconv_desc& d, bool bwd)
         ex.mode = Mode::Tiny;
         return ex;
     }
-    if (make_plan(d, bwd, ex.pl)) {
+    // A forward whose resident plane would leave one workgroup per CU runs in
+    // regions instead, whose single-round passes fit four: measured (us per
+    // forward, k = 5, B16 C64) 112 x 112 L1 76.7 -> 40.5, L3 93.3 -> 75.0;
+    // 96 x 96 L1 58.3 -> 38.8, L3 73.7 -> 66.2. At two workgroups per CU the
+    // resident plane stays ahead (63 x 95 L3 136.6 against 196.9, 84 x 84 L3
+    // 37.0 against 61.9).
+    if (make_plan(d, bwd, ex.pl) &&
+        (bwd || 2L * ex.pl.lds_floats <= kLdsFloatsMax || !make_region_plan(d, bwd, ex.rp))) {
         const int m = tiny_level(d);
         if (m >= 1 && d.L > m) {
             wtconv_desc f = d;
