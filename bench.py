@@ -4,8 +4,7 @@
 Headline workload: ConvNeXt-T stage-1 layer shape, B=64, C=96, H=W=56, k=5,
 L=3, float32, seeded synthetic inputs (see paper_2608_10805_amd/inputs.py).
 One step is the whole operator, forward and backward: wtconv_forward (y),
-then wtconv_backward_partials with dx and wtconv_backward_finalize (together
-exactly wtconv_backward). Inputs are resident in HBM before timing starts;
+then wtconv_backward with dx. Inputs are resident in HBM before timing starts;
 steps rotate over several distinct buffer sets so that the 256 MB Infinity
 Cache cannot hold one step's tensors for the next.
 
@@ -247,8 +246,7 @@ def config_table(steps, dev, table_out=None):
                 x, dy, y, dx = sets[i % nsets]
                 binding.forward(x, bw, bs, lw, ls, out=y, workspace=fws)
                 if with_bwd:
-                    bk.partials(x, dy, dx)
-                    bk.finalize()
+                    bk.run(x, dy, dx)
 
         res = {}
         for with_bwd in (False, True):
@@ -781,18 +779,16 @@ class Step:
         self.binding = binding
 
     def __call__(self, i, ev=None):
-        """wtconv_forward, wtconv_backward_partials (with dx) and
-        wtconv_backward_finalize: the whole operator, forward and backward.
-        With `ev` (three events) the forward and the backward phases are
-        bracketed on the library's stream."""
+        """wtconv_forward, then wtconv_backward (with dx): the whole operator,
+        forward and backward. With `ev` (three events) the forward and the
+        backward phases are bracketed on the library's stream."""
         x, dy, y, dx = self.sets[i % len(self.sets)]
         if ev is not None:
             ev[0].record()
         self.binding.forward(x, self.bw, self.bs, self.lw, self.ls, out=y, workspace=self.fws)
         if ev is not None:
             ev[1].record()
-        self.bk.partials(x, dy, dx)
-        self.bk.finalize()
+        self.bk.run(x, dy, dx)
         if ev is not None:
             ev[2].record()
 
@@ -901,6 +897,10 @@ def main(argv=None):
     headline = args.workload == HEADLINE
     nev = 5 if headline else 3
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(nev)] for _ in range(args.steps)]
+    if headline:
+        # untimed first: the split calls allocate their buffers on first use
+        for i in range(3):
+            step.split(i, evs[i])
     torch.cuda.synchronize()
     for i in range(args.steps):
         if headline:

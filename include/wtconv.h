@@ -145,10 +145,13 @@ size_t wtconv_backward_workspace_bytes(const wtconv_desc* desc);
  *                      aligned); its contents are scratch
  * Outputs must not overlap the inputs, each other or the workspace.
  * For planes above 16 x 16 with L >= 1, and planes above 8 x 8 with L = 1 or
- * 2, dx is the forward pass on dy with every kernel rotated by 180 degrees (the
- * adjoint of the operator) and the kernel gradients come from a separate
- * correlation pass over x and dy; for other shapes one fused pass per plane
- * produces both.
+ * 2 (any L for k = 7, and for k = 5 up to 12 x 12), dx is the forward pass on
+ * dy with every kernel rotated by 180 degrees (the adjoint of the operator)
+ * and the kernel gradients come from a separate correlation pass over x and
+ * dy; the final reduction of those gradients then runs in the launch that
+ * forms dx (wtconv_backward_partials followed by wtconv_backward_finalize
+ * launch it on its own, with bit-identical results). For other shapes one
+ * fused pass per plane produces both.
  */
 wtconv_status wtconv_backward(const wtconv_desc* desc, const void* x, const void* dy,
                               const float* base_w, const float* base_scale, const float* base_bias,

@@ -331,8 +331,8 @@ def backward_data(dy, base_w, base_scale, level_w, level_scale, out=None, worksp
 
 
 class Backward:
-    """Preallocated backward of one problem, callable in its two phases
-    (used by the benchmark to time the fused pass and the finalize separately)."""
+    """Preallocated backward of one problem: whole (wtconv_backward, `run`) or
+    in its two phases (used by the benchmark to time the passes separately)."""
 
     def __init__(self, x, base_w, base_scale, level_w, level_scale, need_dx=True):
         import torch
@@ -360,6 +360,20 @@ class Backward:
     def _check_act(self, name, t):
         shape, dtype, device = self.x_like
         _require(t, name, dtype, shape, device)
+
+    def run(self, x, dy, dx=None):
+        """wtconv_backward into the preallocated gradients; dx into `dx`, else
+        into the preallocated buffer when the object was made with need_dx,
+        else skipped."""
+        bw, bs, _, _ = self.params
+        out = dx if dx is not None else self.dx
+        for name, t in (("x", x), ("dy", dy), ("dx", out)):
+            if t is not None:
+                self._check_act(name, t)
+        _check(wtconv_backward(self.desc, x.data_ptr(), dy.data_ptr(), bw.data_ptr(), bs.data_ptr(), None, self._lw,
+                               self._ls, out.data_ptr() if out is not None else None, self.dbw.data_ptr(),
+                               self.dbs.data_ptr(), None, self._dlw, self._dls, self.workspace.data_ptr(),
+                               self.nbytes, _stream(self.device)))
 
     def partials(self, x, dy, dx=None):
         """Writes dx into `dx`, else into the preallocated buffer when the

@@ -1063,8 +1063,55 @@ FusedPass fused_pass(const wtconv_desc& d, const Exec& ex)
     return {&ex.pl, ex.pl.nchunks * d.C};
 }
 
+wtc::ReduceArgs reduce_args(const wtconv_desc& d, int L, int nchunks, const wtc::ParamPtrs& p, const Grads& gr,
+                            const char* ws, int skip_base)
+{
+    wtc::ReduceArgs r;
+    memset(&r, 0, sizeof(r));
+    r.partial = reinterpret_cast<const float*>(ws);
+    r.nchunks = nchunks;
+    r.C = d.C;
+    r.k = d.k;
+    r.L = L;
+    r.skip_base = skip_base;
+    r.p = p;
+    r.dw0 = gr.dw0;
+    r.ds0 = gr.ds0;
+    r.db0 = skip_base ? nullptr : gr.db0;
+    for (int l = 0; l < L; ++l) {
+        r.dlw[l] = gr.dlw[l];
+        r.dls[l] = gr.dls[l];
+    }
+    return r;
+}
+
+wtconv_status reduce(const wtconv_desc& d, int L, int nchunks, const wtc::ParamPtrs& p, const Grads& gr,
+                     const char* ws, int skip_base, hipStream_t stream)
+{
+    return hip_status(wtc::launch_reduce(reduce_args(d, L, nchunks, p, gr, ws, skip_base), stream));
+}
+
+// A finalize reduction that the last launch of a forward pass runs in extra
+// workgroups ahead of its own (dx of the combined backward); `done` tells
+// whether it was attached (a tiny-plane pass takes none). Their count is
+// rounded up to a multiple of 8 so that the plane workgroups keep their
+// round-robin placement over the eight XCDs.
+struct FinJob {
+    wtc::ReduceArgs r;
+    bool done;
+};
+
+void attach_fin(FusedArgs& a, int& grid, FinJob* fin)
+{
+    if (!fin) return;
+    a.fin = fin->r;
+    a.fin_blocks = ceil_to(cdiv((long)fin->r.C * (1 + 4 * fin->r.L), 4), 8);
+    grid += a.fin_blocks;
+    fin->done = true;
+}
+
 wtconv_status forward_impl(const wtconv_desc& d, const void* x, const wtc::ParamPtrs& p, void* y, char* ws,
-                           int skip_base, hipStream_t stream)
+                           int skip_base, hipStream_t stream, FinJob* fin = nullptr)
 {
     const Exec ex = choose(d, false);
     if (ex.mode == Mode::None) return WTCONV_ERR_UNSUPPORTED;
@@ -1086,7 +1133,9 @@ wtconv_status forward_impl(const wtconv_desc& d, const void* x, const wtc::Param
     FusedArgs a = base_args(d, *fp.pl, x, nullptr, y, p, skip_base);
     if (ex.mode == Mode::Region) set_region(a, d, ex.rp);
     if (carry) set_carry(a, d, ex.m, carry);
-    return hip_status(wtc::launch_forward(d.k, d.dtype, a, fp.grid, stream));
+    int grid = fp.grid;
+    attach_fin(a, grid, fin);
+    return hip_status(wtc::launch_forward(d.k, d.dtype, a, grid, stream));
 }
 
 wtconv_status grad_pass(const wtconv_desc& d, const GradExec& ge, const void* x, const void* dy, float* partial,
@@ -1118,8 +1167,12 @@ wtconv_status grad_pass(const wtconv_desc& d, const GradExec& ge, const void* x,
     return hip_status(wtc::launch_grad(d.k, d.dtype, a, ge.gp.nchunks * d.C, stream));
 }
 
+// With `gr` (the combined backward), the finalize of the kernel gradients of
+// levels 0..Lf of the gradient route runs at the end of the dx launch when it
+// can; *fin_done then tells finalize_impl to skip it.
 wtconv_status partials_impl(const wtconv_desc& d, const void* x, const void* dy, const wtc::ParamPtrs& p,
-                            void* dx, char* ws, int skip_base, hipStream_t stream)
+                            void* dx, char* ws, int skip_base, hipStream_t stream, const Grads* gr = nullptr,
+                            bool* fin_done = nullptr)
 {
     const GradExec ge = choose_grad(d);
     if (ge.use) {
@@ -1155,14 +1208,22 @@ wtconv_status partials_impl(const wtconv_desc& d, const void* x, const void* dy,
         }
         st = grad_pass(d, ge, x, dy, reinterpret_cast<float*>(ws), skip_base, stream);
         if (st != WTCONV_OK || !dx) return st;
+        FinJob fin = {};
+        if (gr) fin.r = reduce_args(d, ge.Lf, ge.gp.nchunks, p, *gr, ws, skip_base);
         if (dx_carry) {
             wtconv_desc f = d;
             f.L = ge.Lf;
             FusedArgs a = base_args(f, dxp, dy, nullptr, dx, pr, skip_base);
             set_carry(a, d, ge.Lf, dx1);
-            return hip_status(wtc::launch_forward(d.k, d.dtype, a, dxp.nchunks * d.C, stream));
+            int grid = dxp.nchunks * d.C;
+            attach_fin(a, grid, gr ? &fin : nullptr);
+            st = hip_status(wtc::launch_forward(d.k, d.dtype, a, grid, stream));
+        } else {
+            st = forward_impl(d, dy, pr, dx, ws + part + grad_coarse_bytes(d, ge), skip_base, stream,
+                              gr ? &fin : nullptr);
         }
-        return forward_impl(d, dy, pr, dx, ws + part + grad_coarse_bytes(d, ge), skip_base, stream);
+        if (fin_done) *fin_done = st == WTCONV_OK && fin.done;
+        return st;
     }
     const Exec ex = choose(d, true);
     if (ex.mode == Mode::None) return WTCONV_ERR_UNSUPPORTED;
@@ -1192,30 +1253,10 @@ wtconv_status partials_impl(const wtconv_desc& d, const void* x, const void* dy,
     return hip_status(wtc::launch_backward(d.k, d.dtype, a, fp.grid, stream));
 }
 
-wtconv_status reduce(const wtconv_desc& d, int L, int nchunks, const wtc::ParamPtrs& p, const Grads& gr,
-                     const char* ws, int skip_base, hipStream_t stream)
-{
-    wtc::ReduceArgs r;
-    memset(&r, 0, sizeof(r));
-    r.partial = reinterpret_cast<const float*>(ws);
-    r.nchunks = nchunks;
-    r.C = d.C;
-    r.k = d.k;
-    r.L = L;
-    r.skip_base = skip_base;
-    r.p = p;
-    r.dw0 = gr.dw0;
-    r.ds0 = gr.ds0;
-    r.db0 = skip_base ? nullptr : gr.db0;
-    for (int l = 0; l < L; ++l) {
-        r.dlw[l] = gr.dlw[l];
-        r.dls[l] = gr.dls[l];
-    }
-    return hip_status(wtc::launch_reduce(r, stream));
-}
-
+// main_done: the reduction of levels 0..Lf of the gradient route already ran
+// with the dx launch (partials_impl with `gr`).
 wtconv_status finalize_impl(const wtconv_desc& d, const wtc::ParamPtrs& p, const Grads& gr, const char* ws,
-                            int skip_base, hipStream_t stream)
+                            int skip_base, hipStream_t stream, bool main_done = false)
 {
     const GradExec ge = choose_grad(d);
     if (ge.use) {
@@ -1227,6 +1268,7 @@ wtconv_status finalize_impl(const wtconv_desc& d, const wtc::ParamPtrs& p, const
                                                    shift_grads(gr, ge.Lf), ws + part + 3 * n1, 1, stream);
             if (st != WTCONV_OK) return st;
         }
+        if (main_done) return WTCONV_OK;
         return reduce(d, ge.Lf, ge.gp.nchunks, p, gr, ws, skip_base, stream);
     }
     const Exec ex = choose(d, true);
@@ -1496,10 +1538,11 @@ wtconv_status wtconv_backward(const wtconv_desc* desc, const void* x, const void
     wtc::ParamPtrs p;
     fill_params(p, d.L, base_w, base_scale, base_bias, level_w, level_scale);
     char* ws = reinterpret_cast<char*>(workspace);
-    st = partials_impl(d, x, dy, p, dx, ws, 0, stream);
+    const Grads gr = grads_of(d.L, d_base_w, d_base_scale, d_base_bias, d_level_w, d_level_scale);
+    bool fin_done = false;
+    st = partials_impl(d, x, dy, p, dx, ws, 0, stream, &gr, &fin_done);
     if (st != WTCONV_OK) return st;
-    return finalize_impl(d, p, grads_of(d.L, d_base_w, d_base_scale, d_base_bias, d_level_w, d_level_scale), ws,
-                         0, stream);
+    return finalize_impl(d, p, gr, ws, 0, stream, fin_done);
 }
 
 }  // extern "C"

@@ -871,6 +871,84 @@ DEV float wave_sum(float v)
     return v;
 }
 
+// Sum the per-workgroup partials over chunks in increasing order, then unfold
+// eq. (foldgrad): dW = s * G and ds = <G, W>, where G is the gradient of the
+// folded kernel s*W (the level partials carry an extra 4^l from the
+// unnormalised pyramids, removed here exactly); for the base row also the bias
+// terms d b0 = s0 * sum(dy) and b0 * sum(dy) in d s0. One wavefront per
+// (channel c, kernel row `band`: 0 = base, else 1 + (l-1)*4 + q); lane t
+// owns tap t (lane k*k the sum of dy); the d(scale) dot product is a
+// fixed-order wavefront reduction.
+DEV void reduce_task(const ReduceArgs& a, int c, int band, int t)
+{
+    const int KK = a.k * a.k;
+    const int NP = partial_floats_per_channel(a.k, a.L);
+    if (band == 0 && a.skip_base) return;
+    float scale, norm;
+    const float* w;
+    float* dw;
+    float* ds;
+    if (band == 0) {
+        scale = a.p.s0[c];
+        norm = 1.f;
+        w = a.p.w0 + (long)c * KK;
+        dw = a.dw0 + (long)c * KK;
+        ds = a.ds0 + c;
+    } else {
+        const int l = (band - 1) / 4 + 1, q = (band - 1) % 4;
+        const int ch = 4 * c + q;
+        scale = a.p.ls[l - 1][ch];
+        norm = __builtin_ldexpf(1.f, -2 * l);
+        w = a.p.lw[l - 1] + (long)ch * KK;
+        dw = a.dlw[l - 1] + (long)ch * KK;
+        ds = a.dls[l - 1] + ch;
+    }
+    float prod = 0.f;
+    if (t < KK) {
+        const float* src = a.partial + (long)c * NP + band * KK + t;
+        const long step = (long)a.C * NP;
+        // chunk order is kept; the loads of a group of 8 chunks are issued
+        // together so that their latencies overlap
+        float G = 0.f;
+        int ch = 0;
+        for (; ch + 8 <= a.nchunks; ch += 8) {
+            float v[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) v[u] = src[(long)(ch + u) * step];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) G += v[u];
+        }
+        for (; ch < a.nchunks; ++ch) G += src[(long)ch * step];
+        G *= norm;
+        dw[t] = scale * G;
+        prod = G * w[t];
+    } else if (band == 0 && t == KK) {
+        // folded base bias b~ = s0 * b0: its gradient is the sum of dy, so
+        // d b0 = s0 * sum(dy) and d s0 gains b0 * sum(dy) (eq. foldgrad)
+        const float* src = a.partial + (long)c * NP + (NP - 1);
+        const long step = (long)a.C * NP;
+        float Gb = 0.f;
+        for (int ch = 0; ch < a.nchunks; ++ch) Gb += src[(long)ch * step];
+        if (a.db0) a.db0[c] = scale * Gb;
+        if (a.p.b0) prod = a.p.b0[c] * Gb;
+    }
+    prod = wave_sum(prod);
+    if (t == 0) *ds = prod;
+}
+
+// A finalize workgroup at the head of a forward launch: wavefront w of
+// workgroup b takes task 4b + w, task c * (1 + 4L) + row being (channel c,
+// kernel row `row`). Dispatched first, these short, latency-bound waves
+// overlap the plane work instead of trailing it.
+DEV void fin_wave(const FusedArgs& a, int lane, int wave)
+{
+    const int rows = 1 + 4 * a.fin.L;
+    const int task = 4 * (int)blockIdx.x + wave;
+    if (task >= a.fin.C * rows) return;
+    const int c = task / rows;
+    reduce_task(a.fin, c, task - c * rows, lane);
+}
+
 // Index of the folded-weight row for the base kernel (0) or level l band q.
 DEV int wrow(int l, int q) { return l == 0 ? 0 : 1 + (l - 1) * 4 + q; }
 
@@ -900,10 +978,16 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(const FusedArgs a)
     const PlaneGeom& g = a.g;  // the plane (or, in region mode, the region) held on chip
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int C = a.C;
-    const int c = blockIdx.x % C;
+    if constexpr (!BWD)
+        if ((int)blockIdx.x < a.fin_blocks) {
+            fin_wave(a, lane, wave);
+            return;
+        }
+    const int bid = (int)blockIdx.x - a.fin_blocks;
+    const int c = bid % C;
     const int ntiles = RGN ? a.rg_ntx * a.rg_nty : 1;
-    const int chunk = (blockIdx.x / C) / ntiles;
-    const int tile = (blockIdx.x / C) - chunk * ntiles;
+    const int chunk = (bid / C) / ntiles;
+    const int tile = (bid / C) - chunk * ntiles;
     const int b_begin = chunk * a.nb;
     const int b_end = min(a.B, b_begin + a.nb);
     const int L = g.L;

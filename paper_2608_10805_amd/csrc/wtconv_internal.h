@@ -116,6 +116,21 @@ struct ParamPtrs {
     int rot;
 };
 
+// Finalize of the kernel gradients: the fixed-order sum of [nchunks][C][NP]
+// partials and the unfold of eq. (foldgrad), one wavefront per (channel,
+// kernel row).
+struct ReduceArgs {
+    const float* partial;
+    int nchunks, C, k, L;
+    int skip_base;  // do not write the base gradients
+    ParamPtrs p;
+    float* dw0;
+    float* ds0;
+    float* db0;  // nullable
+    float* dlw[kMaxLevels];
+    float* dls[kMaxLevels];
+};
+
 struct FusedArgs {
     const void* in;      // forward: x; backward: dy
     const void* aux;     // backward: x (correlation partner of dy); forward: unused
@@ -154,6 +169,13 @@ struct FusedArgs {
     int mx_seg0[kMixedMaxRounds + 1];
     int mx_ntask[kMixedMaxRounds], mx_out0[kMixedMaxRounds];
     int mx_seg[kMixedMaxSegs];
+    // Forward kernels only: when fin_blocks > 0 the first fin_blocks
+    // workgroups of the grid run the finalize `fin` (four (channel, kernel
+    // row) tasks each, one per wavefront) and the plane work starts at
+    // workgroup fin_blocks; the partials come from an earlier launch on the
+    // stream.
+    int fin_blocks;
+    ReduceArgs fin;
     PlaneGeom g;
 };
 
@@ -183,18 +205,6 @@ struct TinyArgs {
     int skip_base;    // 1: no base path and no base-kernel gradient (coarse sub-problem)
 };
 constexpr int kTinyMaxEdge = 8;
-
-struct ReduceArgs {
-    const float* partial;
-    int nchunks, C, k, L;
-    int skip_base;  // do not write the base gradients
-    ParamPtrs p;
-    float* dw0;
-    float* ds0;
-    float* db0;  // nullable
-    float* dlw[kMaxLevels];
-    float* dls[kMaxLevels];
-};
 
 // Kernel-gradient pass (wtconv_grad.hip): one workgroup owns channel c and a
 // run of nb batch planes of it, PP resident at once, at most one 4x4 pixel

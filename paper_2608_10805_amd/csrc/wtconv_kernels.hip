@@ -6,71 +6,10 @@
 namespace wtc {
 namespace {
 
-// Sum the per-workgroup partials over chunks in increasing order, then unfold
-// eq. (foldgrad): dW = s * G and ds = <G, W>, where G is the gradient of the
-// folded kernel s*W (the level partials carry an extra 4^l from the
-// unnormalised pyramids, removed here exactly); for the base row also the bias
-// terms d b0 = s0 * sum(dy) and b0 * sum(dy) in d s0. One wavefront per
-// (channel, band row); lane t owns tap t (lane k*k the sum of dy); the
-// d(scale) dot product is a fixed-order wavefront reduction.
+// One wavefront per (channel, kernel row).
 __global__ void __launch_bounds__(64) reduce_kernel(const ReduceArgs a)
 {
-    const int KK = a.k * a.k;
-    const int NP = partial_floats_per_channel(a.k, a.L);
-    const int c = blockIdx.x;
-    const int band = blockIdx.y;  // 0 = base, else 1 + (l-1)*4 + q
-    const int t = threadIdx.x;
-    if (band == 0 && a.skip_base) return;
-    float scale, norm;
-    const float* w;
-    float* dw;
-    float* ds;
-    if (band == 0) {
-        scale = a.p.s0[c];
-        norm = 1.f;
-        w = a.p.w0 + (long)c * KK;
-        dw = a.dw0 + (long)c * KK;
-        ds = a.ds0 + c;
-    } else {
-        const int l = (band - 1) / 4 + 1, q = (band - 1) % 4;
-        const int ch = 4 * c + q;
-        scale = a.p.ls[l - 1][ch];
-        norm = __builtin_ldexpf(1.f, -2 * l);
-        w = a.p.lw[l - 1] + (long)ch * KK;
-        dw = a.dlw[l - 1] + (long)ch * KK;
-        ds = a.dls[l - 1] + ch;
-    }
-    float prod = 0.f;
-    if (t < KK) {
-        const float* src = a.partial + (long)c * NP + band * KK + t;
-        const long step = (long)a.C * NP;
-        // chunk order is kept; the loads of a group of 8 chunks are issued
-        // together so that their latencies overlap
-        float G = 0.f;
-        int ch = 0;
-        for (; ch + 8 <= a.nchunks; ch += 8) {
-            float v[8];
-#pragma unroll
-            for (int u = 0; u < 8; ++u) v[u] = src[(long)(ch + u) * step];
-#pragma unroll
-            for (int u = 0; u < 8; ++u) G += v[u];
-        }
-        for (; ch < a.nchunks; ++ch) G += src[(long)ch * step];
-        G *= norm;
-        dw[t] = scale * G;
-        prod = G * w[t];
-    } else if (band == 0 && t == KK) {
-        // folded base bias b~ = s0 * b0: its gradient is the sum of dy, so
-        // d b0 = s0 * sum(dy) and d s0 gains b0 * sum(dy) (eq. foldgrad)
-        const float* src = a.partial + (long)c * NP + (NP - 1);
-        const long step = (long)a.C * NP;
-        float Gb = 0.f;
-        for (int ch = 0; ch < a.nchunks; ++ch) Gb += src[(long)ch * step];
-        if (a.db0) a.db0[c] = scale * Gb;
-        if (a.p.b0) prod = a.p.b0[c] * Gb;
-    }
-    prod = wave_sum(prod);
-    if (t == 0) *ds = prod;
+    reduce_task(a, blockIdx.x, blockIdx.y, threadIdx.x);
 }
 
 // Raw LL carrier of level M (1 <= M <= 6): M levels of the orthonormal

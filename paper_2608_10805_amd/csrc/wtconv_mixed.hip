@@ -123,8 +123,13 @@ __global__ void __launch_bounds__(kThreads) mixed_kernel(const FusedArgs a)
     const PlaneGeom& g = a.g;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int C = a.C;
-    const int c = blockIdx.x % C;
-    const int chunk = blockIdx.x / C;
+    if ((int)blockIdx.x < a.fin_blocks) {
+        fin_wave(a, lane, wave);
+        return;
+    }
+    const int bid = (int)blockIdx.x - a.fin_blocks;
+    const int c = bid % C;
+    const int chunk = bid / C;
     const int b_begin = chunk * a.nb;
     const int b_end = min(a.B, b_begin + a.nb);
     const int L = g.L;

@@ -124,6 +124,52 @@ def test_bias_forward_backward(B, C, H, W, k, L, dtype):
     assert not bad, f"rel errs over {tol}: {bad}"
 
 
+# wtconv_backward runs the finalize of the gradient route's kernel gradients
+# (levels 0..Lf) in extra workgroups at the end of the dx launch; the
+# two-phase calls (wtconv_backward_partials, then wtconv_backward_finalize)
+# run it as a launch of its own. Same sums in the same order: bit-identical
+# results, and the combined call within tolerance of the oracle.
+TWO_PHASE = [
+    (2, 8, 56, 56, 5, 3, "f32"),      # gradient pass, resident dx
+    (2, 4, 28, 28, 5, 4, "f32"),      # coarse gradient route: dx with the coarse carry
+    (3, 4, 12, 12, 5, 3, "f32"),      # the same with a mixed-round dx
+    (10, 3, 14, 14, 5, 2, "bf16"),    # mixed-round dx
+    (2, 2, 56, 56, 5, 5, "f32"),      # split dx
+    (2, 2, 112, 112, 5, 3, "f32"),    # region dx
+    (4, 8, 8, 8, 5, 2, "f32"),        # tiny planes (no gradient pass)
+    (2, 3, 13, 11, 5, 3, "f16"),      # fused backward (no gradient pass)
+]
+
+
+@pytest.mark.parametrize("B,C,H,W,k,L,dtype", TWO_PHASE)
+def test_combined_backward_matches_two_phase(B, C, H, W, k, L, dtype):
+    from paper_2608_10805_amd import binding
+
+    inp, dev = setup(B, C, H, W, k, L, dtype)
+    bk = binding.Backward(dev.x, dev.bw, dev.bs, dev.lw, dev.ls, need_dx=True)
+    outs = lambda: [bk.dx, bk.dbw, bk.dbs] + bk.dlw + bk.dls  # noqa: E731
+    got = []
+    for combined in (True, False):
+        for t in outs():
+            t.fill_(float("nan"))  # a skipped write shows
+        if combined:
+            bk.run(dev.x, dev.dy)
+        else:
+            bk.partials(dev.x, dev.dy)
+            bk.finalize()
+        torch.cuda.synchronize()
+        got.append([t.clone() for t in outs()])
+    names = ["dx", "d_base_w", "d_base_scale"] + [f"d_level_w{l + 1}" for l in range(L)] + \
+        [f"d_level_scale{l + 1}" for l in range(L)]
+    diff = [n for n, a, b in zip(names, *got) if not torch.equal(a, b)]
+    assert not diff, f"combined and two-phase backward differ in {diff}"
+    ref = oracle.backward(inp.x, inp.dy, inp.base_w, inp.base_scale, inp.level_w, inp.level_scale)
+    want = [ref["dx"], ref["d_base_w"], ref["d_base_scale"]] + list(ref["d_level_w"]) + list(ref["d_level_scale"])
+    errs = {n: rel_err(to_np(a), w) for n, a, w in zip(names, got[0], want)}
+    bad = {n: v for n, v in errs.items() if not v < TOL[dtype]}
+    assert not bad, f"rel errs over {TOL[dtype]}: {bad}"
+
+
 def test_bias_autograd_module():
     from paper_2608_10805_amd.autograd import WTConv2d
 
