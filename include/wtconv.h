@@ -230,7 +230,7 @@ wtconv_status wtconv_backward_data(const wtconv_desc* desc, const void* dy, cons
  *   The device is the one `stream` belongs to; the array's address there is
  *   looked up on the first call on that device.
  */
-#define WTCONV_NOALLOC_SCRATCH_BYTES ((size_t)32 << 20)
+#define WTCONV_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
 
 wtconv_status wtconv_backward_noalloc(const wtconv_desc* desc, const void* x, const void* dy,
                                       const float* base_w, const float* base_scale, const float* base_bias,

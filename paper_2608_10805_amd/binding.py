@@ -20,7 +20,7 @@ STATUS = {
 EXPORTS = ["wtconv_forward_workspace_bytes", "wtconv_forward", "wtconv_backward", "wtconv_backward_workspace_bytes",
            "wtconv_backward_partials", "wtconv_backward_finalize", "wtconv_backward_data_workspace_bytes",
            "wtconv_backward_data", "wtconv_backward_noalloc", "wtconv_status_string", "wtconv_version"]
-NOALLOC_SCRATCH_BYTES = 32 << 20  # WTCONV_NOALLOC_SCRATCH_BYTES
+NOALLOC_SCRATCH_BYTES = 64 << 20  # WTCONV_NOALLOC_SCRATCH_BYTES
 MAX_LEVELS = 8
 
 

@@ -610,24 +610,24 @@ int tiny_level(const wtconv_desc& d)
 
 // Whether a resident problem runs its levels above m as a tiny sub-problem
 // (measured on MI355X at the ConvNeXt-T shapes). The split costs one extra
-// read of the input per pass (two in the backward) plus the tiny kernel; it
-// pays when the fused pass loses at least two deep levels (one when those
-// start at level 2, where the fused pass is least efficient), or in the
-// backward pass when it brings the workgroup's LDS under the two-per-CU mark.
+// read of the input per pass (two in the backward) plus the tiny kernel; in
+// the forward it pays when the fused pass loses at least three deep levels,
+// and in the backward pass when it sheds any level above m = 1 or two above
+// a deeper m, or when it brings the workgroup's LDS under the two-per-CU mark.
 // The tiny kernel runs one lane per plane, so with few planes it cannot fill
-// the chip: a forward that would shed only two levels above m = 1 stays whole
-// below B * C = 32768 (B * C / 64 = 512 wavefronts). Measured forwards, k = 5,
-// fp32, split -> whole: 16 x 16 L = 3 at B64 C192 37.7 -> 29.3 us, 12 x 12
-// L = 3 at B128 C192 44.7 -> 37.9 us, 14 x 14 L = 3 at B64 C384 52.8 -> 51.7
-// us; at B128 C384 the split wins (79.9 against 91.3 us). Three or more shed
-// levels still pay at any size (14 x 14 L = 5 at B64 C384: 55 against 78 us).
+// the chip: a forward split at m = 1 (planes of at most 16 x 16, whose whole
+// pass runs in mixed task rounds) needs B * C >= 32768 (B * C / 64 = 512
+// wavefronts). Measured forwards, k = 5, split against whole (us): 14 x 14 at
+// B128 C384, L = 3 70.6 / 64.2 (bf16 72.6 / 63.4), L = 4 71.4 / 87.0, L = 5
+// 72.4 / 96.9; L = 5 at B64 C384 66.1 / 60.3, 16 x 16 at B64 C192 65.3 /
+// 59.4, 12 x 12 at B128 C192 80.1 / 74.6.
 constexpr long kSplitMinPlanes = 32768;
 
 bool want_split(const wtconv_desc& d, bool bwd, int m, int full_lds, int split_lds)
 {
     if (m < 1 || m > 6 || d.L <= m) return false;
     const int deep = d.L - m;
-    if (!bwd) return deep >= (m == 1 ? 2 : 3) && (m > 1 || deep >= 3 || (long)d.B * d.C >= kSplitMinPlanes);
+    if (!bwd) return deep >= 3 && (m > 1 || (long)d.B * d.C >= kSplitMinPlanes);
     const int two_per_cu = kLdsFloatsMax / 2;
     return m == 1 || deep >= 2 || (full_lds > two_per_cu && split_lds <= two_per_cu);
 }
@@ -825,13 +825,17 @@ constexpr int kGradSplitMinShed = 2;
 // 14 x 14 L = 3 623 -> 288 us, L = 5 629 -> 299 us, bf16 L = 3 696 -> 317 us,
 // 12 x 12 and 16 x 16 L = 3 -38 %) and at k = 5 on planes of at most 3 x 3
 // pixel blocks (B128 C192 L = 3: 10 x 10 126 -> 112 us, 11 x 11 140 -> 122 us,
-// 12 x 12 124 -> 109 us; 10 x 10 L = 5 129 -> 124 us). It loses at k = 5 from
-// 13 x 13 on (13 x 13 143 -> 158 us, 14 x 14 B128 C384 202 -> 210 us, 16 x 16
-// B64 C192 99 -> 108 us) and at k = 3 (12 x 12 within 2 %, 14 x 14 +5 %).
-// L = 0 runs the fused backward.
+// 12 x 12 124 -> 109 us; 10 x 10 L = 5 129 -> 124 us). Since dx takes the
+// coarse sub-problem's input gradient as a carry and the finalize runs in the
+// dx launch, it also wins at k = 5 up to 16 x 16 (B128 C384 14 x 14, combined
+// backward: L = 3 189.9 -> 180.2 us, L = 4 191.8 -> 182.9, L = 5 193.9 ->
+// 187.5, bf16 L = 3 203.4 -> 196.6; B64 C384 L = 5 129.6 -> 126.5; B64 C192
+// 16 x 16 L = 3 96.1 -> 92.3, L = 5 100.3 -> 96.2). At k = 3 it does not pay
+// (14 x 14 L = 3 152.9 -> 152.8 us; 12 x 12 within 2 %). L = 0 runs the fused
+// backward.
 bool grad_pass_pays_deep(const wtconv_desc& d)
 {
-    return d.k >= 7 || (d.k == 5 && ceil_to(d.H, 4) <= 12 && ceil_to(d.W, 4) <= 12);
+    return d.k >= 5;
 }
 
 GradExec choose_grad(const wtconv_desc& d)

@@ -1120,14 +1120,25 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(const FusedArgs a)
             // one thread doing both while the other half idles.
             const int n = np * per;
             const bool halves = BWD && have_out && !skip_base && 2 * n <= kThreads;
-            // Forward with more output tiles than threads: the tiles past the
-            // last full round, when they fill at most half a round, are taken
-            // as half tiles (two rows each, two threads per tile), so that
-            // every thread's last round costs half a tile rather than half the
-            // threads paying a whole one.
-            const int rem = n % kThreads;
-            const bool tail_halves = !BWD && !ONE && !RGN && n > kThreads && rem != 0 && 2 * rem <= kThreads;
-            const int nmain = tail_halves ? n - rem : n;
+            // Forward, half tiles (two rows each, two threads per tile) for
+            // the tiles [nmain, n) on the threads [hbase, hbase + 2 (n - nmain)):
+            //  - more tiles than threads: the tiles past the last full round,
+            //    when they fill at most half a round, so that every thread's
+            //    last round costs half a tile rather than half the threads
+            //    paying a whole one;
+            //  - a single round: the tiles of the last, partly filled
+            //    wavefront, when they fill at most half of it, so that this
+            //    wavefront's instructions cost half a tile.
+            int nmain = n, hbase = 0;
+            if constexpr (!BWD && !RGN) {
+                const int rem = n % kThreads, rw = n % 64;
+                if (!ONE && n > kThreads && rem != 0 && 2 * rem <= kThreads) {
+                    nmain = n - rem;
+                } else if (ONE && n <= kThreads && rw != 0 && 2 * rw <= 64) {
+                    nmain = n - rw;
+                    hbase = nmain;
+                }
+            }
             for (int it2 = tid; it2 < (halves ? 2 * n : nmain); it2 += kThreads) {
                 const bool corr_only = halves && it2 >= n;
                 const int it = corr_only ? it2 - n : it2;
@@ -1173,10 +1184,11 @@ __global__ void __launch_bounds__(kThreads) fused_kernel(const FusedArgs a)
                     }
                 }
             }
-            if constexpr (!BWD && !ONE && !RGN) {
-                if (tail_halves && tid < 2 * rem) {
-                    const int hrow = tid & 1;  // rows 2 hrow, 2 hrow + 1 of the tile
-                    const TileIdx ti = tile_at(nmain + (tid >> 1), per, g.r_tiles_l, tx, g.r_tiles_xl, 4);
+            if constexpr (!BWD && !RGN) {
+                const int h = tid - hbase;
+                if (nmain < n && h >= 0 && h < 2 * (n - nmain)) {
+                    const int hrow = h & 1;  // rows 2 hrow, 2 hrow + 1 of the tile
+                    const TileIdx ti = tile_at(nmain + (h >> 1), per, g.r_tiles_l, tx, g.r_tiles_xl, 4);
                     if (ti.i0 < 4 * g.tiles_x) {
                         const float* reg = side_in + ti.p * stride;
                         const long plane = (long)(b0 + ti.p) * C + c;

@@ -100,14 +100,18 @@ def test_forward_workspace_query():
 
 
 def test_forward_split_needs_planes_to_fill_the_chip():
-    # 14 x 14 at L = 3 sheds two levels above the 7 x 7 level-1 grid: the tiny
-    # sub-problem (one lane per plane) runs only with at least 32768 planes,
-    # and then the carrier and the coarse output take workspace
-    assert binding.wtconv_forward_workspace_bytes(make_desc(128, 384, 14, 14, 5, 3)) > 0
-    assert binding.wtconv_forward_workspace_bytes(make_desc(64, 384, 14, 14, 5, 3)) == 0
-    assert binding.wtconv_forward_workspace_bytes(make_desc(64, 192, 16, 16, 5, 3)) == 0
-    # three shed levels still split at any size
-    assert binding.wtconv_forward_workspace_bytes(make_desc(2, 3, 14, 14, 5, 4)) > 0
+    # 14 x 14 planes split at level 1 (7 x 7) only when three or more levels
+    # lie above it and there are at least 32768 planes for the tiny
+    # sub-problem's lanes; then the carrier and the coarse output take
+    # workspace. Otherwise the whole pass runs resident (no workspace).
+    assert binding.wtconv_forward_workspace_bytes(make_desc(128, 384, 14, 14, 5, 4)) > 0
+    assert binding.wtconv_forward_workspace_bytes(make_desc(128, 384, 14, 14, 5, 5)) > 0
+    assert binding.wtconv_forward_workspace_bytes(make_desc(128, 384, 14, 14, 5, 3)) == 0
+    assert binding.wtconv_forward_workspace_bytes(make_desc(64, 384, 14, 14, 5, 5)) == 0
+    assert binding.wtconv_forward_workspace_bytes(make_desc(64, 192, 16, 16, 5, 5)) == 0
+    assert binding.wtconv_forward_workspace_bytes(make_desc(2, 3, 14, 14, 5, 4)) == 0
+    # a split above level 2 (28 x 28 planes) needs only the three levels
+    assert binding.wtconv_forward_workspace_bytes(make_desc(2, 3, 28, 28, 5, 5)) > 0
 
 
 def test_forward_large_plane_workspace_checks():

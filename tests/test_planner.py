@@ -53,7 +53,8 @@ def test_headline_workload_plan(planner):
 
 
 @pytest.mark.parametrize("C,H,L,fwd_mode", [(96, 56, 5, "resident"), (192, 28, 4, "resident"),
-                                            (192, 28, 5, "split"), (384, 14, 3, "split"), (768, 7, 3, "tiny")])
+                                            (192, 28, 5, "split"), (384, 14, 3, "resident"),
+                                            (384, 14, 4, "split"), (768, 7, 3, "tiny")])
 def test_convnext_stage_modes(planner, C, H, L, fwd_mode):
     p = planner(128, C, H, H, 5, L)
     assert p["fwd_mode"] == fwd_mode
@@ -73,12 +74,12 @@ def test_tile_row_padding_keeps_the_busy_wavefronts(planner):
 def test_small_planes_take_mixed_rounds(planner):
     """Planes of at most 16 x 16 run the forward with mixed task rounds: at
     14 x 14 L = 1, eight planes' 128 output tiles and 128 level-1 tiles fill
-    one round of 256 lanes; the split 14 x 14 L = 3 forward's level-1 pass is
+    one round of 256 lanes; the split 14 x 14 L = 4 forward's level-1 pass is
     the same plan. Larger planes keep the fused kernel."""
     p = planner(128, 384, 14, 14, 5, 1)
     assert p["fwd_mode"] == "resident" and p["fwd_mx_rounds"] == 1 and p["fwd_PP"] == 8
     assert sorted(map(tuple, p["fwd_mx_seg"][0])) == [(1, 0, 0, 128)] + [(2, 1, q, 32) for q in range(4)]
-    p = planner(128, 384, 14, 14, 5, 3)
+    p = planner(128, 384, 14, 14, 5, 4)
     assert p["fwd_mode"] == "split" and p["fwd_mx_rounds"] == 1
     for H, L in [(56, 3), (28, 3), (20, 3)]:
         assert planner(64, 96, H, H, 5, L)["fwd_mx_rounds"] == 0
