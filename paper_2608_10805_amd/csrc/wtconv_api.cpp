@@ -16,6 +16,12 @@ using wtc::PlaneGeom;
 
 constexpr int kLdsFloatsMax = 160 * 1024 / 4;     // one compute unit's LDS
 constexpr int kLdsFloatsShared = 64 * 1024 / 4;   // keep >= 2 workgroups per CU when possible
+// A workgroup's LDS is allocated in whole granules of 1280 bytes, 128 per
+// compute unit (measured on MI355X with 256-thread workgroups: three of 53760
+// bytes are resident per CU, of 53888 bytes only two; two of 81920 bytes).
+constexpr int kLdsGranuleFloats = 1280 / 4;
+constexpr int kLdsGranules = 128;
+
 // Workgroups the forward aims for (whole batch chunks of a channel each).
 // Measured on MI355X against 4096 (us per forward, k = 5 fp32): 56 x 56 L3
 // B64 C96 67.6 -> 66.9, 28 x 28 L1 B64 C192 37.2 -> 35.0, 14 x 14 L1 B128 C384
@@ -27,6 +33,12 @@ constexpr int kBackwardTargetWorkgroups = 1536;
 
 int ceil_to(int v, int m) { return (v + m - 1) / m * m; }
 int cdiv(long a, long b) { return (int)((a + b - 1) / b); }
+
+// Workgroups per CU that a workgroup LDS size allows.
+int lds_wgs(long lds_floats)
+{
+    return lds_floats <= 0 ? kLdsGranules : kLdsGranules / cdiv(lds_floats, kLdsGranuleFloats);
+}
 
 // Mixed task rounds (wtconv_mixed.hip) of a forward plan: see pack_mixed().
 struct MixedPlan {
@@ -102,7 +114,7 @@ void set_tile_lanes(PlaneGeom& g, int lanes)
 // Lay out one plane's input array and pyramid for a given number of resident
 // planes. Returns false if a level cannot be tiled within the register caps.
 // rows_from: the first level whose kernel-gradient correlation walks whole
-// rows (the fused backward: 2; the gradient pass: 3, its level 2 goes by tiles);
+// rows (the fused backward and the gradient pass: 2);
 // those levels' rows are padded to whole row chunks.
 // share_halo: the four band arrays of a level share their zero halo rows
 // (band q's last R rows are band q + 1's first R: both are zeros that nothing
@@ -136,7 +148,7 @@ bool layout(const wtconv_desc& d, int PP, bool bwd, PlaneGeom& g, bool t4_deep =
         const int rows = R + std::max(lg.eh + R, h + 1);
         int pitch = std::max(lg.ew - lg.T + window_floats(lg.T, R), R + std::max(lg.ew + R, w + 1));
         if (l >= rows_from) {  // whole-row chunks of the coarse kernel-gradient pass stay inside the row
-            const int cw = w <= 8 ? 8 : 16;
+            const int cw = wtc::row_chunk(w);
             pitch = std::max(pitch, ceil_to(w, cw) - cw + ceil_to(cw + 2 * R, 4));
         }
         lg.pitch = ceil_to(pitch, 4);
@@ -351,7 +363,7 @@ bool make_plan(const wtconv_desc& d, bool bwd, Plan& pl, bool allow_mixed = true
                 const int lds = lds_floats_for(d, bwd, pp, g);
                 if (lds > kLdsFloatsMax) continue;
                 const bool one = single_round(d, pp, g);
-                const int wgs = std::min(forward_wgs(d, one), kLdsFloatsMax / lds);
+                const int wgs = std::min(forward_wgs(d, one), lds_wgs(lds));
                 const double score = tile_use(g, pp) * wgs * (one ? 1.0 : 0.75);
                 if (score >= best) {
                     best = score;
@@ -376,7 +388,7 @@ bool make_plan(const wtconv_desc& d, bool bwd, Plan& pl, bool allow_mixed = true
             for (int l = 3; l <= d.L; ++l) lanes += (long)PP * (gm.lv[l].eh / 4) * (gm.lv[l].ew / 4);
             const int lds = lds_floats_for(d, bwd, PP, gm);
             // if it keeps the workgroups per CU of the unmerged layout
-            if (lanes <= 64 && lds <= kLdsFloatsMax && kLdsFloatsMax / lds >= kLdsFloatsMax / pl.lds_floats) {
+            if (lanes <= 64 && lds <= kLdsFloatsMax && lds_wgs(lds) >= lds_wgs(pl.lds_floats)) {
                 pl.g = gm;
                 pl.lds_floats = lds;
                 pl.merge_deep = 1;
@@ -387,7 +399,7 @@ bool make_plan(const wtconv_desc& d, bool bwd, Plan& pl, bool allow_mixed = true
     // modeled issue (more workgroups per CU on ties), if they beat the plan.
     if (!bwd && allow_mixed && d.L >= 1 && d.H <= kMixedMaxEdge && d.W <= kMixedMaxEdge) {
         const double cost_f = issue_fused(d, PP, pl.g, pl.merge_deep != 0);
-        const int wgs_f = std::min(forward_wgs(d, pl.one_round != 0), kLdsFloatsMax / pl.lds_floats);
+        const int wgs_f = std::min(forward_wgs(d, pl.one_round != 0), lds_wgs(pl.lds_floats));
         const long tiles = (long)ceil_to(d.H, 4) * ceil_to(d.W, 4) / 16;
         const int ppmax = (int)std::max(1L, std::min<long>(d.B, (long)wtc::kMixedMaxRounds * wtc::kThreads / tiles));
         double best = -1.0;
@@ -401,7 +413,7 @@ bool make_plan(const wtconv_desc& d, bool bwd, Plan& pl, bool allow_mixed = true
             const int KP = ceil_to(d.k * d.k, 4);
             const long lds = (long)(1 + 4 * d.L) * KP + (long)pp * g.plane_floats;
             if (lds > kLdsFloatsMax) continue;
-            const int wgs = std::min(mixed_wgs(d, m.rounds), (int)(kLdsFloatsMax / lds));
+            const int wgs = std::min(mixed_wgs(d, m.rounds), lds_wgs(lds));
             const double cost = issue_mixed(d, pp, m);
             if (best < 0 || cost < best || (cost == best && wgs > best_wgs)) {
                 best = cost;
@@ -628,8 +640,7 @@ bool want_split(const wtconv_desc& d, bool bwd, int m, int full_lds, int split_l
     if (m < 1 || m > 6 || d.L <= m) return false;
     const int deep = d.L - m;
     if (!bwd) return deep >= 3 && (m > 1 || (long)d.B * d.C >= kSplitMinPlanes);
-    const int two_per_cu = kLdsFloatsMax / 2;
-    return m == 1 || deep >= 2 || (full_lds > two_per_cu && split_lds <= two_per_cu);
+    return m == 1 || deep >= 2 || (lds_wgs(full_lds) < 2 && lds_wgs(split_lds) >= 2);
 }
 
 Exec choose(const wtconv_desc& d, bool bwd)
@@ -646,7 +657,7 @@ Exec choose(const wtconv_desc& d, bool bwd)
     // resident plane stays ahead (63 x 95 L3 136.6 against 196.9, 84 x 84 L3
     // 37.0 against 61.9).
     if (make_plan(d, bwd, ex.pl) &&
-        (bwd || 2L * ex.pl.lds_floats <= kLdsFloatsMax || !make_region_plan(d, bwd, ex.rp))) {
+        (bwd || lds_wgs(ex.pl.lds_floats) >= 2 || !make_region_plan(d, bwd, ex.rp))) {
         const int m = tiny_level(d);
         if (m >= 1 && d.L > m) {
             wtconv_desc f = d;
@@ -692,7 +703,7 @@ int grad_gc_floats(const wtconv_desc& d)
 
 // Compact dy pyramid next to the x side. A level's array covers the sites its
 // tiles read (tile-aligned extents), the sites the block loads write (levels 1
-// and 2), the sources of the next level's butterflies and, for levels >= 3,
+// and 2), the sources of the next level's butterflies and, for levels >= 2,
 // whole row chunks of the row-wise correlation. Level 1 is stored over the x
 // plane when it fits and the block loads write every site that is read.
 bool grad_layout(const wtconv_desc& d, int PP, GradPlan& gp)
@@ -701,7 +712,7 @@ bool grad_layout(const wtconv_desc& d, int PP, GradPlan& gp)
     // halo ring per batch; it pays for large planes (one resident plane), where
     // it decides the number of workgroups per CU
     const bool may_alias = PP == 1;
-    if (!layout(d, PP, true, gp.g, false, false, 3)) return false;
+    if (!layout(d, PP, true, gp.g, false, false, 2)) return false;
     const PlaneGeom& g = gp.g;
     const long xplane = (long)g.xrows * g.xpitch;
     long extra = 0;
@@ -714,7 +725,7 @@ bool grad_layout(const wtconv_desc& d, int PP, GradPlan& gp)
             rows = std::max(rows, 2 * g.lv[l + 1].h);
             cols = std::max(cols, 2 * g.lv[l + 1].w);
         }
-        if (l >= 3) cols = std::max(cols, ceil_to(lg.w, lg.w <= 8 ? 8 : 16));
+        if (l >= 2) cols = std::max(cols, ceil_to(lg.w, wtc::row_chunk(lg.w)));
         const int pitch = ceil_to(cols, 4);
         const long size = 4L * rows * pitch;
         gp.dy_pitch[l] = pitch;
@@ -772,7 +783,7 @@ bool make_grad_plan(const wtconv_desc& d, GradPlan& gp)
         for (int pp = 1; pp <= maxpp; ++pp) {
             GradPlan c;
             if (!grad_layout(d, pp, c)) continue;
-            const int wgs = std::min(3, kLdsFloatsMax / c.lds_floats);
+            const int wgs = std::min(3, lds_wgs(c.lds_floats));
             const double score = (double)pp * per / wtc::kThreads * wgs;
             if (score >= best) {
                 best = score;
@@ -789,7 +800,7 @@ bool make_grad_plan(const wtconv_desc& d, GradPlan& gp)
     // down so that the grid fits the slots: rounding 512 / 192 up to 3 chunks
     // left a second round of 64 workgroups (28 x 28, L = 3: 150 -> 143 us per
     // backward at B = 64, 289 -> 250 us at B = 128 with 2 chunks).
-    const int wgs_per_cu = std::max(1, std::min(3, kLdsFloatsMax / gp.lds_floats));
+    const int wgs_per_cu = std::max(1, std::min(3, lds_wgs(gp.lds_floats)));
     const int slots = 256 * wgs_per_cu;
     const int chunks = std::max(1, std::min(d.B, slots / d.C));
     gp.nb = ceil_to(cdiv(d.B, chunks), gp.PP);

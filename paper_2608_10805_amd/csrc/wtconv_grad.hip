@@ -21,8 +21,9 @@
 //   3. dy levels 1-2 written to a compact pyramid (level 1 over the x plane,
 //      which is not read any more, when it fits there), deeper dy levels by the
 //      butterfly;
-//   4. level correlations, one band per wavefront: levels 1 and 2 over T x T
-//      site tiles into per-lane registers, deeper levels row by row.
+//   4. level correlations, one band per wavefront: level 1 over T x T site
+//      tiles into per-lane registers, level 2 row by row into per-lane
+//      registers, deeper levels row by row into LDS.
 // The sums stay in registers across the workgroup's planes and are reduced
 // once, in a fixed order, into the workgroup's partials (the layout of the
 // fused backward, so the same finalize applies). Both pyramids are
@@ -113,42 +114,64 @@ DEV void grad_row_chunk(const float* __restrict__ dr, const float* __restrict__ 
 }
 
 // Level correlation of band q of a deep level, by rows: lane (tap row p, row
-// group rg) keeps the K sums G[p][0..K-1] over the site rows j = rg, rg + NG,
-// ... of every resident plane, walking each row in CW-site chunks; sites past
-// the grid width are zero on both sides. The row groups are summed with a
-// fixed xor tree and added to one LDS slot per tap (only this wavefront
-// touches the slot), so the result does not depend on timing.
+// group rg) accumulates into acc the K sums G[p][0..K-1] over the site rows
+// j = rg, rg + NG, ... of every resident plane, walking each row in chunks of
+// row_chunk(w) sites; sites past the grid width are zero on both sides.
+// Lanes past the K tap rows read a valid row; their sums are dropped.
 template <int K>
-DEV void grad_band_rows(const float* __restrict__ region0, int stride, const LevelGeom& xl, DyLevel dl, int q,
-                        int np, float* __restrict__ slot, int lane)
+constexpr int rows_lanes() { return K <= 1 ? 1 : (K <= 2 ? 2 : (K <= 4 ? 4 : 8)); }  // lanes per row group
+
+template <int K>
+DEV void grad_rows_acc(const float* __restrict__ region0, int stride, const LevelGeom& xl, DyLevel dl, int q,
+                       int np, float (&acc)[K], int lane)
 {
     constexpr int R = K / 2;
-    constexpr int PS = K <= 1 ? 1 : (K <= 2 ? 2 : (K <= 4 ? 4 : 8));  // lanes per row group
-    constexpr int NG = 64 / PS;                                        // row groups
+    constexpr int PS = rows_lanes<K>();
+    constexpr int NG = 64 / PS;  // row groups
     const int p = lane & (PS - 1), rg = lane / PS;
-    const bool active = p < K;
-    const int prow = active ? p : R;  // inactive lanes read a valid row and are dropped below
-    float acc[K];
-#pragma unroll
-    for (int t = 0; t < K; ++t) acc[t] = 0.f;
+    const int prow = p < K ? p : R;
+    const bool c8 = row_chunk(xl.w) == 8;
     for (int pp = 0; pp < np; ++pp) {
         const float* db = region0 + pp * stride + dl.off + q * dl.band;
         const float* xb = region0 + pp * stride + xl.off + q * xl.band;
         for (int j = rg; j < xl.h; j += NG) {
             const float* dr = db + j * dl.pitch;           // site row j, column 0
             const float* xr = xb + (j + prow) * xl.pitch;  // site row j + p - R, array column 0
-            if (xl.w <= 8) {
-                grad_row_chunk<K, 8>(dr, xr, acc);
+            if (c8) {
+                for (int i0 = 0; i0 < xl.w; i0 += 8) grad_row_chunk<K, 8>(dr + i0, xr + i0, acc);
             } else {
                 for (int i0 = 0; i0 < xl.w; i0 += 16) grad_row_chunk<K, 16>(dr + i0, xr + i0, acc);
             }
         }
     }
+}
+
+// The row groups' sums of grad_rows_acc added with a fixed xor tree: lane
+// p < K of every row group then holds G[p][0..K-1].
+template <int K>
+DEV void rows_reduce(float (&acc)[K])
+{
 #pragma unroll
     for (int t = 0; t < K; ++t)
 #pragma unroll
-        for (int m = PS; m < 64; m <<= 1) acc[t] += __shfl_xor(acc[t], m, 64);
-    if (rg == 0 && active) {
+        for (int m = rows_lanes<K>(); m < 64; m <<= 1) acc[t] += __shfl_xor(acc[t], m, 64);
+}
+
+// A deeper level (l >= 3): this batch's sums added to one LDS slot per tap
+// (only this wavefront touches the slot), so the result does not depend on
+// timing.
+template <int K>
+DEV void grad_band_rows(const float* __restrict__ region0, int stride, const LevelGeom& xl, DyLevel dl, int q,
+                        int np, float* __restrict__ slot, int lane)
+{
+    constexpr int PS = rows_lanes<K>();
+    const int p = lane & (PS - 1), rg = lane / PS;
+    float acc[K];
+#pragma unroll
+    for (int t = 0; t < K; ++t) acc[t] = 0.f;
+    grad_rows_acc<K>(region0, stride, xl, dl, q, np, acc, lane);
+    rows_reduce<K>(acc);
+    if (rg == 0 && p < K) {
 #pragma unroll
         for (int t = 0; t < K; ++t) slot[p * K + t] += acc[t];
     }
@@ -220,9 +243,13 @@ __global__ void __launch_bounds__(kThreads, grad_waves_per_simd<K>()) grad_kerne
     for (int i = tid; i < a.lds_floats / 4; i += kThreads) lds4[i] = make_float4(0.f, 0.f, 0.f, 0.f);
     __syncthreads();
 
-    float g0[KK], g1[KK], g2[KK];
+    // kernel-gradient sums: base and level 1 per lane over its tiles; level 2
+    // per lane (tap row, row group) over its rows (the row-wise correlation)
+    float g0[KK], g1[KK], g2[K];
 #pragma unroll
-    for (int t = 0; t < KK; ++t) g0[t] = g1[t] = g2[t] = 0.f;
+    for (int t = 0; t < KK; ++t) g0[t] = g1[t] = 0.f;
+#pragma unroll
+    for (int t = 0; t < K; ++t) g2[t] = 0.f;
     float gdy = 0.f;  // sum of dy over the workgroup's pixels (bias gradient)
 
     const int per = g.tiles_x * g.tiles_y;
@@ -231,7 +258,7 @@ __global__ void __launch_bounds__(kThreads, grad_waves_per_simd<K>()) grad_kerne
         // Per-thread LDS addresses depend only on the thread index; taking it
         // through an opaque copy inside this loop keeps the compiler from
         // hoisting them out of the loop, which would hold them across it next
-        // to the 3 k^2 kernel-gradient sums and spill them (k <= 5; at k = 7
+        // to the kernel-gradient sums and spill them (k <= 5; at k = 7
         // the sums alone nearly fill the registers and hoisting spills less).
         int tl = threadIdx.x;
         if constexpr (K <= 5) asm volatile("" : "+v"(tl));
@@ -359,14 +386,16 @@ __global__ void __launch_bounds__(kThreads, grad_waves_per_simd<K>()) grad_kerne
             __syncthreads();
         }
 
-        // 4. level correlations, band q per wavefront
+        // 4. level correlations, band q per wavefront: level 1 over register
+        //    tiles, level 2 row by row into per-lane sums, the deeper levels
+        //    row by row into their LDS slots
         for (int l = 1; l <= L; ++l) {
             const LevelGeom& xl = g.lv[l];
             const DyLevel dl = {a.dy_off[l], a.dy_pitch[l], a.dy_band[l]};
             if (l == 1)
                 grad_band<K>(planes, stride, xl, dl, q, np, g1, ll);
             else if (l == 2)
-                grad_band<K>(planes, stride, xl, dl, q, np, g2, ll);
+                grad_rows_acc<K>(planes, stride, xl, dl, q, np, g2, ll);
             else
                 grad_band_rows<K>(planes, stride, xl, dl, q, np, gco + ((l - 3) * 4 + q) * KK, ll);
         }
@@ -380,11 +409,18 @@ __global__ void __launch_bounds__(kThreads, grad_waves_per_simd<K>()) grad_kerne
     for (int t = 0; t < KK; ++t) {
         const float v0 = wave_sum(g0[t]);
         const float v1 = wave_sum(g1[t]);
-        const float v2 = wave_sum(g2[t]);
         if (lane == 0) {
             red[wave * KK + t] = v0;
             red[(kWaves + wave) * KK + t] = v1;
-            red[(2 * kWaves + wave) * KK + t] = v2;
+        }
+    }
+    rows_reduce<K>(g2);
+    {
+        constexpr int PS = rows_lanes<K>();
+        const int p = lane & (PS - 1);
+        if (lane < PS && p < K) {
+#pragma unroll
+            for (int t = 0; t < K; ++t) red[(2 * kWaves + wave) * KK + p * K + t] = g2[t];
         }
     }
     const float vdy = wave_sum(gdy);
@@ -396,7 +432,7 @@ __global__ void __launch_bounds__(kThreads, grad_waves_per_simd<K>()) grad_kerne
         const float* r = red + 3 * kWaves * KK;
         dst[NP - 1] = ((r[0] + r[1]) + r[2]) + r[3];
     }
-    // levels 1-2: band q's sums came from wavefront q
+    // levels 1-2: band q's sums came from wavefront q; deeper levels from the slots
     for (int i = tid; i < 4 * KK * min(L, 2); i += kThreads) dst[KK + i] = red[kWaves * KK + i];
     for (int i = tid; i < 4 * KK * (L - 2); i += kThreads) dst[KK + 8 * KK + i] = gco[i];
 }
