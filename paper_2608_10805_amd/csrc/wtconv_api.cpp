@@ -1153,11 +1153,21 @@ wtconv_status forward_impl(const wtconv_desc& d, const void* x, const wtc::Param
     return hip_status(wtc::launch_forward(d.k, d.dtype, a, grid, stream));
 }
 
+// cx, cdy (nullable): also write the level-cm (1 or 2) carriers of x and dy
+// there, as carrier() would.
 wtconv_status grad_pass(const wtconv_desc& d, const GradExec& ge, const void* x, const void* dy, float* partial,
-                        int skip_base, hipStream_t stream)
+                        int skip_base, hipStream_t stream, void* cx = nullptr, void* cdy = nullptr, int cm = 0)
 {
     wtc::GradArgs a;
     memset(&a, 0, sizeof(a));
+    if (cx) {
+        const wtconv_desc cd = coarse_desc(d, cm);
+        a.cx = cx;
+        a.cdy = cdy;
+        a.cm = cm;
+        a.cH = cd.H;
+        a.cW = cd.W;
+    }
     a.x = x;
     a.dy = dy;
     a.partial = partial;
@@ -1209,19 +1219,27 @@ wtconv_status partials_impl(const wtconv_desc& d, const void* x, const void* dy,
         if (ge.coarse) {
             // kernel gradients of levels Lf+1..L (and the coarse part of dx):
             // the coarse sub-problem's, on the level-Lf carriers of x and dy
-            // (no base path)
+            // (no base path). At Lf <= 2 the gradient pass forms the carriers
+            // from the blocks it loads anyway (a block covers whole carrier
+            // sites), instead of two carrier launches that read x and dy again.
             const size_t n1 = level_bytes(d, ge.Lf);
             void* x1 = ws + part;
             void* dy1 = ws + part + n1;
             dx1 = dx_carry ? ws + part + 2 * n1 : nullptr;
-            st = carrier(d, ge.Lf, x, x1, stream);
-            if (st == WTCONV_OK) st = carrier(d, ge.Lf, dy, dy1, stream);
+            const bool in_pass = ge.Lf <= 2 && ge.gp.rounds == 1;
+            if (in_pass) {
+                st = grad_pass(d, ge, x, dy, reinterpret_cast<float*>(ws), skip_base, stream, x1, dy1, ge.Lf);
+            } else {
+                st = carrier(d, ge.Lf, x, x1, stream);
+                if (st == WTCONV_OK) st = carrier(d, ge.Lf, dy, dy1, stream);
+            }
             if (st == WTCONV_OK)
                 st = partials_impl(coarse_desc(d, ge.Lf), x1, dy1, shift_params(p, ge.Lf), dx1, ws + part + 3 * n1,
                                    1, stream);
-            if (st != WTCONV_OK) return st;
+            if (st == WTCONV_OK && !in_pass) st = grad_pass(d, ge, x, dy, reinterpret_cast<float*>(ws), skip_base, stream);
+        } else {
+            st = grad_pass(d, ge, x, dy, reinterpret_cast<float*>(ws), skip_base, stream);
         }
-        st = grad_pass(d, ge, x, dy, reinterpret_cast<float*>(ws), skip_base, stream);
         if (st != WTCONV_OK || !dx) return st;
         FinJob fin = {};
         if (gr) fin.r = reduce_args(d, ge.Lf, ge.gp.nchunks, p, *gr, ws, skip_base);

@@ -202,6 +202,36 @@ DEV void zero_x_ring(float* __restrict__ reg, const PlaneGeom& g, int R, float r
     }
 }
 
+// The level-M (M = 1, 2) raw LL carrier sites of one 4x4 pixel block at
+// (y0, x0) of a plane: 2^-M times each 2^M x 2^M block sum (pixels outside the
+// plane are the zeros the block loads hold), summed in the carrier kernel's
+// order (pairs within a row, then rows in order) and rounded once to the
+// storage type; sites past the H1 x W1 grid are not written.
+template <typename ST>
+DEV void write_carrier(ST* __restrict__ out, int H1, int W1, int M, int y0, int x0, const float (&v)[4][4])
+{
+    if (M == 1) {
+#pragma unroll
+        for (int a = 0; a < 2; ++a)
+#pragma unroll
+            for (int b = 0; b < 2; ++b) {
+                const int j = (y0 >> 1) + a, i = (x0 >> 1) + b;
+                if (j < H1 && i < W1) {
+                    const float s = (v[2 * a][2 * b] + v[2 * a][2 * b + 1]) + (v[2 * a + 1][2 * b] + v[2 * a + 1][2 * b + 1]);
+                    out[(long)j * W1 + i] = from_f32<ST>(__builtin_ldexpf(s, -1));
+                }
+            }
+    } else {
+        const int j = y0 >> 2, i = x0 >> 2;
+        if (j < H1 && i < W1) {
+            float s = 0.f;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) s += (v[r][0] + v[r][1]) + (v[r][2] + v[r][3]);
+            out[(long)j * W1 + i] = from_f32<ST>(__builtin_ldexpf(s, -2));
+        }
+    }
+}
+
 // At least three waves per SIMD (168 VGPRs) for k <= 5: with three
 // workgroups per CU (the LDS budget of the planner) each SIMD then holds one
 // wavefront of each.
@@ -312,6 +342,11 @@ __global__ void __launch_bounds__(kThreads, grad_waves_per_simd<K>()) grad_kerne
                 fetch_block<ST>(xs + plane * HW, g.H, g.W, ti.j0, ti.i0, vw, v);
                 store_block<K>(v, planes + ti.p * stride, g, ti.j0, ti.i0);
                 fetch_block<ST>(dys + plane * HW, g.H, g.W, ti.j0, ti.i0, vw, dyb);
+                if (a.cx) {
+                    const long co = plane * a.cH * a.cW;
+                    write_carrier<ST>(reinterpret_cast<ST*>(a.cx) + co, a.cH, a.cW, a.cm, ti.j0, ti.i0, v);
+                    write_carrier<ST>(reinterpret_cast<ST*>(a.cdy) + co, a.cH, a.cW, a.cm, ti.j0, ti.i0, dyb);
+                }
             }
             __syncthreads();
 

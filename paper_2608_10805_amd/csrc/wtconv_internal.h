@@ -234,6 +234,13 @@ struct GradArgs {
     // read as zero; tail0 == tail1 when unused
     int tail0, tail1;
     int dy_off[kMaxLevels + 1], dy_pitch[kMaxLevels + 1], dy_band[kMaxLevels + 1];
+    // Optional (one block round only, rounds == 1): the raw LL carriers of x
+    // and dy at level cm (1 or 2) for a coarse sub-problem, [B][C][cH][cW] in
+    // the storage type, as the carrier kernel writes them (same sums in the
+    // same order); null when not wanted.
+    void* cx;
+    void* cdy;
+    int cm, cH, cW;
     PlaneGeom g;
 };
 
