@@ -597,7 +597,10 @@ DEV void corr_band_rows(const float* __restrict__ dz0, const float* __restrict__
         for (int j = rg; j < lg.h; j += NG) {
             const float* dzr = dzb + (j + R) * lg.pitch;  // array column 0 of site row j
             const float* yr = yb + (j + prow) * lg.pitch;  // site row j + p - R
-            if (row_chunk(lg.w) == 8) {
+            const int cw = row_chunk(lg.w);
+            if (cw == 4) {
+                corr_row_chunk<K, 4>(dzr, yr, acc);
+            } else if (cw == 8) {
                 for (int i0 = 0; i0 < lg.w; i0 += 8) corr_row_chunk<K, 8>(dzr + i0, yr + i0, acc);
             } else {
                 for (int i0 = 0; i0 < lg.w; i0 += 16) corr_row_chunk<K, 16>(dzr + i0, yr + i0, acc);

@@ -130,14 +130,16 @@ DEV void grad_rows_acc(const float* __restrict__ region0, int stride, const Leve
     constexpr int NG = 64 / PS;  // row groups
     const int p = lane & (PS - 1), rg = lane / PS;
     const int prow = p < K ? p : R;
-    const bool c8 = row_chunk(xl.w) == 8;
+    const int cw = row_chunk(xl.w);
     for (int pp = 0; pp < np; ++pp) {
         const float* db = region0 + pp * stride + dl.off + q * dl.band;
         const float* xb = region0 + pp * stride + xl.off + q * xl.band;
         for (int j = rg; j < xl.h; j += NG) {
             const float* dr = db + j * dl.pitch;           // site row j, column 0
             const float* xr = xb + (j + prow) * xl.pitch;  // site row j + p - R, array column 0
-            if (c8) {
+            if (cw == 4) {
+                grad_row_chunk<K, 4>(dr, xr, acc);
+            } else if (cw == 8) {
                 for (int i0 = 0; i0 < xl.w; i0 += 8) grad_row_chunk<K, 8>(dr + i0, xr + i0, acc);
             } else {
                 for (int i0 = 0; i0 < xl.w; i0 += 16) grad_row_chunk<K, 16>(dr + i0, xr + i0, acc);

@@ -250,8 +250,12 @@ struct GradArgs {
 __host__ __device__ inline int partial_floats_per_channel(int k, int L) { return k * k * (1 + 4 * L) + 1; }
 
 // Sites per chunk of the row-wise kernel-gradient correlation of a w-site-wide
-// level: 8 or 16, whichever pads the row less (16 on ties: fewer chunks).
-__host__ __device__ inline int row_chunk(int w) { return ((w + 7) / 8 * 8 < (w + 15) / 16 * 16) ? 8 : 16; }
+// level: 4 up to 4 sites, else 8 or 16, whichever pads the row less (16 on
+// ties: fewer chunks).
+__host__ __device__ inline int row_chunk(int w)
+{
+    return w <= 4 ? 4 : (((w + 7) / 8 * 8 < (w + 15) / 16 * 16) ? 8 : 16);
+}
 
 hipError_t launch_forward(int k, wtconv_dtype dt, const FusedArgs& a, int grid, hipStream_t s);
 // Workgroups per CU that the registers of the forward kernel for (k, dt,
