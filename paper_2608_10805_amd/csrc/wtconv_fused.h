@@ -550,8 +550,9 @@ DEV void corr_band(const float* dz0, const float* y0, int stride, const LevelGeo
 }
 
 // Kernel-gradient correlation of one coarse subband, by rows: lane (tap row p,
-// row group rg) keeps the K sums G[p][0..K-1] for the site rows j = rg, rg+NG,
-// ... and walks each row in CW-site chunks read with 16-byte loads:
+// row group rg) keeps the K sums G[p][0..K-1] for the rows rg, rg+NG, ... of
+// the list of every resident plane's site rows and walks each row in CW-site
+// chunks read with 16-byte loads:
 //   G[p][t] += sum_i dZ[j][i] * Y[j+p-R][i+t-R].
 // Reads past the grid width hit zeros (ragged sites / halo), which contribute
 // nothing. The row groups are then summed with a fixed xor tree and added to
@@ -591,20 +592,20 @@ DEV void corr_band_rows(const float* __restrict__ dz0, const float* __restrict__
     float acc[K];
 #pragma unroll
     for (int t = 0; t < K; ++t) acc[t] = 0.f;
-    for (int pp = 0; pp < np; ++pp) {
-        const float* dzb = dz0 + pp * stride + lg.off + q * lg.band;
-        const float* yb = y0 + pp * stride + lg.off + q * lg.band;
-        for (int j = rg; j < lg.h; j += NG) {
-            const float* dzr = dzb + (j + R) * lg.pitch;  // array column 0 of site row j
-            const float* yr = yb + (j + prow) * lg.pitch;  // site row j + p - R
-            const int cw = row_chunk(lg.w);
-            if (cw == 4) {
-                corr_row_chunk<K, 4>(dzr, yr, acc);
-            } else if (cw == 8) {
-                for (int i0 = 0; i0 < lg.w; i0 += 8) corr_row_chunk<K, 8>(dzr + i0, yr + i0, acc);
-            } else {
-                for (int i0 = 0; i0 < lg.w; i0 += 16) corr_row_chunk<K, 16>(dzr + i0, yr + i0, acc);
-            }
+    // the (plane, row) pairs of the resident planes are dealt over the row
+    // groups as one flat list, so small grids keep every group busy
+    const int cw = row_chunk(lg.w);
+    const float r_h = 1.0f / (float)lg.h;
+    for (int e = rg; e < np * lg.h; e += NG) {
+        const int pp = fdiv(e, r_h), j = e - pp * lg.h;
+        const float* dzr = dz0 + pp * stride + lg.off + q * lg.band + (j + R) * lg.pitch;  // array column 0, site row j
+        const float* yr = y0 + pp * stride + lg.off + q * lg.band + (j + prow) * lg.pitch;  // site row j + p - R
+        if (cw == 4) {
+            corr_row_chunk<K, 4>(dzr, yr, acc);
+        } else if (cw == 8) {
+            for (int i0 = 0; i0 < lg.w; i0 += 8) corr_row_chunk<K, 8>(dzr + i0, yr + i0, acc);
+        } else {
+            for (int i0 = 0; i0 < lg.w; i0 += 16) corr_row_chunk<K, 16>(dzr + i0, yr + i0, acc);
         }
     }
 #pragma unroll

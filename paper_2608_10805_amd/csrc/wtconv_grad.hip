@@ -115,8 +115,9 @@ DEV void grad_row_chunk(const float* __restrict__ dr, const float* __restrict__ 
 
 // Level correlation of band q of a deep level, by rows: lane (tap row p, row
 // group rg) accumulates into acc the K sums G[p][0..K-1] over the site rows
-// j = rg, rg + NG, ... of every resident plane, walking each row in chunks of
-// row_chunk(w) sites; sites past the grid width are zero on both sides.
+// rg, rg + NG, ... of the list of every resident plane's rows, walking each
+// row in chunks of row_chunk(w) sites; sites past the grid width are zero on
+// both sides.
 // Lanes past the K tap rows read a valid row; their sums are dropped.
 template <int K>
 constexpr int rows_lanes() { return K <= 1 ? 1 : (K <= 2 ? 2 : (K <= 4 ? 4 : 8)); }  // lanes per row group
@@ -131,19 +132,19 @@ DEV void grad_rows_acc(const float* __restrict__ region0, int stride, const Leve
     const int p = lane & (PS - 1), rg = lane / PS;
     const int prow = p < K ? p : R;
     const int cw = row_chunk(xl.w);
-    for (int pp = 0; pp < np; ++pp) {
-        const float* db = region0 + pp * stride + dl.off + q * dl.band;
-        const float* xb = region0 + pp * stride + xl.off + q * xl.band;
-        for (int j = rg; j < xl.h; j += NG) {
-            const float* dr = db + j * dl.pitch;           // site row j, column 0
-            const float* xr = xb + (j + prow) * xl.pitch;  // site row j + p - R, array column 0
-            if (cw == 4) {
-                grad_row_chunk<K, 4>(dr, xr, acc);
-            } else if (cw == 8) {
-                for (int i0 = 0; i0 < xl.w; i0 += 8) grad_row_chunk<K, 8>(dr + i0, xr + i0, acc);
-            } else {
-                for (int i0 = 0; i0 < xl.w; i0 += 16) grad_row_chunk<K, 16>(dr + i0, xr + i0, acc);
-            }
+    // the (plane, row) pairs of the resident planes are dealt over the row
+    // groups as one flat list, so small grids keep every group busy
+    const float r_h = 1.0f / (float)xl.h;
+    for (int e = rg; e < np * xl.h; e += NG) {
+        const int pp = fdiv(e, r_h), j = e - pp * xl.h;
+        const float* dr = region0 + pp * stride + dl.off + q * dl.band + j * dl.pitch;  // site row j, column 0
+        const float* xr = region0 + pp * stride + xl.off + q * xl.band + (j + prow) * xl.pitch;  // row j + p - R
+        if (cw == 4) {
+            grad_row_chunk<K, 4>(dr, xr, acc);
+        } else if (cw == 8) {
+            for (int i0 = 0; i0 < xl.w; i0 += 8) grad_row_chunk<K, 8>(dr + i0, xr + i0, acc);
+        } else {
+            for (int i0 = 0; i0 < xl.w; i0 += 16) grad_row_chunk<K, 16>(dr + i0, xr + i0, acc);
         }
     }
 }
