@@ -30,6 +30,13 @@ constexpr int kLdsGranules = 128;
 // planes gain more but 56 x 56 loses 19 % (too few workgroups for the tail).
 constexpr int kForwardTargetWorkgroups = 2048;
 constexpr int kBackwardTargetWorkgroups = 1536;
+// The region backward (planes beyond one CU's LDS) aims for fewer, longer
+// workgroups: each carries a larger working set, and more batch planes per
+// workgroup amortise its set-up. Measured (combined backward, us, 1536 ->
+// 768): 224 x 224 B16 C64 L1 401.1 -> 382.3, L3 682.9 -> 669.9; B8 C32 k = 3
+// 128 x 128 L1 67.6 -> 59.1, 256 x 256 L3 292.6 -> 283.4; 512 x 512 within
+// 0.1 %. 3072 was slower everywhere (up to +13 %).
+constexpr int kRegionBackwardTargetWorkgroups = 768;
 
 int ceil_to(int v, int m) { return (v + m - 1) / m * m; }
 int cdiv(long a, long b) { return (int)((a + b - 1) / b); }
@@ -583,7 +590,7 @@ bool make_region_plan(const wtconv_desc& d, bool bwd, RegionPlan& rp)
         rp.ntx = cdiv(d.W, T);
         rp.nty = cdiv(d.H, T);
         const long ntiles = (long)rp.ntx * rp.nty;
-        const int target = bwd ? kBackwardTargetWorkgroups : kForwardTargetWorkgroups;
+        const int target = bwd ? kRegionBackwardTargetWorkgroups : kForwardTargetWorkgroups;
         const long chunks_target = std::max(1L, (target + d.C * ntiles - 1) / (d.C * ntiles));
         pl.nb = (int)((d.B + chunks_target - 1) / chunks_target);
         pl.nchunks = cdiv(d.B, pl.nb);
