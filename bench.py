@@ -484,7 +484,7 @@ def kernel_source_hash():
 # Kernels of the headline step, by the symbol prefix rocprofv3 reports: the
 # fused forward kernel runs twice per step (y, and dx on dy with rotated
 # kernels), the kernel-gradient pass and the finalize once.
-STEP_KERNELS = {"forward": "fused_kernel<5, float, false, true, false>", "grad": "grad_kernel<5, float, false>",
+STEP_KERNELS = {"forward": "fused_kernel<5, float, false, true, false>", "grad": "grad_kernel<5, float, false, false>",
                 "finalize": "reduce_kernel"}
 
 

@@ -705,7 +705,8 @@ struct GradPlan {
 
 int grad_gc_floats(const wtconv_desc& d)
 {
-    return d.L > 2 ? ceil_to((d.L - 2) * 4 * d.k * d.k, 4) : 0;
+    const int rl = wtc::grad_reg_levels(d.L >= 4);
+    return d.L > rl ? ceil_to((d.L - rl) * 4 * d.k * d.k, 4) : 0;
 }
 
 // Compact dy pyramid next to the x side. A level's array covers the sites its
@@ -758,7 +759,7 @@ bool grad_layout(const wtconv_desc& d, int PP, GradPlan& gp)
         if (g.plane_floats + extra > (1L << 28)) return false;
     }
     gp.stride = (int)(g.plane_floats + extra);
-    const long planes = std::max((long)PP * gp.stride, 12L * d.k * d.k + 4);  // also the final reduction scratch
+    const long planes = std::max((long)PP * gp.stride, 24L * d.k * d.k + 4);  // also the final reduction scratch
     const long total = grad_gc_floats(d) + ceil_to((int)std::min(planes, 1L << 28), 4);
     if (total > kLdsFloatsMax) return false;
     gp.lds_floats = (int)total;

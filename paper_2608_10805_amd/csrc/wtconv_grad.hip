@@ -243,7 +243,10 @@ constexpr int grad_waves_per_simd() { return K <= 5 ? 3 : 2; }
 
 // MR: planes with more 4x4 blocks than threads, one resident plane, block
 // rounds (a separate instantiation keeps the one-round kernel's registers).
-template <int K, typename ST, bool MR>
+// DR: L >= 4; levels 3..5 keep their sums in registers too (another 3k per
+// lane, an instantiation of its own so that shallower pyramids keep the
+// smaller register budget).
+template <int K, typename ST, bool MR, bool DR>
 __global__ void __launch_bounds__(kThreads, grad_waves_per_simd<K>()) grad_kernel(const GradArgs a)
 {
     constexpr int R = K / 2, KK = K * K;
@@ -265,7 +268,8 @@ __global__ void __launch_bounds__(kThreads, grad_waves_per_simd<K>()) grad_kerne
     const int q = wave;                              // the subband this wavefront correlates
 
     // LDS: [deep-level kernel-gradient sums][plane regions]
-    const int gc_floats = L > 2 ? ceil4c((L - 2) * 4 * KK) : 0;
+    constexpr int RL = grad_reg_levels(DR);  // levels whose sums stay in registers
+    const int gc_floats = L > RL ? ceil4c((L - RL) * 4 * KK) : 0;
     float* gco = lds;
     float* planes = lds + gc_floats;
     const int stride = a.stride;
@@ -278,11 +282,14 @@ __global__ void __launch_bounds__(kThreads, grad_waves_per_simd<K>()) grad_kerne
 
     // kernel-gradient sums: base and level 1 per lane over its tiles; level 2
     // per lane (tap row, row group) over its rows (the row-wise correlation)
-    float g0[KK], g1[KK], g2[K];
+    constexpr int KD = DR ? K : 1;
+    float g0[KK], g1[KK], g2[K], g3[KD], g4[KD], g5[KD];
 #pragma unroll
     for (int t = 0; t < KK; ++t) g0[t] = g1[t] = 0.f;
 #pragma unroll
     for (int t = 0; t < K; ++t) g2[t] = 0.f;
+#pragma unroll
+    for (int t = 0; t < KD; ++t) g3[t] = g4[t] = g5[t] = 0.f;
     float gdy = 0.f;  // sum of dy over the workgroup's pixels (bias gradient)
 
     const int per = g.tiles_x * g.tiles_y;
@@ -434,8 +441,18 @@ __global__ void __launch_bounds__(kThreads, grad_waves_per_simd<K>()) grad_kerne
                 grad_band<K>(planes, stride, xl, dl, q, np, g1, ll);
             else if (l == 2)
                 grad_rows_acc<K>(planes, stride, xl, dl, q, np, g2, ll);
-            else
-                grad_band_rows<K>(planes, stride, xl, dl, q, np, gco + ((l - 3) * 4 + q) * KK, ll);
+            else if (DR && l <= RL) {
+                if constexpr (DR) {
+                    if (l == 3)
+                        grad_rows_acc<K>(planes, stride, xl, dl, q, np, g3, ll);
+                    else if (l == 4)
+                        grad_rows_acc<K>(planes, stride, xl, dl, q, np, g4, ll);
+                    else
+                        grad_rows_acc<K>(planes, stride, xl, dl, q, np, g5, ll);
+                }
+            } else {
+                grad_band_rows<K>(planes, stride, xl, dl, q, np, gco + ((l - RL - 1) * 4 + q) * KK, ll);
+            }
         }
         __syncthreads();
     }
@@ -453,36 +470,48 @@ __global__ void __launch_bounds__(kThreads, grad_waves_per_simd<K>()) grad_kerne
         }
     }
     rows_reduce<K>(g2);
+    if constexpr (DR) {
+        rows_reduce<K>(g3);
+        rows_reduce<K>(g4);
+        rows_reduce<K>(g5);
+    }
     {
         constexpr int PS = rows_lanes<K>();
         const int p = lane & (PS - 1);
         if (lane < PS && p < K) {
 #pragma unroll
-            for (int t = 0; t < K; ++t) red[(2 * kWaves + wave) * KK + p * K + t] = g2[t];
+            for (int t = 0; t < K; ++t) {
+                red[(2 * kWaves + wave) * KK + p * K + t] = g2[t];
+                if constexpr (DR) {
+                    red[(3 * kWaves + wave) * KK + p * K + t] = g3[t];
+                    red[(4 * kWaves + wave) * KK + p * K + t] = g4[t];
+                    red[(5 * kWaves + wave) * KK + p * K + t] = g5[t];
+                }
+            }
         }
     }
     const float vdy = wave_sum(gdy);
-    if (lane == 0) red[3 * kWaves * KK + wave] = vdy;
+    if (lane == 0) red[(RL + 1) * kWaves * KK + wave] = vdy;
     __syncthreads();
     float* dst = a.partial + ((long)chunk * C + c) * NP;
     for (int t = tid; t < KK; t += kThreads) dst[t] = ((red[t] + red[KK + t]) + red[2 * KK + t]) + red[3 * KK + t];
     if (tid == 0) {
-        const float* r = red + 3 * kWaves * KK;
+        const float* r = red + (RL + 1) * kWaves * KK;
         dst[NP - 1] = ((r[0] + r[1]) + r[2]) + r[3];
     }
-    // levels 1-2: band q's sums came from wavefront q; deeper levels from the slots
-    for (int i = tid; i < 4 * KK * min(L, 2); i += kThreads) dst[KK + i] = red[kWaves * KK + i];
-    for (int i = tid; i < 4 * KK * (L - 2); i += kThreads) dst[KK + 8 * KK + i] = gco[i];
+    // levels 1..RL: band q's sums came from wavefront q; deeper levels from the slots
+    for (int i = tid; i < 4 * KK * min(L, RL); i += kThreads) dst[KK + i] = red[kWaves * KK + i];
+    for (int i = tid; i < 4 * KK * (L - RL); i += kThreads) dst[KK + 4 * RL * KK + i] = gco[i];
 }
 
-template <int K, typename ST, bool MR>
+template <int K, typename ST, bool MR, bool DR>
 hipError_t launch_grad_v(const GradArgs& a, int grid, hipStream_t s)
 {
     const size_t bytes = (size_t)a.lds_floats * sizeof(float);
     static std::atomic<unsigned long long> lds_done{0};
-    const hipError_t e = allow_full_lds(reinterpret_cast<const void*>(&grad_kernel<K, ST, MR>), lds_done);
+    const hipError_t e = allow_full_lds(reinterpret_cast<const void*>(&grad_kernel<K, ST, MR, DR>), lds_done);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((grad_kernel<K, ST, MR>), dim3(grid), dim3(kThreads), bytes, s, a);
+    hipLaunchKernelGGL((grad_kernel<K, ST, MR, DR>), dim3(grid), dim3(kThreads), bytes, s, a);
     return hipGetLastError();
 }
 
@@ -491,9 +520,9 @@ hipError_t launch_grad_t(const GradArgs& a, int grid, hipStream_t s)
 {
     if (a.rounds > 1) {
         if (a.PP != 1) return hipErrorInvalidValue;  // block rounds need one resident plane
-        return launch_grad_v<K, ST, true>(a, grid, s);
+        return a.g.L >= 4 ? launch_grad_v<K, ST, true, true>(a, grid, s) : launch_grad_v<K, ST, true, false>(a, grid, s);
     }
-    return launch_grad_v<K, ST, false>(a, grid, s);
+    return a.g.L >= 4 ? launch_grad_v<K, ST, false, true>(a, grid, s) : launch_grad_v<K, ST, false, false>(a, grid, s);
 }
 
 }  // namespace

@@ -244,6 +244,11 @@ struct GradArgs {
     PlaneGeom g;
 };
 
+// Gradient pass: levels 1..grad_reg_levels(L >= 4) keep their kernel-gradient
+// sums in registers across a workgroup's planes (levels 3-5 only in the
+// variant for pyramids of 4 or more levels); deeper levels use LDS slots.
+__host__ __device__ constexpr int grad_reg_levels(bool deep) { return deep ? 5 : 2; }
+
 // Number of kernel-gradient floats per (chunk, channel): base k*k, then
 // levels 1..L x bands 0..3 x k*k, then the sum of dy over the channel's pixels
 // (the gradient of the folded base bias).
