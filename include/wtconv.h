@@ -49,11 +49,12 @@
  *   - Entry points are reentrant; the library's only global state is the
  *     static scratch of wtconv_backward_noalloc (see there). Results are
  *     bitwise reproducible for identical inputs and shapes.
- *   - Supported: B, C, H, W >= 1; k in {1, 3, 5, 7}; 0 <= L <= 8. Even k has no
- *     centred halo (Section 4.1 takes the radius (k-1)/2) and is refused; so is
- *     k = 9, which the paper's experiments never use (they take k = 3, 5 and
- *     7) and whose 3k^2 per-lane gradient sums exceed the register budget the
- *     backward kernels are built around. Planes whose
+ *   - Supported: B, C, H, W >= 1; odd k with 1 <= k <= 9; 0 <= L <= 8. Even
+ *     k has no centred halo (Section 4.1 takes the radius (k-1)/2) and is
+ *     refused. The paper's experiments take k = 3, 5 and 7; k = 9 runs the same
+ *     kernels, whose per-lane kernel-gradient sums then overflow the register
+ *     budget the backward kernels are sized for (it is correct, not tuned).
+ *     Planes whose
  *     fused working set fits one compute unit's 160 KB of LDS (float32, k = 5:
  *     forward up to about 120 x 120 pixels, backward up to about 112 x 112, or
  *     about 90 x 90 at L = 1) run
@@ -70,7 +71,7 @@ extern "C" {
 #endif
 
 #define WTCONV_MAX_LEVELS 8
-#define WTCONV_MAX_KSIZE 7
+#define WTCONV_MAX_KSIZE 9
 
 typedef enum {
     WTCONV_F32 = 0,
@@ -82,7 +83,7 @@ typedef enum {
     WTCONV_OK = 0,
     WTCONV_ERR_NULL = 1,        /* a required pointer is NULL                     */
     WTCONV_ERR_SHAPE = 2,       /* B, C, H or W < 1, or a size overflows int      */
-    WTCONV_ERR_KSIZE = 3,       /* k not in {1, 3, 5, 7} (even k, or k >= 9)      */
+    WTCONV_ERR_KSIZE = 3,       /* k even, k < 1 or k > 9                         */
     WTCONV_ERR_LEVELS = 4,      /* L < 0 or L > WTCONV_MAX_LEVELS                 */
     WTCONV_ERR_DTYPE = 5,       /* unknown dtype                                  */
     WTCONV_ERR_ALIAS = 6,       /* an output overlaps an input or another output  */

@@ -17,7 +17,7 @@ CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libwtconv.so")
 SOURCES = ["wtconv_api.cpp", "wtconv_noalloc.cpp", "wtconv_fwd.hip", "wtconv_mixed.hip", "wtconv_bwd.hip",
-           "wtconv_grad.hip", "wtconv_kernels.hip", "wtconv_tiny.hip"]
+           "wtconv_bwd9.hip", "wtconv_grad.hip", "wtconv_kernels.hip", "wtconv_tiny.hip"]
 # measurement helper used only by the benchmark (sustained VALU rate)
 PROBE_LIB = os.path.join(HERE, "libvalu_probe.so")
 PROBE_SOURCES = ["valu_probe.hip"]

@@ -480,7 +480,7 @@ wtconv_status check_desc(const wtconv_desc* d)
     if ((long)d->H * d->W > (1L << 30) || (long)d->B * d->C > (1L << 30) ||
         (long)d->C * 4 * 49 > (1L << 30) || (long)d->B * d->C * d->H * d->W > (1L << 40))
         return WTCONV_ERR_SHAPE;
-    if (d->k != 1 && d->k != 3 && d->k != 5 && d->k != 7) return WTCONV_ERR_KSIZE;
+    if (d->k < 1 || d->k > 9 || (d->k % 2) == 0) return WTCONV_ERR_KSIZE;
     if (d->L < 0 || d->L > WTCONV_MAX_LEVELS) return WTCONV_ERR_LEVELS;
     if (d->dtype != WTCONV_F32 && d->dtype != WTCONV_BF16 && d->dtype != WTCONV_F16) return WTCONV_ERR_DTYPE;
     return WTCONV_OK;
@@ -612,7 +612,14 @@ struct Exec {
     bool coarse = false;  // split / region: a coarse sub-problem exists (L > m)
 };
 
-bool use_tiny(const wtconv_desc& d) { return d.H <= wtc::kTinyMaxEdge && d.W <= wtc::kTinyMaxEdge; }
+// Planes of at most 8 x 8 run one plane per lane, unless the tiny backward's
+// LDS (staging rows plus every folded kernel of four channels) would not fit:
+// k = 9 with L >= 6; those planes run resident like larger ones.
+bool use_tiny(const wtconv_desc& d)
+{
+    return d.H <= wtc::kTinyMaxEdge && d.W <= wtc::kTinyMaxEdge &&
+           wtc::tiny_lds_bytes(d.k, d.L, true) <= (size_t)wtc::kLdsBytesMax;
+}
 int tiny_groups(const wtconv_desc& d) { return cdiv(d.B, 64); }
 
 // The first level whose grid is at most 8 x 8.
@@ -1426,7 +1433,7 @@ const char* wtconv_status_string(wtconv_status s)
         case WTCONV_OK: return "ok";
         case WTCONV_ERR_NULL: return "a required pointer is NULL";
         case WTCONV_ERR_SHAPE: return "invalid shape (B, C, H, W must be >= 1 and sizes must fit)";
-        case WTCONV_ERR_KSIZE: return "unsupported kernel size (k must be 1, 3, 5 or 7)";
+        case WTCONV_ERR_KSIZE: return "unsupported kernel size (k must be 1, 3, 5, 7 or 9)";
         case WTCONV_ERR_LEVELS: return "unsupported number of levels (0 <= L <= 8)";
         case WTCONV_ERR_DTYPE: return "unknown dtype";
         case WTCONV_ERR_ALIAS: return "an output overlaps an input or another output";

@@ -584,7 +584,7 @@ DEV void corr_band_rows(const float* __restrict__ dz0, const float* __restrict__
                         const LevelGeom& lg, int q, int np, float* __restrict__ slot, int lane)
 {
     constexpr int R = K / 2;
-    constexpr int PS = K <= 1 ? 1 : (K <= 2 ? 2 : (K <= 4 ? 4 : 8));  // lanes per row group
+    constexpr int PS = row_group_lanes(K);  // lanes per row group
     constexpr int NG = 64 / PS;                                        // row groups
     const int p = lane & (PS - 1), rg = lane / PS;
     const bool active = p < K;
@@ -881,8 +881,9 @@ DEV float wave_sum(float v)
 // unnormalised pyramids, removed here exactly); for the base row also the bias
 // terms d b0 = s0 * sum(dy) and b0 * sum(dy) in d s0. One wavefront per
 // (channel c, kernel row `band`: 0 = base, else 1 + (l-1)*4 + q); lane t
-// owns tap t (lane k*k the sum of dy); the d(scale) dot product is a
-// fixed-order wavefront reduction.
+// owns tap t (lane k*k the sum of dy; at k = 9 the taps and the sum wrap
+// round the 64 lanes); the d(scale) dot product is a fixed-order wavefront
+// reduction.
 DEV void reduce_task(const ReduceArgs& a, int c, int band, int t)
 {
     const int KK = a.k * a.k;
@@ -907,34 +908,37 @@ DEV void reduce_task(const ReduceArgs& a, int c, int band, int t)
         dw = a.dlw[l - 1] + (long)ch * KK;
         ds = a.dls[l - 1] + ch;
     }
+    // lane t takes taps t, t + 64, ... (more than one only for k = 9) and the
+    // bias sum at index k * k
     float prod = 0.f;
-    if (t < KK) {
-        const float* src = a.partial + (long)c * NP + band * KK + t;
-        const long step = (long)a.C * NP;
-        // chunk order is kept; the loads of a group of 8 chunks are issued
-        // together so that their latencies overlap
-        float G = 0.f;
-        int ch = 0;
-        for (; ch + 8 <= a.nchunks; ch += 8) {
-            float v[8];
+    const long step = (long)a.C * NP;
+    for (int tt = t; tt <= KK; tt += 64) {
+        if (tt < KK) {
+            const float* src = a.partial + (long)c * NP + band * KK + tt;
+            // chunk order is kept; the loads of a group of 8 chunks are issued
+            // together so that their latencies overlap
+            float G = 0.f;
+            int ch = 0;
+            for (; ch + 8 <= a.nchunks; ch += 8) {
+                float v[8];
 #pragma unroll
-            for (int u = 0; u < 8; ++u) v[u] = src[(long)(ch + u) * step];
+                for (int u = 0; u < 8; ++u) v[u] = src[(long)(ch + u) * step];
 #pragma unroll
-            for (int u = 0; u < 8; ++u) G += v[u];
+                for (int u = 0; u < 8; ++u) G += v[u];
+            }
+            for (; ch < a.nchunks; ++ch) G += src[(long)ch * step];
+            G *= norm;
+            dw[tt] = scale * G;
+            prod = tt == t ? G * w[tt] : __builtin_fmaf(G, w[tt], prod);
+        } else if (band == 0) {
+            // folded base bias b~ = s0 * b0: its gradient is the sum of dy, so
+            // d b0 = s0 * sum(dy) and d s0 gains b0 * sum(dy) (eq. foldgrad)
+            const float* src = a.partial + (long)c * NP + (NP - 1);
+            float Gb = 0.f;
+            for (int ch = 0; ch < a.nchunks; ++ch) Gb += src[(long)ch * step];
+            if (a.db0) a.db0[c] = scale * Gb;
+            if (a.p.b0) prod = tt == t ? a.p.b0[c] * Gb : __builtin_fmaf(a.p.b0[c], Gb, prod);
         }
-        for (; ch < a.nchunks; ++ch) G += src[(long)ch * step];
-        G *= norm;
-        dw[t] = scale * G;
-        prod = G * w[t];
-    } else if (band == 0 && t == KK) {
-        // folded base bias b~ = s0 * b0: its gradient is the sum of dy, so
-        // d b0 = s0 * sum(dy) and d s0 gains b0 * sum(dy) (eq. foldgrad)
-        const float* src = a.partial + (long)c * NP + (NP - 1);
-        const long step = (long)a.C * NP;
-        float Gb = 0.f;
-        for (int ch = 0; ch < a.nchunks; ++ch) Gb += src[(long)ch * step];
-        if (a.db0) a.db0[c] = scale * Gb;
-        if (a.p.b0) prod = a.p.b0[c] * Gb;
     }
     prod = wave_sum(prod);
     if (t == 0) *ds = prod;
@@ -1277,24 +1281,32 @@ hipError_t launch_one(const FusedArgs& a, int grid, hipStream_t s)
                        : launch_variant<K, ST, BWD, false, false>(a, grid, s);
 }
 
+template <int K, bool BWD>
+hipError_t launch_dt(wtconv_dtype dt, const FusedArgs& a, int grid, hipStream_t s)
+{
+    switch (dt) {
+        case WTCONV_F32: return launch_one<K, float, BWD>(a, grid, s);
+        case WTCONV_BF16: return launch_one<K, uint16_t, BWD>(a, grid, s);
+        case WTCONV_F16: return launch_one<K, _Float16, BWD>(a, grid, s);
+    }
+    return hipErrorInvalidValue;
+}
+
 template <bool BWD>
 hipError_t dispatch(int k, wtconv_dtype dt, const FusedArgs& a, int grid, hipStream_t s)
 {
-#define WTC_CASE(KV)                                                            \
-    case KV:                                                                    \
-        switch (dt) {                                                           \
-            case WTCONV_F32: return launch_one<KV, float, BWD>(a, grid, s);     \
-            case WTCONV_BF16: return launch_one<KV, uint16_t, BWD>(a, grid, s); \
-            case WTCONV_F16: return launch_one<KV, _Float16, BWD>(a, grid, s);  \
-        }                                                                       \
-        break;
     switch (k) {
-        WTC_CASE(1)
-        WTC_CASE(3)
-        WTC_CASE(5)
-        WTC_CASE(7)
+        case 1: return launch_dt<1, BWD>(dt, a, grid, s);
+        case 3: return launch_dt<3, BWD>(dt, a, grid, s);
+        case 5: return launch_dt<5, BWD>(dt, a, grid, s);
+        case 7: return launch_dt<7, BWD>(dt, a, grid, s);
+        case 9:
+            // the k = 9 backward is compiled in a translation unit of its own
+            if constexpr (BWD)
+                return launch_backward_k9(dt, a, grid, s);
+            else
+                return launch_dt<9, false>(dt, a, grid, s);
     }
-#undef WTC_CASE
     return hipErrorInvalidValue;
 }
 

@@ -44,6 +44,7 @@ int forward_wgs_by_regs(int k, wtconv_dtype dt, bool one, int fallback)
         case 3: return wgs_k<3>(dt, one, fallback);
         case 5: return wgs_k<5>(dt, one, fallback);
         case 7: return wgs_k<7>(dt, one, fallback);
+        case 9: return wgs_k<9>(dt, one, fallback);
     }
     return fallback;
 }

@@ -120,7 +120,7 @@ DEV void grad_row_chunk(const float* __restrict__ dr, const float* __restrict__ 
 // both sides.
 // Lanes past the K tap rows read a valid row; their sums are dropped.
 template <int K>
-constexpr int rows_lanes() { return K <= 1 ? 1 : (K <= 2 ? 2 : (K <= 4 ? 4 : 8)); }  // lanes per row group
+constexpr int rows_lanes() { return row_group_lanes(K); }  // lanes per row group
 
 template <int K>
 DEV void grad_rows_acc(const float* __restrict__ region0, int stride, const LevelGeom& xl, DyLevel dl, int q,
@@ -237,9 +237,11 @@ DEV void write_carrier(ST* __restrict__ out, int H1, int W1, int M, int y0, int 
 
 // At least three waves per SIMD (168 VGPRs) for k <= 5: with three
 // workgroups per CU (the LDS budget of the planner) each SIMD then holds one
-// wavefront of each.
+// wavefront of each. k = 7 keeps two; at k = 9 the 2 x 81 per-lane sums
+// alone need most of a wavefront's 256 VGPRs, so one wavefront per SIMD may
+// use the accumulation registers too.
 template <int K>
-constexpr int grad_waves_per_simd() { return K <= 5 ? 3 : 2; }
+constexpr int grad_waves_per_simd() { return K <= 5 ? 3 : (K <= 7 ? 2 : 1); }
 
 // MR: planes with more 4x4 blocks than threads, one resident plane, block
 // rounds (a separate instantiation keeps the one-round kernel's registers).
@@ -542,6 +544,7 @@ hipError_t launch_grad(int k, wtconv_dtype dt, const GradArgs& a, int grid, hipS
         WTC_GRAD_CASE(3)
         WTC_GRAD_CASE(5)
         WTC_GRAD_CASE(7)
+        WTC_GRAD_CASE(9)
     }
 #undef WTC_GRAD_CASE
     return hipErrorInvalidValue;

@@ -262,6 +262,14 @@ __host__ __device__ inline int row_chunk(int w)
     return w <= 4 ? 4 : (((w + 7) / 8 * 8 < (w + 15) / 16 * 16) ? 8 : 16);
 }
 
+// Lanes per row group of the row-wise kernel-gradient correlation: one lane
+// per tap row, rounded up to a power of two (the groups are summed with an xor
+// tree over the wavefront).
+__host__ __device__ constexpr int row_group_lanes(int k)
+{
+    return k <= 1 ? 1 : (k <= 2 ? 2 : (k <= 4 ? 4 : (k <= 8 ? 8 : 16)));
+}
+
 hipError_t launch_forward(int k, wtconv_dtype dt, const FusedArgs& a, int grid, hipStream_t s);
 // Workgroups per CU that the registers of the forward kernel for (k, dt,
 // single-round variant) allow; `fallback` if the runtime cannot tell.
@@ -272,10 +280,20 @@ hipError_t launch_forward_mixed(int k, wtconv_dtype dt, const FusedArgs& a, int 
 // rounds) allow; `fallback` if the runtime cannot tell.
 int mixed_wgs_by_regs(int k, wtconv_dtype dt, int rounds, int fallback);
 hipError_t launch_backward(int k, wtconv_dtype dt, const FusedArgs& a, int grid, hipStream_t s);
+// The fused backward kernels for k = 9 (wtconv_bwd9.hip).
+hipError_t launch_backward_k9(wtconv_dtype dt, const FusedArgs& a, int grid, hipStream_t s);
 hipError_t launch_reduce(const ReduceArgs& a, hipStream_t s);
 hipError_t launch_grad(int k, wtconv_dtype dt, const GradArgs& a, int grid, hipStream_t s);
 hipError_t launch_carrier(wtconv_dtype dt, const CarrierArgs& a, hipStream_t s);
 hipError_t launch_tiny(int k, wtconv_dtype dt, bool bwd, const TinyArgs& a, hipStream_t s);
-size_t tiny_lds_bytes(int k, int L, bool bwd);
+// LDS of one workgroup of the tiny kernel (wtconv_tiny.hip): a staging area
+// of 64 rows of 65 floats per wavefront (also the gradient scratch), the
+// folded kernels of its four channels, 4 x 64 flush offsets and, in the
+// backward pass, four more staging areas for the dx accumulation.
+constexpr int kTinyStageFloats = 64 * 65;
+inline size_t tiny_lds_bytes(int k, int L, bool bwd)
+{
+    return (size_t)((bwd ? 8 : 4) * kTinyStageFloats + 4 * (1 + 4 * L) * k * k + 4 * 64) * sizeof(float);
+}
 
 }  // namespace wtc

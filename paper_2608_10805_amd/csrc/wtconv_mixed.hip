@@ -337,6 +337,7 @@ hipError_t launch_forward_mixed(int k, wtconv_dtype dt, const FusedArgs& a, int 
         WTC_MCASE(3)
         WTC_MCASE(5)
         WTC_MCASE(7)
+        WTC_MCASE(9)
     }
 #undef WTC_MCASE
     return hipErrorInvalidValue;
@@ -349,6 +350,7 @@ int mixed_wgs_by_regs(int k, wtconv_dtype dt, int rounds, int fallback)
         case 3: return mixed_wgs_k<3>(dt, rounds, fallback);
         case 5: return mixed_wgs_k<5>(dt, rounds, fallback);
         case 7: return mixed_wgs_k<7>(dt, rounds, fallback);
+        case 9: return mixed_wgs_k<9>(dt, rounds, fallback);
     }
     return fallback;
 }

@@ -40,6 +40,7 @@ constexpr int kTPos = kTE * kTE;   // positions per plane
 // entries) fall in distinct LDS banks.
 constexpr int kTPitch = 65;
 constexpr int kTStage = 64 * kTPitch;  // floats per wavefront
+static_assert(kTStage == kTinyStageFloats, "tiny_lds_bytes() sizes the staging areas");
 
 
 // Index of the folded-kernel row for the base kernel (0) or level l band q.
@@ -232,6 +233,8 @@ DEV void gq_put(GradQueue& q, const float (&g)[K * K], int off, float* __restric
 #pragma unroll
     for (int t = 0; t < KK; ++t) {
         if (tap_live<K, N>(t)) {
+            if constexpr (KK > 64)  // k = 9: more live taps than a flush holds
+                if (q.n == 64) gq_flush(q, dst, lane, store);
             q.scr[lane * kTPitch + q.n] = g[t];
             if (lane == 0) q.offs[q.n] = off + t;
             ++q.n;
@@ -536,12 +539,6 @@ __global__ void __launch_bounds__(256) tiny_kernel(const TinyArgs a)
 
 }  // namespace
 
-// LDS of one workgroup: staging rows (also the gradient scratch), folded
-// kernels, flush offsets and, in the backward pass, the dx accumulation rows.
-size_t tiny_lds_bytes(int k, int L, bool bwd)
-{
-    return (size_t)((bwd ? 8 : 4) * kTStage + 4 * (1 + 4 * L) * k * k + 4 * 64) * sizeof(float);
-}
 
 namespace {
 
@@ -573,6 +570,7 @@ hipError_t tiny_dispatch(int k, wtconv_dtype dt, const TinyArgs& a, hipStream_t 
         WTC_TCASE(3)
         WTC_TCASE(5)
         WTC_TCASE(7)
+        WTC_TCASE(9)
     }
 #undef WTC_TCASE
     return hipErrorInvalidValue;

@@ -13,7 +13,6 @@ hipError_t launch_reduce(const ReduceArgs&, hipStream_t) { return hipSuccess; }
 hipError_t launch_grad(int, wtconv_dtype, const GradArgs&, int, hipStream_t) { return hipSuccess; }
 hipError_t launch_carrier(wtconv_dtype, const CarrierArgs&, hipStream_t) { return hipSuccess; }
 hipError_t launch_tiny(int, wtconv_dtype, bool, const TinyArgs&, hipStream_t) { return hipSuccess; }
-size_t tiny_lds_bytes(int, int, bool) { return 0; }
 int forward_wgs_by_regs(int, wtconv_dtype, bool, int fallback) { return fallback; }
 hipError_t launch_forward_mixed(int, wtconv_dtype, const FusedArgs&, int, hipStream_t) { return hipSuccess; }
 int mixed_wgs_by_regs(int, wtconv_dtype, int, int fallback) { return fallback; }

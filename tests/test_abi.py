@@ -53,7 +53,7 @@ def fwd(desc, x=FAKE, bw=FAKE + 4096, bs=FAKE + 8192, lw=None, ls=None, y=FAKE +
 
 @pytest.mark.parametrize("shape,code", [
     ((0, 1, 8, 8, 5, 1), 2), ((1, 0, 8, 8, 5, 1), 2), ((1, 1, 0, 8, 5, 1), 2), ((1, 1, 8, -3, 5, 1), 2),
-    ((1, 1, 8, 8, 4, 1), 3), ((1, 1, 8, 8, 9, 1), 3), ((1, 1, 8, 8, 0, 1), 3), ((1, 1, 8, 8, -1, 1), 3),
+    ((1, 1, 8, 8, 4, 1), 3), ((1, 1, 8, 8, 11, 1), 3), ((1, 1, 8, 8, 0, 1), 3), ((1, 1, 8, 8, -1, 1), 3),
     ((1, 1, 8, 8, 5, -1), 4), ((1, 1, 8, 8, 5, 9), 4),
 ])
 def test_forward_rejects_bad_descriptors(shape, code):
@@ -97,6 +97,19 @@ def test_forward_workspace_query():
     # a single Haar level (or none) needs no carrier
     assert binding.wtconv_forward_workspace_bytes(make_desc(16, 64, 224, 224, 5, 1)) == 0
     assert binding.wtconv_forward_workspace_bytes(make_desc(16, 64, 224, 224, 5, 0)) == 0
+
+
+def test_kernel_sizes_up_to_nine_are_planned():
+    # odd k from 1 to 9 has a plan (the backward always needs partials);
+    # k = 11 and even k are refused, which the size queries report as 0
+    for k in (1, 3, 5, 7, 9):
+        for shape in ((2, 3, 7, 7), (2, 3, 14, 14), (2, 3, 56, 56), (2, 3, 130, 126)):
+            assert binding.wtconv_backward_workspace_bytes(make_desc(*shape, k, 3)) > 0, (shape, k)
+    assert binding.wtconv_backward_workspace_bytes(make_desc(2, 3, 14, 14, 11, 3)) == 0
+    assert binding.wtconv_backward_workspace_bytes(make_desc(2, 3, 14, 14, 8, 3)) == 0
+    # 8 x 8 planes at k = 9 with the deepest pyramids: the one-plane-per-lane
+    # backward's LDS would not fit, and the resident plan takes them
+    assert binding.wtconv_backward_workspace_bytes(make_desc(2, 3, 8, 8, 9, 8)) > 0
 
 
 def test_forward_split_needs_planes_to_fill_the_chip():

@@ -571,6 +571,56 @@ def test_large_plane_determinism_bitwise():
         assert torch.equal(a, b)
 
 
+# k = 9 (the largest kernel the boundary takes; the paper's experiments stop
+# at 7), one shape per execution path: tiny planes, 8 x 8 planes whose tiny
+# backward LDS would not fit (resident with mixed rounds instead), mixed
+# forward rounds, forward regions on small planes, the split backward, the
+# gradient pass with one block per thread and with block rounds, the fused
+# region backward, L = 0 and a deep split. At k = 9 a kernel row has 81 taps,
+# more than a wavefront's lanes: the finalize wraps them round the lanes and
+# the tiny backward flushes its gradient queue within one kernel.
+K9 = [
+    (70, 3, 7, 6, 9, 4, "f32"),
+    (2, 3, 7, 7, 9, 3, "bf16"),
+    (2, 3, 8, 8, 9, 8, "f32"),
+    (2, 3, 14, 14, 9, 2, "f32"),
+    (16, 8, 16, 16, 9, 3, "f32"),
+    (2, 3, 28, 28, 9, 3, "f16"),
+    (2, 3, 40, 40, 9, 3, "f32"),
+    (2, 2, 56, 56, 9, 3, "f32"),
+    (2, 2, 63, 95, 9, 4, "f32"),
+    (1, 2, 130, 126, 9, 3, "f32"),
+    (2, 3, 14, 14, 9, 0, "f32"),
+    (2, 3, 28, 28, 9, 1, "bf16"),
+    (66, 2, 14, 14, 9, 5, "f32"),
+]
+
+
+@pytest.mark.parametrize("B,C,H,W,k,L,dtype", K9)
+def test_k9_forward(B, C, H, W, k, L, dtype):
+    check_forward(B, C, H, W, k, L, dtype)
+
+
+@pytest.mark.parametrize("B,C,H,W,k,L,dtype", K9)
+def test_k9_backward(B, C, H, W, k, L, dtype):
+    check_backward(B, C, H, W, k, L, dtype)
+
+
+@pytest.mark.parametrize("B,C,H,W,k,L,dtype", [(2, 4, 28, 28, 9, 3, "f32"), (70, 3, 7, 6, 9, 4, "f32"),
+                                                (1, 2, 130, 126, 9, 3, "f32")])
+def test_k9_bias(B, C, H, W, k, L, dtype):
+    test_bias_forward_backward(B, C, H, W, k, L, dtype)
+
+
+def test_k9_determinism_bitwise():
+    test_determinism_bitwise(4, 6, 56, 56, 9, 3)
+
+
+@pytest.mark.parametrize("B,C,H,W,L,dtype", [(32, 64, 56, 56, 3, "f32"), (128, 384, 14, 14, 4, "bf16")])
+def test_k9_full_size(B, C, H, W, L, dtype):
+    check_full_size(B, C, H, W, 9, L, dtype, backward=True)
+
+
 def _random_cases(seed, n):
     """Seeded random shapes across every execution path: tiny, resident with one
     or several planes, split, gradient pass (one block per thread or block

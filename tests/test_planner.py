@@ -113,8 +113,8 @@ def test_mixed_round_plans_hold_their_invariants(mixed_check):
     inside its array and the LDS (tests/planner/mixed_check.cpp)."""
     rng = random.Random(7)
     lines = [f"{rng.randint(1, 140)} {rng.randint(1, 400)} {rng.randint(9, 16)} {rng.randint(9, 16)} "
-             f"{rng.choice([1, 3, 5, 7])} {rng.randint(1, 8)} {rng.randint(0, 2)}" for _ in range(3000)]
-    lines += [f"128 384 14 14 {k} {L} 0" for k in (3, 5, 7) for L in range(1, 6)]
+             f"{rng.choice([1, 3, 5, 7, 9])} {rng.randint(1, 8)} {rng.randint(0, 2)}" for _ in range(3000)]
+    lines += [f"128 384 14 14 {k} {L} 0" for k in (3, 5, 7, 9) for L in range(1, 6)]
     out = subprocess.run([mixed_check], input="\n".join(lines) + "\n", capture_output=True, text=True,
                          check=True, timeout=120).stdout.split("\n")[:len(lines)]
     fails = [(l, o) for l, o in zip(lines, out) if not (o.startswith("ok") or o == "fused")]
