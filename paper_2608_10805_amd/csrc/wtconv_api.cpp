@@ -837,6 +837,18 @@ struct GradExec {
 // plane). Measured on MI355X, backward us, split / not: 28x28 B64 L4 174 / 198,
 // L5 187 / 238, B128 L5 278 / 439; 56x56 (one resident plane) B128 L5 429 / 382.
 constexpr int kGradSplitMinShed = 2;
+// A single level above m >= 2 is shed too once the coarse sub-problem has
+// enough planes for its one-plane-per-lane kernel: at least this many. The
+// gradient pass then keeps the smaller LDS of levels 1..m (the carriers come
+// from the pass itself). Measured on MI355X, k = 5, L = 3, combined backward
+// us, shed / not: B128 C192 18 x 18 158 / 180, 20 x 20 142 / 161, 26 x 26 216
+// / 257, 28 x 28 193 / 225 (bf16 199 / 234), 30 x 30 257 / 272, 32 x 32 219 /
+// 232, 24 x 24 172 / 175; B96 C192 28 x 28 155 / 173. Below it the gain
+// shrinks and turns into a loss: B80 C192 28 x 28 142 / 152, B128 C128
+// 32 x 32 145 / 143, B64 C192 28 x 28 124 / 122, 20 x 20 101 / 89, 24 x 24
+// 110 / 99. k = 3 and 7 at B128 C192 28 x 28: within 1 %. (Shedding the level in the forward pass too
+// was slower at every one of these shapes: 28 x 28 B128 108 against 83 us.)
+constexpr long kGradShedOneMinPlanes = 18432;
 
 // Measured on MI355X: the gradient pass beats the fused backward when the
 // plane's first level at most 8 x 8 is level 2 or deeper (planes above 16 x 16)
@@ -871,7 +883,7 @@ GradExec choose_grad(const wtconv_desc& d)
     const int m = tiny_level(d);
     if (m < 1 || (m == 1 && d.L > 2 && !grad_pass_pays_deep(d))) return ge;
     wtconv_desc f = d;
-    if (d.L - m >= kGradSplitMinShed) {
+    if (d.L - m >= kGradSplitMinShed || (m >= 2 && d.L > m && (long)d.B * d.C >= kGradShedOneMinPlanes)) {
         GradPlan full;
         if (make_grad_plan(d, full) && full.PP > 1) f.L = m;
     }

@@ -505,6 +505,15 @@ def test_split_rule_shapes_full(B, C, H, k, L, dtype):
     check_full_size(B, C, H, H, k, L, dtype, backward=True, n_planes=6, n_channels=2)
 
 
+@pytest.mark.parametrize("B,C,H,L,dtype", [(96, 192, 18, 3, "bf16"), (128, 192, 26, 3, "f32"),
+                                           (64, 192, 20, 3, "f32")])
+def test_grad_shed_one_level_full(B, C, H, L, dtype):
+    """Backwards around the plane count from which the gradient pass sheds a
+    single level above m = 2 to the coarse sub-problem (B96 and B128 C192:
+    shed; B64 C192: whole)."""
+    check_full_size(B, C, H, H, 5, L, dtype, backward=True, n_planes=6, n_channels=2)
+
+
 # Planes whose working set does not fit one compute unit's LDS take the split
 # path: the coarse levels run on the level-1 carrier (recursively, if that is
 # still too large) and the base path plus level 1 run on halo tiles. Every
