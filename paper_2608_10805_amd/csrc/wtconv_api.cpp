@@ -129,7 +129,7 @@ void set_tile_lanes(PlaneGeom& g, int lanes)
 // plans also pass rows_from = kMaxLevels + 1: only the backward runs the
 // kernel-gradient row chunks that the row padding is for.
 bool layout(const wtconv_desc& d, int PP, bool bwd, PlaneGeom& g, bool t4_deep = false, bool one_pref = false,
-            int rows_from = 2, bool t4_all = false, bool share_halo = false)
+            int rows_from = 2, bool t4_all = false, bool share_halo = false, int t1_max = 4)
 {
     const int R = d.k / 2;
     memset(&g, 0, sizeof(g));
@@ -149,6 +149,7 @@ bool layout(const wtconv_desc& d, int PP, bool bwd, PlaneGeom& g, bool t4_deep =
         lg.h = h;
         lg.w = w;
         lg.T = (t4_all || (t4_deep && l >= 3)) ? 4 : pick_tile(h, w, PP, d.k, bwd, one_pref);
+        if (l == 1 && lg.T > t1_max) lg.T = t1_max;
         if (lg.T == 0) return false;
         lg.eh = ceil_to(h, lg.T);
         lg.ew = ceil_to(w, lg.T);
@@ -721,13 +722,13 @@ int grad_gc_floats(const wtconv_desc& d)
 // and 2), the sources of the next level's butterflies and, for levels >= 2,
 // whole row chunks of the row-wise correlation. Level 1 is stored over the x
 // plane when it fits and the block loads write every site that is read.
-bool grad_layout(const wtconv_desc& d, int PP, GradPlan& gp)
+bool grad_layout(const wtconv_desc& d, int PP, GradPlan& gp, int t1_max = 4)
 {
     // storing dy level 1 over the x plane costs a re-zeroing of the x plane's
     // halo ring per batch; it pays for large planes (one resident plane), where
     // it decides the number of workgroups per CU
     const bool may_alias = PP == 1;
-    if (!layout(d, PP, true, gp.g, false, false, 2)) return false;
+    if (!layout(d, PP, true, gp.g, false, false, 2, false, false, t1_max)) return false;
     const PlaneGeom& g = gp.g;
     const long xplane = (long)g.xrows * g.xpitch;
     long extra = 0;
@@ -795,17 +796,43 @@ bool make_grad_plan(const wtconv_desc& d, GradPlan& gp)
     } else {
         const int maxpp = (int)std::min<long>(d.B, wtc::kThreads / per);
         double best = -1.0;
-        for (int pp = 1; pp <= maxpp; ++pp) {
-            GradPlan c;
-            if (!grad_layout(d, pp, c)) continue;
-            const int wgs = std::min(3, lds_wgs(c.lds_floats));
-            const double score = (double)pp * per / wtc::kThreads * wgs;
-            if (score >= best) {
-                best = score;
-                gp = c;
-                gp.PP = pp;
+        // Level 1 in 4 x 4 site tiles first. Tiles of 2 x 2 sites take the
+        // same FMA issue in four times the rounds, but the level's arrays
+        // then cover the grid rounded to 2 rather than to 4 sites (14 x 14
+        // instead of 16 x 16 at 28 x 28): they replace the 4 x 4 plan when
+        // that lets more planes or workgroups fit, i.e. when the score with
+        // the workgroups per CU that the kernel's registers allow (3 for
+        // k <= 5, 2 for k = 7, 1 for k = 9) rises without fewer workgroups.
+        // Measured on MI355X (combined backward, us, 4 x 4 -> 2 x 2): B64
+        // C192 28 x 28 L1 82.0 -> 74.1 (bf16 80.4 -> 71.7), B128 C192 L1 142.4
+        // -> 122.6, 26 x 26 L1 95.9 -> 82.5; B64 C96 50 x 50 L3 203.3 ->
+        // 168.0, 52 x 52 L5 213.2 -> 178.8, 58 x 58 L2 194.9 -> 169.3, L3
+        // 224.2 -> 192.8, 49 x 49 L4 225.8 -> 187.6, 18 x 18 L3 61.5 -> 54.4;
+        // k = 3 B64 C192 28 x 28 L1 65.7 -> 59.7, B64 C96 58 x 58 L3 181.3 ->
+        // 153.1; k = 7 28 x 28 L2 188.6 -> 177.2, L4 229.7 -> 218.0, B128 C192
+        // 26 x 26 L3 418.3 -> 390.2. Taken without the register limit it also
+        // moved 12 x 12 L2 B128 C384 to more planes at fewer workgroups (101.2
+        // -> 113.1) and k = 7 58 x 58 L1 to tiles that only added rounds
+        // (220.4 -> 270.4).
+        const int reg_wgs = d.k <= 5 ? 3 : (d.k <= 7 ? 2 : 1);
+        double best_r = -1.0;
+        int best_wgs = 0;
+        for (int t1 : {4, 2})
+            for (int pp = 1; pp <= maxpp; ++pp) {
+                GradPlan c;
+                if (!grad_layout(d, pp, c, t1)) continue;
+                const int wgs = std::min(3, lds_wgs(c.lds_floats));
+                const double lanes = (double)pp * per / wtc::kThreads;
+                const double score = lanes * wgs;
+                const double score_r = lanes * std::min(wgs, reg_wgs);
+                if (t1 == 4 ? score >= best : (score_r > best_r && std::min(wgs, reg_wgs) >= best_wgs)) {
+                    best = score;
+                    best_r = score_r;
+                    best_wgs = std::min(wgs, reg_wgs);
+                    gp = c;
+                    gp.PP = pp;
+                }
             }
-        }
         if (best < 0) return false;
     }
     // One round of resident workgroups: the per-workgroup setup and the final

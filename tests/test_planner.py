@@ -91,6 +91,23 @@ def test_small_planes_take_mixed_rounds(planner):
         assert planner(64, 96, H, H, 5, L)["fwd_mx_rounds"] == 0
 
 
+def test_gradient_pass_level1_tiles_and_shed(planner):
+    """The gradient pass takes level 1 in 2 x 2 site tiles where the smaller
+    footprint fits three workgroups per CU (B64 C192 28 x 28 L1: four planes
+    in 13440 floats instead of five in 16800), not where it would trade
+    workgroups for planes (B128 C384 12 x 12 L2 keeps ten planes at three per
+    CU). A single level above m = 2 goes to the coarse sub-problem from
+    18432 planes on (28 x 28 L3: B128 C192 yes, B64 C192 no)."""
+    p = planner(64, 192, 28, 28, 5, 1)
+    assert p["grad_PP"] == 4 and lds_wgs(p["grad_lds_floats"]) == 3
+    p = planner(128, 384, 12, 12, 5, 2)
+    assert p["grad_PP"] == 10 and lds_wgs(p["grad_lds_floats"]) == 3
+    p = planner(128, 192, 28, 28, 5, 3)
+    assert p["grad_levels"] == 2 and p["grad_coarse"] == 1
+    p = planner(64, 192, 28, 28, 5, 3)
+    assert p["grad_levels"] == 3 and p["grad_coarse"] == 0
+
+
 @pytest.fixture(scope="module")
 def mixed_check(tmp_path_factory):
     gxx = shutil.which("g++")
