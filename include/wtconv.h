@@ -46,9 +46,11 @@
  *     launch errors are returned as WTCONV_ERR_HIP; device faults surface at
  *     the caller's next synchronisation.
  *   - Gradient outputs are overwritten, not accumulated into.
- *   - Entry points are reentrant; the library's only global state is the
- *     static scratch of wtconv_backward_noalloc (see there). Results are
- *     bitwise reproducible for identical inputs and shapes.
+ *   - Entry points are reentrant and thread-safe; the library's global state
+ *     is the static scratch of wtconv_backward_noalloc (see there) and a
+ *     mutex-guarded cache of execution plans by descriptor (64 entries, a
+ *     plan depends only on the descriptor). Results are bitwise reproducible
+ *     for identical inputs and shapes.
  *   - Supported: B, C, H, W >= 1; odd k with 1 <= k <= 9; 0 <= L <= 8. Even
  *     k has no centred halo (Section 4.1 takes the radius (k-1)/2) and is
  *     refused. The paper's experiments take k = 3, 5 and 7; k = 9 runs the same

@@ -4,6 +4,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <mutex>
 
 #include "wtconv_internal.h"
 
@@ -128,8 +129,15 @@ void set_tile_lanes(PlaneGeom& g, int lanes)
 // writes, and every window or row read of band q ends within them). Forward
 // plans also pass rows_from = kMaxLevels + 1: only the backward runs the
 // kernel-gradient row chunks that the row padding is for.
+// t1_max: the largest tile edge level 1 may take (the gradient pass tries 2).
+// pitch2: levels filtered in 2 x 2 or single-site tiles (8-byte and 4-byte
+// LDS reads, forward only) get rows padded to 2 floats instead of 4; every
+// level still starts 16-byte aligned. Smaller, but rows starting on odd
+// float pairs cost 0.5-3 % in bank conflicts, and offered to the plan search
+// it traded workgroups for planes badly (12 x 12 L = 3 +28 %, 14 x 14 L = 4
+// +20 %), so only the merge of the deep levels below uses it.
 bool layout(const wtconv_desc& d, int PP, bool bwd, PlaneGeom& g, bool t4_deep = false, bool one_pref = false,
-            int rows_from = 2, bool t4_all = false, bool share_halo = false, int t1_max = 4)
+            int rows_from = 2, bool t4_all = false, bool share_halo = false, int t1_max = 4, bool pitch2 = false)
 {
     const int R = d.k / 2;
     memset(&g, 0, sizeof(g));
@@ -159,7 +167,7 @@ bool layout(const wtconv_desc& d, int PP, bool bwd, PlaneGeom& g, bool t4_deep =
             const int cw = wtc::row_chunk(w);
             pitch = std::max(pitch, ceil_to(w, cw) - cw + ceil_to(cw + 2 * R, 4));
         }
-        lg.pitch = ceil_to(pitch, 4);
+        lg.pitch = ceil_to(pitch, (pitch2 && lg.T < 4) ? 2 : 4);
         const int shared = share_halo ? R : 0;  // halo rows a band shares with the next
         lg.band = (rows - shared) * lg.pitch;
         lg.off = (int)off;
@@ -168,6 +176,7 @@ bool layout(const wtconv_desc& d, int PP, bool bwd, PlaneGeom& g, bool t4_deep =
         lg.r_tx = 1.0f / (float)(lg.ew / lg.T);
         lg.r_tper = 1.0f / (float)((lg.ew / lg.T) * (lg.eh / lg.T));
         off += 4L * lg.band + (long)shared * lg.pitch;
+        off = (off + 3) / 4 * 4;  // the next level's rows start 16-byte aligned
         if (off > (1L << 30)) return false;
     }
     g.plane_floats = (int)off;
@@ -389,14 +398,25 @@ bool make_plan(const wtconv_desc& d, bool bwd, Plan& pl, bool allow_mixed = true
     // with a handful of busy lanes) take 4x4 tiles too and share level 1's
     // round on the lanes level 1 leaves idle, if they fit (measured on MI355X:
     // the 7x7 level 3 of a 56x56 plane cost 5 us of a 73 us forward on its own).
+    // It is taken if it keeps the workgroups per CU of the unmerged layout
+    // (registers and LDS), with the even row padding if that is what keeps
+    // them. Measured on MI355X (us per forward, k = 5): B128 C96 56 x 56 L = 5
+    // 153.6 -> 137.0 (bf16 154.1 -> 136.2; merged it needs 10272 floats with
+    // 4-float rows, past the 10240 of four workgroups, and 10140 with 2-float
+    // rows); B64 C96 48 x 48 L = 5 79.0 -> 70.2 and 45 x 45 89.5 -> 78.3 (5
+    // workgroups' LDS down to 4, which the registers allow anyway). Merged at
+    // one workgroup fewer it was slower: 56 x 56 L = 5 +4.6 %, k = 7 40 x 40
+    // L = 3 +12 %.
     if (!bwd && pl.one_round && d.L >= 3 && pl.g.lv[1].T == 4) {
-        PlaneGeom gm;
-        if (layout(d, PP, bwd, gm, true, pref_used, kMaxLevels + 1, false, true)) {
+        const int reg_wgs = forward_wgs(d, true);
+        for (int p2 = 0; p2 < 2 && !pl.merge_deep; ++p2) {
+            PlaneGeom gm;
+            if (!layout(d, PP, bwd, gm, true, pref_used, kMaxLevels + 1, false, true, 4, p2 == 1)) continue;
             long lanes = (long)PP * (gm.lv[1].eh / 4) * (gm.lv[1].ew / 4);
             for (int l = 3; l <= d.L; ++l) lanes += (long)PP * (gm.lv[l].eh / 4) * (gm.lv[l].ew / 4);
             const int lds = lds_floats_for(d, bwd, PP, gm);
-            // if it keeps the workgroups per CU of the unmerged layout
-            if (lanes <= 64 && lds <= kLdsFloatsMax && lds_wgs(lds) >= lds_wgs(pl.lds_floats)) {
+            if (lanes <= 64 && lds <= kLdsFloatsMax &&
+                std::min(reg_wgs, lds_wgs(lds)) >= std::min(reg_wgs, lds_wgs(pl.lds_floats))) {
                 pl.g = gm;
                 pl.lds_floats = lds;
                 pl.merge_deep = 1;
@@ -658,7 +678,56 @@ bool want_split(const wtconv_desc& d, bool bwd, int m, int full_lds, int split_l
     return m == 1 || deep >= 2 || (lds_wgs(full_lds) < 2 && lds_wgs(split_lds) >= 2);
 }
 
+// Plans by descriptor. The plan search costs tens of microseconds of host
+// time for small planes (every resident-plane count, tile layout and
+// mixed-round packing is tried), as long as the kernels it plans: uncached,
+// a loop of 12 x 12 forwards left the GPU waiting on it. A fixed table of the
+// last kSlots descriptors, replaced round-robin; lookups and inserts hold a
+// mutex, the search runs outside it (two threads that miss on the same
+// descriptor compute the same plan). Plans depend only on the descriptor and
+// on the compiled kernels' register counts.
+template <typename V>
+class PlanCache {
+  public:
+    template <typename F>
+    V get(const wtconv_desc& d, int tag, F compute)
+    {
+        const Key key = {{d.B, d.C, d.H, d.W, d.k, d.L, (int)d.dtype, tag}};
+        {
+            std::lock_guard<std::mutex> lock(mu_);
+            for (int i = 0; i < n_; ++i)
+                if (keys_[i] == key) return vals_[i];
+        }
+        const V v = compute();
+        std::lock_guard<std::mutex> lock(mu_);
+        const int slot = n_ < kSlots ? n_++ : (int)(next_++ % kSlots);
+        keys_[slot] = key;
+        vals_[slot] = v;
+        return v;
+    }
+
+  private:
+    struct Key {
+        int v[8];
+        bool operator==(const Key& o) const { return memcmp(v, o.v, sizeof(v)) == 0; }
+    };
+    static constexpr int kSlots = 64;
+    std::mutex mu_;
+    Key keys_[kSlots];
+    V vals_[kSlots];
+    int n_ = 0;
+    unsigned next_ = 0;
+};
+
+Exec choose_uncached(const wtconv_desc& d, bool bwd);
+
 Exec choose(const wtconv_desc& d, bool bwd)
+{
+    static PlanCache<Exec> cache;
+    return cache.get(d, bwd ? 1 : 0, [&] { return choose_uncached(d, bwd); });
+}
+
+Exec choose_uncached(const wtconv_desc& d, bool bwd)
 {
     Exec ex;
     if (use_tiny(d)) {
@@ -903,7 +972,15 @@ bool grad_pass_pays_deep(const wtconv_desc& d)
     return d.k >= 5;
 }
 
+GradExec choose_grad_uncached(const wtconv_desc& d);
+
 GradExec choose_grad(const wtconv_desc& d)
+{
+    static PlanCache<GradExec> cache;
+    return cache.get(d, 2, [&] { return choose_grad_uncached(d); });
+}
+
+GradExec choose_grad_uncached(const wtconv_desc& d)
 {
     GradExec ge;
     if (use_tiny(d) || d.L < 1) return ge;
@@ -1021,7 +1098,19 @@ bool dx_pass_plan(const wtconv_desc& d, int m, Plan& pl)
 {
     wtconv_desc f = d;
     f.L = m;
-    return m >= 1 && !use_tiny(d) && make_plan(f, false, pl);
+    if (m < 1 || use_tiny(d)) return false;
+    struct Found {
+        bool ok;
+        Plan pl;
+    };
+    static PlanCache<Found> cache;
+    const Found r = cache.get(f, 3, [&] {
+        Found v;
+        v.ok = make_plan(f, false, v.pl);
+        return v;
+    });
+    if (r.ok) pl = r.pl;
+    return r.ok;
 }
 
 // [X_m][dY_m][dX_m][coarse backward]
