@@ -237,14 +237,13 @@ def config_table(steps, dev, table_out=None):
             x = torch.randn(B, C, H, W, generator=gen, device=dev).to(tdt[dt])
             dy = torch.randn(B, C, H, W, generator=gen, device=dev).to(tdt[dt])
             sets.append((x, dy, torch.empty_like(x), torch.empty_like(x)))
-        fws = torch.empty(max(1, binding.wtconv_forward_workspace_bytes(
-            binding.make_desc(B, C, H, W, k, L, binding._dtype_code(sets[0][0])))), dtype=torch.uint8, device=dev)
+        fw = binding.Forward(sets[0][0], bw, bs, lw, ls)
         bk = binding.Backward(sets[0][0], bw, bs, lw, ls, need_dx=True)
 
         def run(n, with_bwd):
             for i in range(n):
                 x, dy, y, dx = sets[i % nsets]
-                binding.forward(x, bw, bs, lw, ls, out=y, workspace=fws)
+                fw.run(x, y)
                 if with_bwd:
                     bk.run(x, dy, dx)
 
@@ -278,7 +277,7 @@ def config_table(steps, dev, table_out=None):
         log(f"table: {name:28s} fwd {fwd_ms * 1e3:8.1f} us  fwd+bwd {fb_ms * 1e3:8.1f} us  "
             f"{row['fwdbwd_GBps']:7.1f} GB/s  hbm {row['fwdbwd_hbm_frac']:.3f}  fma {row['fwdbwd_fma_frac']:.3f}")
         rows.append(row)
-        del sets, bk, fws
+        del sets, bk, fw
         torch.cuda.empty_cache()
     if table_out:
         with open(table_out, "w") as f:
@@ -772,8 +771,7 @@ class Step:
             x = self.x0 if s == 0 else self.x0.clone()
             dy = self.dy0 if s == 0 else self.dy0.clone()
             self.sets.append((x, dy, torch.empty_like(x), torch.empty_like(x)))
-        self.fws = torch.empty(max(1, binding.wtconv_forward_workspace_bytes(
-            binding.make_desc(B, C, H, W, k, L, binding._dtype_code(self.x0)))), dtype=torch.uint8, device=dev)
+        self.fw = binding.Forward(self.x0, self.bw, self.bs, self.lw, self.ls)
         self.bk = binding.Backward(self.x0, self.bw, self.bs, self.lw, self.ls, need_dx=True)
         self.bk_nodx = None  # split(): the gradient pass alone, dx from wtconv_backward_data
         self.binding = binding
@@ -785,7 +783,7 @@ class Step:
         x, dy, y, dx = self.sets[i % len(self.sets)]
         if ev is not None:
             ev[0].record()
-        self.binding.forward(x, self.bw, self.bs, self.lw, self.ls, out=y, workspace=self.fws)
+        self.fw.run(x, y)
         if ev is not None:
             ev[1].record()
         self.bk.run(x, dy, dx)
@@ -803,7 +801,7 @@ class Step:
         bk = self.bk_nodx
         x, dy, y, dx = self.sets[i % len(self.sets)]
         ev[0].record()
-        self.binding.forward(x, self.bw, self.bs, self.lw, self.ls, out=y, workspace=self.fws)
+        self.fw.run(x, y)
         ev[1].record()
         bk.partials(x, dy, None)
         ev[2].record()

@@ -330,6 +330,42 @@ def backward_data(dy, base_w, base_scale, level_w, level_scale, out=None, worksp
     return dx
 
 
+class Forward:
+    """Prepared forward of one problem shape for loops that call it many times
+    (serving, benchmarks): the parameters are validated once and their
+    pointer arrays and the workspace are built once; `run(x, y)` checks that
+    x and y match the prepared shape, dtype and device and calls
+    wtconv_forward on the current stream. The parameters are kept by
+    reference: later in-place updates to them are seen by later calls."""
+
+    def __init__(self, x, base_w, base_scale, level_w, level_scale, bias=None):
+        import torch
+        B, C, H, W, k, L = validate(x, base_w, base_scale, level_w, level_scale, bias=bias)
+        self.desc = make_desc(B, C, H, W, k, L, _dtype_code(x))
+        self.x_like = (tuple(x.shape), x.dtype, x.device)
+        self.nbytes = wtconv_forward_workspace_bytes(self.desc)
+        self.workspace = torch.empty(self.nbytes, dtype=torch.uint8, device=x.device) if self.nbytes else None
+        self.params = (base_w, base_scale, list(level_w), list(level_scale), bias)
+        self.device = x.device
+        self._fn = load().wtconv_forward
+        self._desc_ref = ctypes.byref(self.desc)
+        self._lw = _ptr_array([t.data_ptr() for t in level_w])
+        self._ls = _ptr_array([t.data_ptr() for t in level_scale])
+        self._bw, self._bs = base_w.data_ptr(), base_scale.data_ptr()
+        self._bias = bias.data_ptr() if bias is not None else None
+        self._ws = self.workspace.data_ptr() if self.workspace is not None else None
+        self._nbytes = ctypes.c_size_t(self.nbytes)
+
+    def run(self, x, y):
+        """y = WTConv(x) into the preallocated `y`."""
+        shape, dtype, device = self.x_like
+        _require(x, "x", dtype, shape, device)
+        _require(y, "y", dtype, shape, device)
+        _check(self._fn(self._desc_ref, x.data_ptr(), self._bw, self._bs, self._bias, self._lw, self._ls,
+                        y.data_ptr(), self._ws, self._nbytes, _stream(self.device)))
+        return y
+
+
 class Backward:
     """Preallocated backward of one problem: whole (wtconv_backward, `run`) or
     in its two phases (used by the benchmark to time the passes separately)."""

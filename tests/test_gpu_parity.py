@@ -412,6 +412,31 @@ def test_identity_pattern_reproduces_input():
     assert rel_err(y, inp.x) < 1e-6
 
 
+@pytest.mark.parametrize("B,C,H,W,k,L,dtype,with_bias", [(2, 3, 13, 11, 5, 3, "f32", False),
+                                                          (1, 2, 130, 126, 5, 3, "f32", True),
+                                                          (70, 3, 7, 6, 5, 4, "bf16", False)])
+def test_prepared_forward_matches(B, C, H, W, k, L, dtype, with_bias):
+    """binding.Forward (parameters validated once, workspace kept) gives
+    bit-for-bit the output of binding.forward, on repeated calls and across
+    inputs; it refuses activations of another shape before any library call."""
+    from paper_2608_10805_amd import binding
+    from paper_2608_10805_amd.inputs import make_bias
+
+    inp, dev = setup(B, C, H, W, k, L, dtype)
+    bias = torch.from_numpy(make_bias(C)).to("cuda:0") if with_bias else None
+    fw = binding.Forward(dev.x, dev.bw, dev.bs, dev.lw, dev.ls, bias=bias)
+    ref = binding.forward(dev.x, dev.bw, dev.bs, dev.lw, dev.ls, bias=bias)
+    x2 = dev.x.flip(-1).contiguous()
+    ref2 = binding.forward(x2, dev.bw, dev.bs, dev.lw, dev.ls, bias=bias)
+    y = torch.empty_like(dev.x)
+    for _ in range(2):
+        assert torch.equal(fw.run(dev.x, y), ref)
+        assert torch.equal(fw.run(x2, y), ref2)
+    torch.cuda.synchronize()
+    with pytest.raises(ValueError):
+        fw.run(dev.x, torch.empty(B, C, H + 1, W, dtype=dev.x.dtype, device="cuda:0"))
+
+
 def test_autograd_module_matches_binding():
     from paper_2608_10805_amd.autograd import WTConv2d
 
