@@ -392,6 +392,12 @@ class Backward:
         self.device = x.device
         self.data_nbytes = wtconv_backward_data_workspace_bytes(self.desc)
         self.data_workspace = None
+        # the whole call's fixed arguments, marshalled once for run()
+        self._run_fn = load().wtconv_backward
+        self._run_fixed = (ctypes.byref(self.desc), base_w.data_ptr(), base_scale.data_ptr(), None,
+                           _ptr_array(self._lw), _ptr_array(self._ls))
+        self._run_grads = (self.dbw.data_ptr(), self.dbs.data_ptr(), None, _ptr_array(self._dlw),
+                           _ptr_array(self._dls), self.workspace.data_ptr(), ctypes.c_size_t(self.nbytes))
 
     def _check_act(self, name, t):
         shape, dtype, device = self.x_like
@@ -401,15 +407,13 @@ class Backward:
         """wtconv_backward into the preallocated gradients; dx into `dx`, else
         into the preallocated buffer when the object was made with need_dx,
         else skipped."""
-        bw, bs, _, _ = self.params
         out = dx if dx is not None else self.dx
         for name, t in (("x", x), ("dy", dy), ("dx", out)):
             if t is not None:
                 self._check_act(name, t)
-        _check(wtconv_backward(self.desc, x.data_ptr(), dy.data_ptr(), bw.data_ptr(), bs.data_ptr(), None, self._lw,
-                               self._ls, out.data_ptr() if out is not None else None, self.dbw.data_ptr(),
-                               self.dbs.data_ptr(), None, self._dlw, self._dls, self.workspace.data_ptr(),
-                               self.nbytes, _stream(self.device)))
+        desc, bw, bs, bias, lw, ls = self._run_fixed
+        _check(self._run_fn(desc, x.data_ptr(), dy.data_ptr(), bw, bs, bias, lw, ls,
+                            out.data_ptr() if out is not None else None, *self._run_grads, _stream(self.device)))
 
     def partials(self, x, dy, dx=None):
         """Writes dx into `dx`, else into the preallocated buffer when the
