@@ -242,3 +242,29 @@ def test_noalloc_scratch_covers_the_convnext_stage_shapes():
             for dt in (0, 1):
                 n = binding.wtconv_backward_workspace_bytes(make_desc(128, C, H, H, 5, L, dt))
                 assert 0 < n <= binding.NOALLOC_SCRATCH_BYTES, (C, H, L, dt, n)
+
+
+def test_plan_cache_under_threads():
+    """Plans are cached by descriptor in a fixed table shared by all threads:
+    sizes queried from several threads at once, over more descriptors than
+    the table holds (so entries are replaced while others are read), equal
+    the sizes of a sequential pass."""
+    import itertools
+    from concurrent.futures import ThreadPoolExecutor
+
+    descs = [(B, C, H, H, k, L) for B, C in ((2, 3), (64, 96)) for H in (7, 14, 28, 56, 130)
+             for k in (3, 5, 7) for L in (1, 3, 5)]
+    assert len(descs) > 64
+
+    def sizes(d):
+        desc = make_desc(*d)
+        return (binding.wtconv_forward_workspace_bytes(desc), binding.wtconv_backward_workspace_bytes(desc),
+                binding.wtconv_backward_data_workspace_bytes(desc))
+
+    want = [sizes(d) for d in descs]
+    order = list(itertools.chain.from_iterable([descs, descs[::-1], descs[::3]] * 3))
+    with ThreadPoolExecutor(8) as pool:
+        got = list(pool.map(sizes, order))
+    index = {d: i for i, d in enumerate(descs)}
+    assert all(g == want[index[d]] for d, g in zip(order, got))
+
