@@ -442,6 +442,13 @@ bool make_plan(const wtconv_desc& d, bool bwd, Plan& pl, bool allow_mixed = true
             const long lds = (long)(1 + 4 * d.L) * KP + (long)pp * g.plane_floats;
             if (lds > kLdsFloatsMax) continue;
             const int wgs = std::min(mixed_wgs(d, m.rounds), lds_wgs(lds));
+            // only plane counts that keep the workgroups per CU of the plan
+            // compete (the cheapest count overall may not, and used to veto
+            // the mixed rounds altogether: B128 C192 12 x 12 L = 2 forward
+            // 30.3 -> 24.2 us, L = 3 34.5 -> 28.5, 10 x 10 L = 3 35.4 ->
+            // 30.1, 9 x 9 L = 2 B64 21.2 -> 18.1, k = 3 B128 C384 14 x 14
+            // L = 3 58.6 -> 49.3)
+            if (wgs < std::min(wgs_f, 3)) continue;
             const double cost = issue_mixed(d, pp, m);
             if (best < 0 || cost < best || (cost == best && wgs > best_wgs)) {
                 best = cost;
@@ -452,7 +459,7 @@ bool make_plan(const wtconv_desc& d, bool bwd, Plan& pl, bool allow_mixed = true
                 mp.lds_floats = (int)lds;
             }
         }
-        if (best >= 0 && best <= kMixedGain * cost_f && best_wgs >= std::min(wgs_f, 3)) {
+        if (best >= 0 && best <= kMixedGain * cost_f) {
             pl.g = mp.g;
             pl.mx = mp.mx;
             pl.PP = PP = mp.PP;

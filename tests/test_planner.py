@@ -68,9 +68,9 @@ def test_convnext_stage_modes(planner, C, H, L, fwd_mode):
 
 def test_tile_row_padding_keeps_the_busy_wavefronts(planner):
     """Padding tile rows to 8 lanes is skipped where it would put work on more
-    wavefronts: 12 x 12 planes have 3 tiles per row (7 planes: 63 tiles, one
-    wavefront; padded, three)."""
-    p = planner(128, 192, 12, 12, 5, 3)
+    wavefronts: 12 x 12 planes have 3 tiles per row (at L = 4, 16 planes: 144
+    tiles on three wavefronts; padded, more)."""
+    p = planner(128, 192, 12, 12, 5, 4)
     assert p["fwd_mx_rounds"] == 0 and p["fwd_one_round"] == 1
     assert p["fwd_tiles_xl"] == p["fwd_tiles_x"] == 3
     p = planner(64, 192, 28, 28, 5, 1)
