@@ -1305,11 +1305,25 @@ wtconv_status forward_impl(const wtconv_desc& d, const void* x, const wtc::Param
 
 // cx, cdy (nullable): also write the level-cm (1 or 2) carriers of x and dy
 // there, as carrier() would.
+// rp (nullable): region mode, over the region tiles of rp with its chunks.
 wtconv_status grad_pass(const wtconv_desc& d, const GradExec& ge, const void* x, const void* dy, float* partial,
-                        int skip_base, hipStream_t stream, void* cx = nullptr, void* cdy = nullptr, int cm = 0)
+                        int skip_base, hipStream_t stream, void* cx = nullptr, void* cdy = nullptr, int cm = 0,
+                        const RegionPlan* rp = nullptr)
 {
     wtc::GradArgs a;
     memset(&a, 0, sizeof(a));
+    int grid = ge.gp.nchunks * d.C;
+    a.nb = ge.gp.nb;
+    if (rp) {
+        a.rg_ntx = rp->ntx;
+        a.rg_nty = rp->nty;
+        a.rg_T = rp->T;
+        a.rg_h = rp->h;
+        a.real_H = d.H;
+        a.real_W = d.W;
+        a.nb = rp->pl.nb;
+        grid = rp->pl.nchunks * rp->ntx * rp->nty * d.C;
+    }
     if (cx) {
         const wtconv_desc cd = coarse_desc(d, cm);
         a.cx = cx;
@@ -1323,7 +1337,6 @@ wtconv_status grad_pass(const wtconv_desc& d, const GradExec& ge, const void* x,
     a.partial = partial;
     a.B = d.B;
     a.C = d.C;
-    a.nb = ge.gp.nb;
     a.PP = ge.gp.PP;
     a.rounds = ge.gp.rounds;
     a.vec_ok = vec_ok(x, dy, x);
@@ -1339,15 +1352,76 @@ wtconv_status grad_pass(const wtconv_desc& d, const GradExec& ge, const void* x,
         a.dy_band[l] = ge.gp.dy_band[l];
     }
     a.g = ge.gp.g;
-    return hip_status(wtc::launch_grad(d.k, d.dtype, a, ge.gp.nchunks * d.C, stream));
+    return hip_status(wtc::launch_grad(d.k, d.dtype, a, grid, stream));
+}
+
+// Backward of a problem in region mode by the gradient route: the gradient
+// pass over the same region tiles and chunks as the fused region backward
+// (so the partials, the workspace and the finalize are the same), writing
+// the level-1 carriers of x and dy from the tiles' own blocks; the coarse
+// sub-problem's backward on them; dx as the forward on dy with rotated
+// kernels over levels 1..1 with the coarse input gradient as its carry.
+// False (nothing launched) if the region does not fit one block round.
+constexpr bool kRegionGradRoute = true;
+
+bool region_grad_exec(const wtconv_desc& d, const Exec& ex, GradExec& ge)
+{
+    if (!kRegionGradRoute || ex.mode != Mode::Region || ex.m != 1) return false;
+    wtconv_desc rd = d;
+    rd.B = 1;
+    rd.H = rd.W = ex.rp.T + 2 * ex.rp.h;
+    rd.L = 1;
+    if (!make_grad_plan(rd, ge.gp) || ge.gp.PP != 1 || ge.gp.rounds != 1 || ge.gp.g.L != 1) return false;
+    ge.use = true;
+    ge.Lf = 1;
+    ge.coarse = ex.coarse;
+    return true;
+}
+
+wtconv_status partials_impl(const wtconv_desc& d, const void* x, const void* dy, const wtc::ParamPtrs& p,
+                            void* dx, char* ws, int skip_base, hipStream_t stream, const Grads* gr = nullptr,
+                            bool* fin_done = nullptr);
+
+wtconv_status region_grad_backward(const wtconv_desc& d, const Exec& ex, const GradExec& ge, const void* x,
+                                   const void* dy, const wtc::ParamPtrs& p, void* dx, char* ws, int skip_base,
+                                   hipStream_t stream)
+{
+    const size_t part = pass_partial_bytes(d, ex);
+    void* x1 = nullptr;
+    void* dy1 = nullptr;
+    void* dx1 = nullptr;
+    if (ex.coarse) {
+        const size_t n1 = level_bytes(d, 1);
+        x1 = ws + part;
+        dy1 = ws + part + n1;
+        dx1 = dx ? ws + part + 2 * n1 : nullptr;
+    }
+    wtconv_status st = grad_pass(d, ge, x, dy, reinterpret_cast<float*>(ws), skip_base, stream, x1, dy1, x1 ? 1 : 0,
+                                 &ex.rp);
+    if (st == WTCONV_OK && ex.coarse)
+        st = partials_impl(coarse_desc(d, 1), x1, dy1, shift_params(p, 1), dx1, ws + part + 3 * level_bytes(d, 1), 1,
+                           stream, nullptr, nullptr);
+    if (st != WTCONV_OK || !dx) return st;
+    wtc::ParamPtrs pr = p;
+    pr.rot = 1;
+    pr.b0 = nullptr;  // the bias does not reach dx
+    wtconv_desc f = d;
+    f.L = 1;
+    const Exec fx = choose(f, false);
+    if (fx.mode != Mode::Region && fx.mode != Mode::Resident) return WTCONV_ERR_UNSUPPORTED;
+    const FusedPass fp = fused_pass(f, fx);
+    FusedArgs a = base_args(f, *fp.pl, dy, nullptr, dx, pr, skip_base);
+    if (fx.mode == Mode::Region) set_region(a, f, fx.rp);
+    if (dx1) set_carry(a, d, 1, dx1);
+    return hip_status(wtc::launch_forward(d.k, d.dtype, a, fp.grid, stream));
 }
 
 // With `gr` (the combined backward), the finalize of the kernel gradients of
 // levels 0..Lf of the gradient route runs at the end of the dx launch when it
 // can; *fin_done then tells finalize_impl to skip it.
 wtconv_status partials_impl(const wtconv_desc& d, const void* x, const void* dy, const wtc::ParamPtrs& p,
-                            void* dx, char* ws, int skip_base, hipStream_t stream, const Grads* gr = nullptr,
-                            bool* fin_done = nullptr)
+                            void* dx, char* ws, int skip_base, hipStream_t stream, const Grads* gr,
+                            bool* fin_done)
 {
     const GradExec ge = choose_grad(d);
     if (ge.use) {
@@ -1413,6 +1487,10 @@ wtconv_status partials_impl(const wtconv_desc& d, const void* x, const void* dy,
     if (ex.mode == Mode::Tiny)
         return hip_status(wtc::launch_tiny(
             d.k, d.dtype, true, tiny_args(d, dy, x, dx, reinterpret_cast<float*>(ws), p, skip_base), stream));
+    {
+        GradExec rge;
+        if (region_grad_exec(d, ex, rge)) return region_grad_backward(d, ex, rge, x, dy, p, dx, ws, skip_base, stream);
+    }
     const size_t part = pass_partial_bytes(d, ex);
     const void* carry = nullptr;
     if (ex.coarse) {

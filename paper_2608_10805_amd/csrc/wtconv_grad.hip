@@ -62,9 +62,11 @@ struct DyLevel {
 // Level correlation of band q over T x T site tiles of every resident plane:
 //   acc[p][t] += sum over sites s of dY(s) * X(s + (p - R, t - R)),
 // dY from the compact dy pyramid, X from the zero-haloed x pyramid.
-template <int K, int T>
+// RGN: only the sites [m0, m1) x [m0, m1) of the region's grid count (the
+// tile's own); the dy values of the others are taken as zero.
+template <int K, int T, bool RGN>
 DEV void grad_band_tiles(const float* __restrict__ region0, int stride, const LevelGeom& xl, DyLevel dl, int q,
-                         int np, float (&acc)[K * K], int lane)
+                         int np, float (&acc)[K * K], int lane, int m0, int m1)
 {
     const int tx = xl.ew / T;
     const int per = tx * (xl.eh / T);
@@ -73,20 +75,29 @@ DEV void grad_band_tiles(const float* __restrict__ region0, int stride, const Le
         const float* base = region0 + ti.p * stride;
         float ctr[T][T];
         load_tile<T>(base + dl.off + q * dl.band, dl.pitch, ti.j0, ti.i0, ctr);
+        if constexpr (RGN) {
+#pragma unroll
+            for (int r = 0; r < T; ++r)
+#pragma unroll
+                for (int c = 0; c < T; ++c) {
+                    const int j = ti.j0 + r, i = ti.i0 + c;
+                    if (j < m0 || j >= m1 || i < m0 || i >= m1) ctr[r][c] = 0.f;
+                }
+        }
         corr_tile<K, T>(base + xl.off + q * xl.band, xl.pitch, ti.j0, ti.i0, ctr, acc);
     }
 }
 
-template <int K>
+template <int K, bool RGN = false>
 DEV void grad_band(const float* region0, int stride, const LevelGeom& xl, DyLevel dl, int q, int np,
-                   float (&acc)[K * K], int lane)
+                   float (&acc)[K * K], int lane, int m0 = 0, int m1 = 0)
 {
     if (xl.T == 4)
-        grad_band_tiles<K, 4>(region0, stride, xl, dl, q, np, acc, lane);
+        grad_band_tiles<K, 4, RGN>(region0, stride, xl, dl, q, np, acc, lane, m0, m1);
     else if (xl.T == 2)
-        grad_band_tiles<K, 2>(region0, stride, xl, dl, q, np, acc, lane);
+        grad_band_tiles<K, 2, RGN>(region0, stride, xl, dl, q, np, acc, lane, m0, m1);
     else
-        grad_band_tiles<K, 1>(region0, stride, xl, dl, q, np, acc, lane);
+        grad_band_tiles<K, 1, RGN>(region0, stride, xl, dl, q, np, acc, lane, m0, m1);
 }
 
 // One CW-site chunk of a site row for the row-wise correlation below:
@@ -248,10 +259,13 @@ constexpr int grad_waves_per_simd() { return K <= 5 ? 3 : (K <= 7 ? 2 : 1); }
 // DR: L >= 4; levels 3..5 keep their sums in registers too (another 3k per
 // lane, an instantiation of its own so that shallower pyramids keep the
 // smaller register budget).
-template <int K, typename ST, bool MR, bool DR>
+// RGN: region mode (one block round, one resident region, L = 1; see
+// GradArgs).
+template <int K, typename ST, bool MR, bool DR, bool RGN>
 __global__ void __launch_bounds__(kThreads, grad_waves_per_simd<K>()) grad_kernel(const GradArgs a)
 {
     constexpr int R = K / 2, KK = K * K;
+    static_assert(!RGN || (!MR && !DR), "region mode takes one block round and level 1 only");
     extern __shared__ float4 lds4[];
     float* lds = reinterpret_cast<float*>(lds4);
 
@@ -259,13 +273,20 @@ __global__ void __launch_bounds__(kThreads, grad_waves_per_simd<K>()) grad_kerne
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int C = a.C;
     const int c = blockIdx.x % C;
-    const int chunk = blockIdx.x / C;
+    const int ct = blockIdx.x / C;  // chunk (region mode: chunk * tiles + tile)
+    const int ntiles = RGN ? a.rg_ntx * a.rg_nty : 1;
+    const int chunk = ct / ntiles;
+    const int tile = ct - chunk * ntiles;
     const int b_begin = chunk * a.nb;
     const int b_end = min(a.B, b_begin + a.nb);
     const int L = g.L;
-    const long HW = (long)g.H * g.W;
+    // region mode: origin of the region in the real plane (multiples of 4)
+    const int oy = RGN ? (tile / a.rg_ntx) * a.rg_T - a.rg_h : 0;
+    const int ox = RGN ? (tile % a.rg_ntx) * a.rg_T - a.rg_h : 0;
+    const int PH = RGN ? a.real_H : g.H, PW = RGN ? a.real_W : g.W;  // the real plane
+    const long HW = (long)PH * PW;
     const bool skip_base = a.skip_base != 0;
-    const int vw = a.vec_ok == 0 ? 1 : ((g.W % 4) == 0 ? 4 : ((g.W % 2) == 0 ? 2 : 1));  // row vector width
+    const int vw = a.vec_ok == 0 ? 1 : ((PW % 4) == 0 ? 4 : ((PW % 2) == 0 ? 2 : 1));  // row vector width
     const bool alias1 = L >= 1 && a.dy_off[1] == 0;  // dy level 1 is stored over the x plane
     const int q = wave;                              // the subband this wavefront correlates
 
@@ -343,6 +364,10 @@ __global__ void __launch_bounds__(kThreads, grad_waves_per_simd<K>()) grad_kerne
         if constexpr (!MR) {
             const bool mine = tl < np * per;  // at most one block per thread (planned on the host)
             const TileIdx ti = tile_at(mine ? tl : 0, per, g.r_tiles, g.tiles_x, g.r_tiles_x, 4);
+            // region mode: the blocks of the tile's own pixels (rg_h and rg_T
+            // are multiples of 4, so a block is wholly inside or outside)
+            const bool inner = !RGN || (ti.j0 >= a.rg_h && ti.j0 < a.rg_h + a.rg_T && ti.i0 >= a.rg_h &&
+                                        ti.i0 < a.rg_h + a.rg_T);
 
             // 1. x block -> LDS with its levels 1-2; dy block in registers
             if (alias1 && b0 != b_begin)
@@ -351,19 +376,20 @@ __global__ void __launch_bounds__(kThreads, grad_waves_per_simd<K>()) grad_kerne
             if (mine) {
                 const long plane = (long)(b0 + ti.p) * C + c;
                 float v[4][4];
-                fetch_block<ST>(xs + plane * HW, g.H, g.W, ti.j0, ti.i0, vw, v);
+                fetch_block<ST>(xs + plane * HW, PH, PW, oy + ti.j0, ox + ti.i0, vw, v);
                 store_block<K>(v, planes + ti.p * stride, g, ti.j0, ti.i0);
-                fetch_block<ST>(dys + plane * HW, g.H, g.W, ti.j0, ti.i0, vw, dyb);
-                if (a.cx) {
+                fetch_block<ST>(dys + plane * HW, PH, PW, oy + ti.j0, ox + ti.i0, vw, dyb);
+                if (a.cx && inner) {
                     const long co = plane * a.cH * a.cW;
-                    write_carrier<ST>(reinterpret_cast<ST*>(a.cx) + co, a.cH, a.cW, a.cm, ti.j0, ti.i0, v);
-                    write_carrier<ST>(reinterpret_cast<ST*>(a.cdy) + co, a.cH, a.cW, a.cm, ti.j0, ti.i0, dyb);
+                    write_carrier<ST>(reinterpret_cast<ST*>(a.cx) + co, a.cH, a.cW, a.cm, oy + ti.j0, ox + ti.i0, v);
+                    write_carrier<ST>(reinterpret_cast<ST*>(a.cdy) + co, a.cH, a.cW, a.cm, oy + ti.j0, ox + ti.i0,
+                                      dyb);
                 }
             }
             __syncthreads();
 
             // 2. base correlation; x level 3
-            if (mine && !skip_base) base_corr(ti, dyb);
+            if (mine && inner && !skip_base) base_corr(ti, dyb);
             if (L >= 3) {
                 const LevelGeom& lg = g.lv[3];
                 const LevelGeom& lp = g.lv[2];
@@ -440,7 +466,7 @@ __global__ void __launch_bounds__(kThreads, grad_waves_per_simd<K>()) grad_kerne
             const LevelGeom& xl = g.lv[l];
             const DyLevel dl = {a.dy_off[l], a.dy_pitch[l], a.dy_band[l]};
             if (l == 1)
-                grad_band<K>(planes, stride, xl, dl, q, np, g1, ll);
+                grad_band<K, RGN>(planes, stride, xl, dl, q, np, g1, ll, a.rg_h >> 1, (a.rg_h + a.rg_T) >> 1);
             else if (l == 2)
                 grad_rows_acc<K>(planes, stride, xl, dl, q, np, g2, ll);
             else if (DR && l <= RL) {
@@ -495,7 +521,7 @@ __global__ void __launch_bounds__(kThreads, grad_waves_per_simd<K>()) grad_kerne
     const float vdy = wave_sum(gdy);
     if (lane == 0) red[(RL + 1) * kWaves * KK + wave] = vdy;
     __syncthreads();
-    float* dst = a.partial + ((long)chunk * C + c) * NP;
+    float* dst = a.partial + ((long)ct * C + c) * NP;
     for (int t = tid; t < KK; t += kThreads) dst[t] = ((red[t] + red[KK + t]) + red[2 * KK + t]) + red[3 * KK + t];
     if (tid == 0) {
         const float* r = red + (RL + 1) * kWaves * KK;
@@ -506,20 +532,25 @@ __global__ void __launch_bounds__(kThreads, grad_waves_per_simd<K>()) grad_kerne
     for (int i = tid; i < 4 * KK * (L - RL); i += kThreads) dst[KK + 4 * RL * KK + i] = gco[i];
 }
 
-template <int K, typename ST, bool MR, bool DR>
+template <int K, typename ST, bool MR, bool DR, bool RGN = false>
 hipError_t launch_grad_v(const GradArgs& a, int grid, hipStream_t s)
 {
     const size_t bytes = (size_t)a.lds_floats * sizeof(float);
     static std::atomic<unsigned long long> lds_done{0};
-    const hipError_t e = allow_full_lds(reinterpret_cast<const void*>(&grad_kernel<K, ST, MR, DR>), lds_done);
+    const hipError_t e = allow_full_lds(reinterpret_cast<const void*>(&grad_kernel<K, ST, MR, DR, RGN>), lds_done);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((grad_kernel<K, ST, MR, DR>), dim3(grid), dim3(kThreads), bytes, s, a);
+    hipLaunchKernelGGL((grad_kernel<K, ST, MR, DR, RGN>), dim3(grid), dim3(kThreads), bytes, s, a);
     return hipGetLastError();
 }
 
 template <int K, typename ST>
 hipError_t launch_grad_t(const GradArgs& a, int grid, hipStream_t s)
 {
+    if (a.rg_ntx > 0) {
+        // one block round, one resident region, level 1 only (planned on the host)
+        if (a.rounds != 1 || a.PP != 1 || a.g.L != 1) return hipErrorInvalidValue;
+        return launch_grad_v<K, ST, false, false, true>(a, grid, s);
+    }
     if (a.rounds > 1) {
         if (a.PP != 1) return hipErrorInvalidValue;  // block rounds need one resident plane
         return a.g.L >= 4 ? launch_grad_v<K, ST, true, true>(a, grid, s) : launch_grad_v<K, ST, true, false>(a, grid, s);

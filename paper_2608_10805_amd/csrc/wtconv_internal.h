@@ -241,6 +241,14 @@ struct GradArgs {
     void* cx;
     void* cdy;
     int cm, cH, cW;
+    // Region mode (rg_ntx > 0; one block round, one resident region, L = 1):
+    // workgroup (chunk, tile) covers the rg_T x rg_T output tile whose
+    // top-left pixel is (ty * rg_T, tx * rg_T) of the real_H x real_W plane
+    // through a region with a halo of rg_h pixels on every side; g describes
+    // the region. Only the tile's own pixels and level-1 sites are counted,
+    // and carriers are written for the tile's own sites; partials are
+    // [nchunks * tiles][C][NP], tile-minor, as the fused region backward's.
+    int rg_ntx, rg_nty, rg_T, rg_h, real_H, real_W;
     PlaneGeom g;
 };
 

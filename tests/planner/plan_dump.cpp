@@ -38,7 +38,10 @@ int main()
         const Exec f = choose(d, false);
         const GradExec ge = choose_grad(d);
         const Exec b = choose(d, true);
-        printf("{\"fwd_mx_rounds\": %d, \"fwd_mx_first_out\": %d, \"fwd_mx_seg\": [", f.pl.mx.rounds,
+        GradExec rge;
+        const bool region_grad = !ge.use && region_grad_exec(d, b, rge);
+        printf("{\"bwd_region_grad\": %d, ", region_grad ? 1 : 0);
+        printf("\"fwd_mx_rounds\": %d, \"fwd_mx_first_out\": %d, \"fwd_mx_seg\": [", f.pl.mx.rounds,
                f.pl.mx.first_out);
         for (int r = 0; r < f.pl.mx.rounds; ++r) {
             printf("%s[", r ? ", " : "");
