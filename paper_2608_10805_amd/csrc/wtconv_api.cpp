@@ -38,6 +38,12 @@ constexpr int kBackwardTargetWorkgroups = 1536;
 // 128 x 128 L1 67.6 -> 59.1, 256 x 256 L3 292.6 -> 283.4; 512 x 512 within
 // 0.1 %. 3072 was slower everywhere (up to +13 %).
 constexpr int kRegionBackwardTargetWorkgroups = 768;
+// The gradient route over region tiles (grad_kernel, then the rotated forward
+// for dx) keeps less per workgroup and gains from a fuller grid: measured
+// (combined backward, us, 768 -> 1536, k = 5 L3): 224 x 224 B16 C64 576.0 ->
+// 541.3 (bf16 543.2 -> 504.0), 128 x 128 B8 C128 280.9 -> 264.9; 256 x 256 and
+// 512 x 512 within 1 %, 128 x 128 B8 C32 +1.2 %. 3072 lost up to 12 %.
+constexpr int kRegionGradTargetWorkgroups = 1536;
 
 int ceil_to(int v, int m) { return (v + m - 1) / m * m; }
 int cdiv(long a, long b) { return (int)((a + b - 1) / b); }
@@ -600,7 +606,7 @@ struct RegionPlan {
     int T = 0, h = 0, ntx = 0, nty = 0;
 };
 
-bool make_region_plan(const wtconv_desc& d, bool bwd, RegionPlan& rp)
+bool make_region_plan(const wtconv_desc& d, bool bwd, RegionPlan& rp, int target = 0)
 {
     // the carrier kernel decomposes small offsets with fp32 reciprocals
     if (d.H >= (1 << 19) || d.W >= (1 << 19)) return false;
@@ -618,7 +624,7 @@ bool make_region_plan(const wtconv_desc& d, bool bwd, RegionPlan& rp)
         rp.ntx = cdiv(d.W, T);
         rp.nty = cdiv(d.H, T);
         const long ntiles = (long)rp.ntx * rp.nty;
-        const int target = bwd ? kRegionBackwardTargetWorkgroups : kForwardTargetWorkgroups;
+        if (target <= 0) target = bwd ? kRegionBackwardTargetWorkgroups : kForwardTargetWorkgroups;
         const long chunks_target = std::max(1L, (target + d.C * ntiles - 1) / (d.C * ntiles));
         pl.nb = (int)((d.B + chunks_target - 1) / chunks_target);
         pl.nchunks = cdiv(d.B, pl.nb);
@@ -727,6 +733,7 @@ class PlanCache {
 };
 
 Exec choose_uncached(const wtconv_desc& d, bool bwd);
+bool region_grad_fits(const wtconv_desc& d, const Exec& ex);
 
 Exec choose(const wtconv_desc& d, bool bwd)
 {
@@ -769,6 +776,8 @@ Exec choose_uncached(const wtconv_desc& d, bool bwd)
         ex.mode = Mode::Region;
         ex.m = d.L > 0 ? 1 : 0;
         ex.coarse = d.L >= 2;
+        // the tile edge does not depend on the target, only the batch chunks
+        if (bwd && region_grad_fits(d, ex)) make_region_plan(d, bwd, ex.rp, kRegionGradTargetWorkgroups);
     }
     return ex;
 }
@@ -1376,6 +1385,12 @@ bool region_grad_exec(const wtconv_desc& d, const Exec& ex, GradExec& ge)
     ge.Lf = 1;
     ge.coarse = ex.coarse;
     return true;
+}
+
+bool region_grad_fits(const wtconv_desc& d, const Exec& ex)
+{
+    GradExec ge;
+    return region_grad_exec(d, ex, ge);
 }
 
 wtconv_status partials_impl(const wtconv_desc& d, const void* x, const void* dy, const wtc::ParamPtrs& p,
