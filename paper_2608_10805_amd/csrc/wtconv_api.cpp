@@ -39,10 +39,14 @@ constexpr int kBackwardTargetWorkgroups = 1536;
 // 0.1 %. 3072 was slower everywhere (up to +13 %).
 constexpr int kRegionBackwardTargetWorkgroups = 768;
 // The gradient route over region tiles (grad_kernel, then the rotated forward
-// for dx) keeps less per workgroup and gains from a fuller grid: measured
-// (combined backward, us, 768 -> 1536, k = 5 L3): 224 x 224 B16 C64 576.0 ->
-// 541.3 (bf16 543.2 -> 504.0), 128 x 128 B8 C128 280.9 -> 264.9; 256 x 256 and
-// 512 x 512 within 1 %, 128 x 128 B8 C32 +1.2 %. 3072 lost up to 12 %.
+// for dx) keeps less per workgroup and, when a region is one block round
+// (k <= 5), gains from a fuller grid: measured (combined backward, us, 768 ->
+// 1536, k = 5 L3): 224 x 224 B16 C64 576.0 -> 541.3 (bf16 543.2 -> 504.0),
+// 128 x 128 B8 C128 280.9 -> 264.9; 256 x 256 and 512 x 512 within 1 %,
+// 128 x 128 B8 C32 +1.2 %. 3072 lost up to 12 %. With two block rounds (k = 7,
+// 9) 768 stays ahead: 224 x 224 B16 C64 k = 7 L3 1380.3 -> 1353.1 at 768,
+// k = 9 L3 2444.8 -> 2355.2, k = 9 L1 2047.0 -> 1954.4; k = 7 128 x 128 B8
+// C128 751.8 -> 765.3.
 constexpr int kRegionGradTargetWorkgroups = 1536;
 
 int ceil_to(int v, int m) { return (v + m - 1) / m * m; }
@@ -733,7 +737,7 @@ class PlanCache {
 };
 
 Exec choose_uncached(const wtconv_desc& d, bool bwd);
-bool region_grad_fits(const wtconv_desc& d, const Exec& ex);
+bool region_grad_one_round(const wtconv_desc& d, const Exec& ex);
 
 Exec choose(const wtconv_desc& d, bool bwd)
 {
@@ -777,7 +781,7 @@ Exec choose_uncached(const wtconv_desc& d, bool bwd)
         ex.m = d.L > 0 ? 1 : 0;
         ex.coarse = d.L >= 2;
         // the tile edge does not depend on the target, only the batch chunks
-        if (bwd && region_grad_fits(d, ex)) make_region_plan(d, bwd, ex.rp, kRegionGradTargetWorkgroups);
+        if (bwd && region_grad_one_round(d, ex)) make_region_plan(d, bwd, ex.rp, kRegionGradTargetWorkgroups);
     }
     return ex;
 }
@@ -1365,12 +1369,13 @@ wtconv_status grad_pass(const wtconv_desc& d, const GradExec& ge, const void* x,
 }
 
 // Backward of a problem in region mode by the gradient route: the gradient
-// pass over the same region tiles and chunks as the fused region backward
-// (so the partials, the workspace and the finalize are the same), writing
-// the level-1 carriers of x and dy from the tiles' own blocks; the coarse
-// sub-problem's backward on them; dx as the forward on dy with rotated
-// kernels over levels 1..1 with the coarse input gradient as its carry.
-// False (nothing launched) if the region does not fit one block round.
+// pass over the same region tiles as the fused region backward (so the
+// partials and the finalize are the same), writing the level-1 carriers of x
+// and dy from the tiles' own blocks; the coarse sub-problem's backward on
+// them; dx as the forward on dy with rotated kernels over levels 1..1 with
+// the coarse input gradient as its carry. A region of more 4x4 blocks than
+// threads (k = 7 and 9) walks them in rounds. False (nothing launched) if the
+// region's gradient pass needs more than one resident region.
 constexpr bool kRegionGradRoute = true;
 
 bool region_grad_exec(const wtconv_desc& d, const Exec& ex, GradExec& ge)
@@ -1380,17 +1385,17 @@ bool region_grad_exec(const wtconv_desc& d, const Exec& ex, GradExec& ge)
     rd.B = 1;
     rd.H = rd.W = ex.rp.T + 2 * ex.rp.h;
     rd.L = 1;
-    if (!make_grad_plan(rd, ge.gp) || ge.gp.PP != 1 || ge.gp.rounds != 1 || ge.gp.g.L != 1) return false;
+    if (!make_grad_plan(rd, ge.gp) || ge.gp.PP != 1 || ge.gp.g.L != 1) return false;
     ge.use = true;
     ge.Lf = 1;
     ge.coarse = ex.coarse;
     return true;
 }
 
-bool region_grad_fits(const wtconv_desc& d, const Exec& ex)
+bool region_grad_one_round(const wtconv_desc& d, const Exec& ex)
 {
     GradExec ge;
-    return region_grad_exec(d, ex, ge);
+    return region_grad_exec(d, ex, ge) && ge.gp.rounds == 1;
 }
 
 wtconv_status partials_impl(const wtconv_desc& d, const void* x, const void* dy, const wtc::ParamPtrs& p,

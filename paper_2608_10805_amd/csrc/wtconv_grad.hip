@@ -259,13 +259,13 @@ constexpr int grad_waves_per_simd() { return K <= 5 ? 3 : (K <= 7 ? 2 : 1); }
 // DR: L >= 4; levels 3..5 keep their sums in registers too (another 3k per
 // lane, an instantiation of its own so that shallower pyramids keep the
 // smaller register budget).
-// RGN: region mode (one block round, one resident region, L = 1; see
-// GradArgs).
+// RGN: region mode (one resident region, L = 1; see GradArgs); with MR its
+// blocks take several rounds (k = 7 and 9: 72 x 72 regions).
 template <int K, typename ST, bool MR, bool DR, bool RGN>
 __global__ void __launch_bounds__(kThreads, grad_waves_per_simd<K>()) grad_kernel(const GradArgs a)
 {
     constexpr int R = K / 2, KK = K * K;
-    static_assert(!RGN || (!MR && !DR), "region mode takes one block round and level 1 only");
+    static_assert(!RGN || !DR, "region mode takes level 1 only");
     extern __shared__ float4 lds4[];
     float* lds = reinterpret_cast<float*>(lds4);
 
@@ -355,6 +355,11 @@ __global__ void __launch_bounds__(kThreads, grad_waves_per_simd<K>()) grad_kerne
             }
         };
         // base correlation of one block (dy centre, x window) and its dy sum
+        // region mode: the blocks of the tile's own pixels (rg_h and rg_T
+        // are multiples of 4, so a block is wholly inside or outside)
+        auto is_inner = [&](const TileIdx& ti) {
+            return !RGN || (ti.j0 >= a.rg_h && ti.j0 < a.rg_h + a.rg_T && ti.i0 >= a.rg_h && ti.i0 < a.rg_h + a.rg_T);
+        };
         auto base_corr = [&](const TileIdx& ti, const float (&dyb)[4][4]) {
             corr_tile<K, 4>(planes + ti.p * stride, g.xpitch, ti.j0, ti.i0, dyb, g0);
 #pragma unroll
@@ -364,10 +369,7 @@ __global__ void __launch_bounds__(kThreads, grad_waves_per_simd<K>()) grad_kerne
         if constexpr (!MR) {
             const bool mine = tl < np * per;  // at most one block per thread (planned on the host)
             const TileIdx ti = tile_at(mine ? tl : 0, per, g.r_tiles, g.tiles_x, g.r_tiles_x, 4);
-            // region mode: the blocks of the tile's own pixels (rg_h and rg_T
-            // are multiples of 4, so a block is wholly inside or outside)
-            const bool inner = !RGN || (ti.j0 >= a.rg_h && ti.j0 < a.rg_h + a.rg_T && ti.i0 >= a.rg_h &&
-                                        ti.i0 < a.rg_h + a.rg_T);
+            const bool inner = is_inner(ti);
 
             // 1. x block -> LDS with its levels 1-2; dy block in registers
             if (alias1 && b0 != b_begin)
@@ -409,18 +411,22 @@ __global__ void __launch_bounds__(kThreads, grad_waves_per_simd<K>()) grad_kerne
             // be stored over it.
             if (alias1 && b0 != b_begin) zero_x_ring(planes, g, R, a.r_ring, tl);
             const long plane = (long)b0 * C + c;
+            const long co = plane * a.cH * a.cW;  // region mode: the plane's level-1 carriers
             for (int it = tl; it < per; it += kThreads) {
                 const TileIdx ti = tile_at(it, per, g.r_tiles, g.tiles_x, g.r_tiles_x, 4);
                 float v[4][4];
-                fetch_block<ST>(xs + plane * HW, g.H, g.W, ti.j0, ti.i0, vw, v);
+                fetch_block<ST>(xs + plane * HW, PH, PW, oy + ti.j0, ox + ti.i0, vw, v);
                 store_block<K>(v, planes, g, ti.j0, ti.i0);
+                if (RGN && a.cx && is_inner(ti))
+                    write_carrier<ST>(reinterpret_cast<ST*>(a.cx) + co, a.cH, a.cW, a.cm, oy + ti.j0, ox + ti.i0, v);
             }
             __syncthreads();
             if (!skip_base) {
                 for (int it = tl; it < per; it += kThreads) {
                     const TileIdx ti = tile_at(it, per, g.r_tiles, g.tiles_x, g.r_tiles_x, 4);
+                    if (!is_inner(ti)) continue;
                     float dyb[4][4];
-                    fetch_block<ST>(dys + plane * HW, g.H, g.W, ti.j0, ti.i0, vw, dyb);
+                    fetch_block<ST>(dys + plane * HW, PH, PW, oy + ti.j0, ox + ti.i0, vw, dyb);
                     base_corr(ti, dyb);
                 }
             }
@@ -434,7 +440,10 @@ __global__ void __launch_bounds__(kThreads, grad_waves_per_simd<K>()) grad_kerne
             for (int it = tl; it < per; it += kThreads) {
                 const TileIdx ti = tile_at(it, per, g.r_tiles, g.tiles_x, g.r_tiles_x, 4);
                 float dyb[4][4];
-                fetch_block<ST>(dys + plane * HW, g.H, g.W, ti.j0, ti.i0, vw, dyb);
+                fetch_block<ST>(dys + plane * HW, PH, PW, oy + ti.j0, ox + ti.i0, vw, dyb);
+                if (RGN && a.cx && is_inner(ti))
+                    write_carrier<ST>(reinterpret_cast<ST*>(a.cdy) + co, a.cH, a.cW, a.cm, oy + ti.j0, ox + ti.i0,
+                                      dyb);
                 dy_levels(ti, dyb);
             }
         }
@@ -547,9 +556,10 @@ template <int K, typename ST>
 hipError_t launch_grad_t(const GradArgs& a, int grid, hipStream_t s)
 {
     if (a.rg_ntx > 0) {
-        // one block round, one resident region, level 1 only (planned on the host)
-        if (a.rounds != 1 || a.PP != 1 || a.g.L != 1) return hipErrorInvalidValue;
-        return launch_grad_v<K, ST, false, false, true>(a, grid, s);
+        // one resident region, level 1 only (planned on the host)
+        if (a.PP != 1 || a.g.L != 1) return hipErrorInvalidValue;
+        return a.rounds > 1 ? launch_grad_v<K, ST, true, false, true>(a, grid, s)
+                            : launch_grad_v<K, ST, false, false, true>(a, grid, s);
     }
     if (a.rounds > 1) {
         if (a.PP != 1) return hipErrorInvalidValue;  // block rounds need one resident plane

@@ -609,8 +609,8 @@ def test_large_plane_determinism_bitwise():
 # at 7), one shape per execution path: tiny planes, 8 x 8 planes whose tiny
 # backward LDS would not fit (resident with mixed rounds instead), mixed
 # forward rounds, forward regions on small planes, the split backward, the
-# gradient pass with one block per thread and with block rounds, the fused
-# region backward, L = 0 and a deep split. At k = 9 a kernel row has 81 taps,
+# gradient pass with one block per thread and with block rounds, the region
+# gradient route (72 x 72 regions: block rounds), L = 0 and a deep split. At k = 9 a kernel row has 81 taps,
 # more than a wavefront's lanes: the finalize wraps them round the lanes and
 # the tiny backward flushes its gradient queue within one kernel.
 K9 = [
@@ -624,6 +624,7 @@ K9 = [
     (2, 2, 56, 56, 9, 3, "f32"),
     (2, 2, 63, 95, 9, 4, "f32"),
     (1, 2, 130, 126, 9, 3, "f32"),
+    (1, 2, 150, 140, 9, 1, "bf16"),
     (2, 3, 14, 14, 9, 0, "f32"),
     (2, 3, 28, 28, 9, 1, "bf16"),
     (66, 2, 14, 14, 9, 5, "f32"),
@@ -644,6 +645,28 @@ def test_k9_backward(B, C, H, W, k, L, dtype):
                                                 (1, 2, 130, 126, 9, 3, "f32")])
 def test_k9_bias(B, C, H, W, k, L, dtype):
     test_bias_forward_backward(B, C, H, W, k, L, dtype)
+
+
+# Large planes at k = 7: the region gradient route walks the 72 x 72 regions'
+# blocks in rounds (ragged tiles, a coarse sub-problem or none, 16-bit
+# storage); at L = 0 the fused region backward runs.
+K7_REGION = [
+    (1, 2, 130, 126, 7, 3, "f32"),
+    (2, 3, 150, 140, 7, 2, "bf16"),
+    (1, 3, 129, 131, 7, 1, "f16"),
+    (1, 2, 130, 126, 7, 4, "f32"),
+    (1, 2, 130, 126, 5, 0, "f32"),
+    (1, 2, 130, 126, 7, 0, "bf16"),
+]
+
+
+@pytest.mark.parametrize("B,C,H,W,k,L,dtype", K7_REGION)
+def test_k7_region_backward(B, C, H, W, k, L, dtype):
+    check_backward(B, C, H, W, k, L, dtype)
+
+
+def test_k7_region_full_size():
+    check_full_size(16, 64, 224, 224, 7, 3, "f32", backward=True)
 
 
 def test_k9_determinism_bitwise():

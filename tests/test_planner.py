@@ -148,16 +148,17 @@ def test_odd_shape_block_rounds(planner):
 
 def test_large_planes_take_the_region_path(planner):
     """Planes larger than one CU's LDS run in region tiles; their backward is
-    the gradient pass over the tiles plus the rotated forward for dx when a
-    region is one block round (k = 3, 5: 64 x 64 regions), else the fused
-    region backward (k = 7, 9: 72 x 72)."""
+    the gradient pass over the tiles plus the rotated forward for dx (64 x 64
+    regions at k = 3, 5; 72 x 72 at k = 7, 9, whose blocks take two rounds),
+    and the fused region backward when there is no level (L = 0)."""
     p = planner(16, 64, 224, 224, 5, 3)
     assert p["fwd_mode"] == "region" and p["fwd_ws"] > 0 and p["bwd_ws"] > 0
     assert p["bwd_mode"] == "region" and p["bwd_region_grad"] == 1
     assert planner(8, 32, 512, 512, 3, 3)["bwd_region_grad"] == 1
     assert planner(8, 128, 128, 128, 5, 1)["bwd_region_grad"] == 1
-    assert planner(1, 1, 300, 300, 7, 4)["bwd_region_grad"] == 0
-    assert planner(1, 2, 130, 126, 9, 3)["bwd_region_grad"] == 0
+    assert planner(1, 1, 300, 300, 7, 4)["bwd_region_grad"] == 1
+    assert planner(1, 2, 130, 126, 9, 3)["bwd_region_grad"] == 1
+    assert planner(1, 2, 130, 126, 5, 0)["bwd_region_grad"] == 0  # no level: the fused region backward
 
 
 def test_lds_granule_model():
