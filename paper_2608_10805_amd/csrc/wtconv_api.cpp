@@ -48,6 +48,13 @@ constexpr int kRegionBackwardTargetWorkgroups = 768;
 // k = 9 L3 2444.8 -> 2355.2, k = 9 L1 2047.0 -> 1954.4; k = 7 128 x 128 B8
 // C128 751.8 -> 765.3.
 constexpr int kRegionGradTargetWorkgroups = 1536;
+// A region that would take two block rounds (k = 7, 9: 56 x 56 tiles in
+// 72 x 72 regions) is re-tiled at 48 x 48, whose 64 x 64 regions are one
+// round at the larger target: combined backward, us, 224 x 224 B16 C64 L3
+// k = 7 1350.4 -> 1257.2, k = 9 2350.5 -> 2106.3; 128 x 128 B8 C128 k = 7
+// 763.0 -> 548.9; 512 x 512 B8 C32 k = 7 2299.0 -> 1848.0, k = 9 4235.0 ->
+// 3368.5. The multi-round region branch stays as the fallback.
+constexpr bool kRegionGradSmallTiles = true;
 
 int ceil_to(int v, int m) { return (v + m - 1) / m * m; }
 int cdiv(long a, long b) { return (int)((a + b - 1) / b); }
@@ -610,7 +617,7 @@ struct RegionPlan {
     int T = 0, h = 0, ntx = 0, nty = 0;
 };
 
-bool make_region_plan(const wtconv_desc& d, bool bwd, RegionPlan& rp, int target = 0)
+bool make_region_plan(const wtconv_desc& d, bool bwd, RegionPlan& rp, int target = 0, int t_max = 56)
 {
     // the carrier kernel decomposes small offsets with fp32 reciprocals
     if (d.H >= (1 << 19) || d.W >= (1 << 19)) return false;
@@ -618,6 +625,7 @@ bool make_region_plan(const wtconv_desc& d, bool bwd, RegionPlan& rp, int target
     const int m = d.L > 0 ? 1 : 0;
     rp.h = ceil_to(m ? 2 * R : R, 4);
     for (int T : {56, 48, 40, 32, 24, 16, 8}) {
+        if (T > t_max) continue;
         wtconv_desc rd = d;
         rd.B = 1;  // one region resident at a time
         rd.H = rd.W = T + 2 * rp.h;
@@ -781,7 +789,13 @@ Exec choose_uncached(const wtconv_desc& d, bool bwd)
         ex.m = d.L > 0 ? 1 : 0;
         ex.coarse = d.L >= 2;
         // the tile edge does not depend on the target, only the batch chunks
-        if (bwd && region_grad_one_round(d, ex)) make_region_plan(d, bwd, ex.rp, kRegionGradTargetWorkgroups);
+        if (bwd && region_grad_one_round(d, ex)) {
+            make_region_plan(d, bwd, ex.rp, kRegionGradTargetWorkgroups);
+        } else if (bwd && kRegionGradSmallTiles) {
+            Exec alt = ex;
+            if (make_region_plan(d, bwd, alt.rp, kRegionGradTargetWorkgroups, 48) && region_grad_one_round(d, alt))
+                ex = alt;
+        }
     }
     return ex;
 }

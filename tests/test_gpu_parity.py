@@ -610,7 +610,7 @@ def test_large_plane_determinism_bitwise():
 # backward LDS would not fit (resident with mixed rounds instead), mixed
 # forward rounds, forward regions on small planes, the split backward, the
 # gradient pass with one block per thread and with block rounds, the region
-# gradient route (72 x 72 regions: block rounds), L = 0 and a deep split. At k = 9 a kernel row has 81 taps,
+# gradient route, L = 0 and a deep split. At k = 9 a kernel row has 81 taps,
 # more than a wavefront's lanes: the finalize wraps them round the lanes and
 # the tiny backward flushes its gradient queue within one kernel.
 K9 = [
@@ -647,9 +647,9 @@ def test_k9_bias(B, C, H, W, k, L, dtype):
     test_bias_forward_backward(B, C, H, W, k, L, dtype)
 
 
-# Large planes at k = 7: the region gradient route walks the 72 x 72 regions'
-# blocks in rounds (ragged tiles, a coarse sub-problem or none, 16-bit
-# storage); at L = 0 the fused region backward runs.
+# Large planes at k = 7: the region gradient route over 48 x 48 tiles
+# (ragged tiles, a coarse sub-problem or none, 16-bit storage); at L = 0 the
+# fused region backward runs.
 K7_REGION = [
     (1, 2, 130, 126, 7, 3, "f32"),
     (2, 3, 150, 140, 7, 2, "bf16"),

@@ -149,8 +149,8 @@ def test_odd_shape_block_rounds(planner):
 def test_large_planes_take_the_region_path(planner):
     """Planes larger than one CU's LDS run in region tiles; their backward is
     the gradient pass over the tiles plus the rotated forward for dx (64 x 64
-    regions at k = 3, 5; 72 x 72 at k = 7, 9, whose blocks take two rounds),
-    and the fused region backward when there is no level (L = 0)."""
+    regions: 56 x 56 tiles at k = 3, 5, 48 x 48 at k = 7, 9), and the fused
+    region backward when there is no level (L = 0)."""
     p = planner(16, 64, 224, 224, 5, 3)
     assert p["fwd_mode"] == "region" and p["fwd_ws"] > 0 and p["bwd_ws"] > 0
     assert p["bwd_mode"] == "region" and p["bwd_region_grad"] == 1
